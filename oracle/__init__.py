@@ -1,0 +1,177 @@
+"""CPU oracle for the interface-adjoint scan -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The HIP library never calls it and
+shares no code with it.
+
+What it computes (paper: "LBI: Parallel Scan Backpropagation via Latent
+Bounded Interfaces"):
+
+* ``recurrence`` -- Theorem "Bounded-Interface Backpropagation":
+  mbar_k = J_k^T mbar_{k+1} for k = K-1..0, extended with the affine term b_k
+  (the direct gradient of loss terms that read m_k):
+  ``lambda_j = A_j lambda_{j+1} + b_j`` with ``A_j = J_j^T``.  This is the plain
+  definition of what the scan returns; fp64, inputs widened exactly.
+* ``suffix_composites`` -- Proposition "Scan Formulation of Backpropagation":
+  the suffix products ``P_j = A_j ... A_{K-1}`` (empty product I) and offsets
+  ``c_j``, obtained by folding the combine (A, b) o (A', b') = (AA', Ab' + b)
+  from the right end of the chain.  fp64.
+
+Every function here is pinned by the CPU tests against closed forms, exact
+rational brute force, invariants and torch autograd (see tests/test_oracle_*).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "lbi_oracle.c")
+_LIBDIR = os.path.join(_HERE, "_lib")
+_LIB = os.path.join(_LIBDIR, "liblbi_oracle.so")
+
+_F64, _F32, _BF16 = 0, 1, 2
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the C oracle with gcc (-O2 -ffp-contract=off -fopenmp)."""
+    if not force and os.path.exists(_LIB):
+        return _LIB
+    os.makedirs(_LIBDIR, exist_ok=True)
+    tmp = _LIB + f".tmp{os.getpid()}"
+    cmd = ["gcc", "-O2", "-ffp-contract=off", "-fopenmp", "-fPIC", "-shared",
+           "-Wall", "-Wextra", "-o", tmp, _SRC]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build(force=True)
+        lib = ctypes.CDLL(_LIB)
+        vp, i64, i32, ci = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int
+        lib.lbi_oracle_recurrence.argtypes = [vp, vp, vp, vp, i64, i64, i32, ci, ci]
+        lib.lbi_oracle_recurrence.restype = ci
+        lib.lbi_oracle_suffix_composites.argtypes = [vp, vp, vp, vp, i64, i64, i32, ci]
+        lib.lbi_oracle_suffix_composites.restype = ci
+        lib.lbi_oracle_threads.argtypes = [ci]
+        lib.lbi_oracle_threads.restype = ci
+        _lib = lib
+    return _lib
+
+
+def _host_array(x) -> Tuple[object, int]:
+    """A C-contiguous host buffer for x (torch tensor or numpy) + its dtype code.
+
+    The returned object keeps the buffer alive; bf16 is passed as raw bits.
+    """
+    try:
+        import torch
+    except ImportError:  # pragma: no cover - torch is always present here
+        torch = None
+    if torch is not None and isinstance(x, torch.Tensor):
+        t = x.detach().to("cpu").contiguous()
+        if t.dtype == torch.float64:
+            return t, _F64
+        if t.dtype == torch.float32:
+            return t, _F32
+        if t.dtype == torch.bfloat16:
+            return t, _BF16
+        raise TypeError(f"unsupported oracle input dtype {t.dtype}")
+    a = np.ascontiguousarray(x)
+    if a.dtype == np.float64:
+        return a, _F64
+    if a.dtype == np.float32:
+        return a, _F32
+    raise TypeError(f"unsupported oracle input dtype {a.dtype}")
+
+
+def _ptr(obj) -> int:
+    if isinstance(obj, np.ndarray):
+        return obj.ctypes.data
+    return obj.data_ptr()
+
+
+def threads(nthreads: int = 0) -> int:
+    """Threads the recurrence runs on for ``nthreads`` (<= 0: OpenMP default)."""
+    return int(_load().lbi_oracle_threads(int(nthreads)))
+
+
+def recurrence(A, b, lamK, nthreads: int = 0) -> np.ndarray:
+    """lambda[B, K, r] (float64) from A[B, K, r, r], b[B, K, r] or None, lamK[B, r]."""
+    lib = _load()
+    a_buf, dt = _host_array(A)
+    l_buf, dt_l = _host_array(lamK)
+    if dt_l != dt:
+        raise TypeError("A and lamK must share a dtype")
+    shape = tuple(a_buf.shape)
+    if len(shape) != 4 or shape[2] != shape[3]:
+        raise ValueError(f"A must be [B, K, r, r], got {shape}")
+    B, K, r, _ = shape
+    if tuple(l_buf.shape) != (B, r):
+        raise ValueError("lamK must be [B, r]")
+    b_ptr = None
+    b_buf = None
+    if b is not None:
+        b_buf, dt_b = _host_array(b)
+        if dt_b != dt or tuple(b_buf.shape) != (B, K, r):
+            raise ValueError("b must be [B, K, r] in A's dtype")
+        b_ptr = _ptr(b_buf)
+    out = np.empty((B, K, r), dtype=np.float64)
+    if B == 0:
+        return out
+    rc = lib.lbi_oracle_recurrence(_ptr(a_buf), b_ptr, _ptr(l_buf), out.ctypes.data,
+                                   B, K, r, dt, int(nthreads))
+    if rc != 0:
+        raise ValueError("oracle rejected its arguments")
+    return out
+
+
+def suffix_composites(A, b) -> Tuple[np.ndarray, np.ndarray]:
+    """(P[B, K, r, r], c[B, K, r]) in float64: the inclusive suffix scan."""
+    lib = _load()
+    a_buf, dt = _host_array(A)
+    B, K, r, _ = a_buf.shape
+    b_ptr = None
+    b_buf = None
+    if b is not None:
+        b_buf, dt_b = _host_array(b)
+        if dt_b != dt or tuple(b_buf.shape) != (B, K, r):
+            raise ValueError("b must be [B, K, r] in A's dtype")
+        b_ptr = _ptr(b_buf)
+    P = np.empty((B, K, r, r), dtype=np.float64)
+    c = np.empty((B, K, r), dtype=np.float64)
+    if B == 0:
+        return P, c
+    rc = lib.lbi_oracle_suffix_composites(_ptr(a_buf), b_ptr, P.ctypes.data, c.ctypes.data,
+                                          B, K, r, dt)
+    if rc != 0:
+        raise ValueError("oracle rejected its arguments")
+    return P, c
+
+
+def rel_frobenius(x: np.ndarray, ref: np.ndarray) -> float:
+    """||x - ref||_F / ||ref||_F (the absolute error when ||ref||_F = 0)."""
+    x = np.asarray(x, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    num = float(np.linalg.norm((x - ref).ravel()))
+    den = float(np.linalg.norm(ref.ravel()))
+    return num / den if den > 0 else num
+
+
+def per_chain_rel_frobenius(x: np.ndarray, ref: np.ndarray) -> np.ndarray:
+    """Relative Frobenius error of each chain (leading axis)."""
+    x = np.asarray(x, dtype=np.float64).reshape(x.shape[0], -1)
+    ref = np.asarray(ref, dtype=np.float64).reshape(ref.shape[0], -1)
+    num = np.linalg.norm(x - ref, axis=1)
+    den = np.linalg.norm(ref, axis=1)
+    return np.where(den > 0, num / np.where(den > 0, den, 1.0), num)
