@@ -1,0 +1,289 @@
+#!/usr/bin/env python3
+"""Throughput of the interface-adjoint scan on one MI355X.
+
+One step = one ``lbi_scan_backward`` call over the whole batch of a synthetic
+workload (every slot of every chain composed and applied).  Prints one JSON
+line.  Default workload: ``long_chain`` (B=512 chains, K=512 regions, r=64,
+fp32), the largest batched r=64 workload.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                  [--no-cpu-baseline] [--copy-calibration MiB]
+
+Accounting (flop = 2 per multiply-add; the paper counts r^3 per r x r
+product, i.e. one per multiply-add, in its scan-negligibility estimate):
+  combine of slot j into the suffix composite S_{j+1} = (P_{j+1}, c_{j+1}):
+      2 r_j r_{j+1} r_K + 2 r_j r_{j+1} + r_j flop,
+  apply lambda_j = P_j lambda_K + c_j: 2 r_j r_K + r_j flop,
+  algorithmic flops = B [sum_{j<K-1} combine_j + sum_j apply_j],
+  algorithmic bytes = A (true-width tiles), b, lambda_K read once, lambda
+  written once (fp32, padded rows included).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(ROOT, "paper_2605_09204_amd", "csrc", "lbi_scan.hip")
+TRAFFIC_DIR = os.path.join(ROOT, "profiles")
+
+METRIC = "interface combines/sec and achieved MFMA TFLOP/s (r=64, bf16/fp32), % of peak"
+PEAK = {  # MI355X published peaks
+    "hbm_gbs": 8000.0,
+    "mfma_f32_tflops": 157.3,
+    "mfma_bf16_tflops": 2516.6,
+}
+ELEM = {"f32": 4, "bf16": 2}
+
+
+# ----------------------------------------------------------------------------
+# accounting
+# ----------------------------------------------------------------------------
+
+def widths_of(wl):
+    return wl.interface_widths()
+
+
+def combines(wl) -> int:
+    """Algorithmic combines: K-1 per chain (a right-to-left inclusive scan)."""
+    return wl.B * (wl.K - 1)
+
+
+def flops_alg(wl) -> int:
+    w = widths_of(wl)
+    rK = w[wl.K]
+    per_chain = 0
+    for j in range(wl.K):
+        rj, rj1 = w[j], w[j + 1]
+        if j < wl.K - 1:
+            per_chain += 2 * rj * rj1 * rK + 2 * rj * rj1 + rj
+        per_chain += 2 * rj * rK + rj
+    return wl.B * per_chain
+
+
+def flops_seq(wl) -> int:
+    """The sequential chain of K matvecs: lambda_j = A_j lambda_{j+1} + b_j."""
+    w = widths_of(wl)
+    return wl.B * sum(2 * w[j] * w[j + 1] + w[j] for j in range(wl.K))
+
+
+def bytes_alg(wl, padded: bool = False) -> int:
+    w = widths_of(wl)
+    e = ELEM[wl.dtype]
+    R = wl.r
+    if padded:
+        a = wl.K * R * R
+    else:
+        a = sum(w[j] * w[j + 1] for j in range(wl.K))
+    bb = (wl.K * R if padded else sum(w[:wl.K])) if wl.affine else 0
+    lk = R if padded else w[wl.K]
+    out = wl.K * R * 4
+    return wl.B * ((a + bb + lk) * e + out)
+
+
+def scan_payload_bytes(K: int, r: int, elem: int) -> int:
+    """K interface matrices of r x r (the paper's cross-device scan payload)."""
+    return K * r * r * elem
+
+
+def source_hash() -> str:
+    with open(SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def load_traffic(workload: str):
+    """Measured HBM bytes per launch from the rocprofv3 PMC runs, if they were
+    taken on the current kernel source; else None."""
+    path = os.path.join(TRAFFIC_DIR, f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_sha256_16") != source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+# ----------------------------------------------------------------------------
+# CPU baseline: the oracle on a bounded sample of the same workload
+# ----------------------------------------------------------------------------
+
+def cpu_baseline(x, target_s: float = 10.0):
+    import oracle
+    import torch
+
+    wl = x.workload
+    threads = oracle.threads(0)
+    n_cal = min(wl.B, max(1, threads))
+    host = x.chains(torch.arange(n_cal)).to("cpu")
+    t0 = time.perf_counter()
+    oracle.recurrence(host.A, host.b, host.lamK)
+    t_cal = max(time.perf_counter() - t0, 1e-6)
+    n = int(min(wl.B, max(n_cal, n_cal * target_s / t_cal)))
+    host = x.chains(torch.arange(n)).to("cpu")
+    t0 = time.perf_counter()
+    oracle.recurrence(host.A, host.b, host.lamK)
+    t = time.perf_counter() - t0
+    reps = 1
+    while t < 0.5 * target_s and reps < 64:  # whole batch is quick: repeat it
+        t0 = time.perf_counter()
+        oracle.recurrence(host.A, host.b, host.lamK)
+        t += time.perf_counter() - t0
+        reps += 1
+    return {
+        "value": reps * n * (wl.K - 1) / t,
+        "unit": "combines/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"{n} of {wl.B} chains x {reps} pass(es), all K={wl.K} slots, "
+                  f"fp64 recurrence over the same {wl.dtype} inputs ({t:.1f} s)",
+    }
+
+
+# ----------------------------------------------------------------------------
+# main
+# ----------------------------------------------------------------------------
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="long_chain")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="also run a plain device copy of this many MiB (for PMC scaling)")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(chains are independent, so B shards across GPUs with no communication)",
+              file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2605_09204_amd import binding, synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    binding.load()  # fail loudly before any work if the library is missing
+    if args.workload not in synth.WORKLOADS:
+        print(f"unknown workload {args.workload}; one of {list(synth.WORKLOADS)}",
+              file=sys.stderr)
+        return 2
+    wl = synth.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    print(f"[bench] generating {wl.name}: B={wl.B} K={wl.K} r={wl.r} {wl.dtype}",
+          file=sys.stderr, flush=True)
+    t0 = time.time()
+    x = synth.generate(wl, device=dev)
+    torch.cuda.synchronize()
+    print(f"[bench] inputs ready in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+
+    # rotate through enough input copies that no step reuses the last-level cache
+    in_bytes = bytes_alg(wl, padded=True)
+    ncopy = max(1, min(8, -(-(1 << 30) // in_bytes)))
+    copies = [x] + [synth.Inputs(x.A.clone(), None if x.b is None else x.b.clone(),
+                                 x.lamK.clone(), x.widths, wl) for _ in range(ncopy - 1)]
+    lam = torch.empty((wl.B, wl.K, wl.r), dtype=torch.float32, device=dev)
+    hint = wl.widths
+
+    def step(i):
+        c = copies[i % ncopy]
+        if hint is None:
+            binding.lbi_scan_backward(c.A, c.b, c.lamK, lam=lam)
+        else:
+            binding.lbi_scan_backward_widths(c.A, c.b, c.lamK, hint, lam=lam)
+
+    if args.copy_calibration > 0:
+        n = args.copy_calibration << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream(dev)
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    for i in range(args.steps):
+        starts[i].record(stream)
+        step(i)
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    per_launch_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    total_ms = starts[0].elapsed_time(ends[-1])
+    avg_launch_s = sum(per_launch_ms) / len(per_launch_ms) / 1e3
+    ms_per_step = total_ms / args.steps
+
+    value = combines(wl) * args.steps / (total_ms / 1e3)
+    f_alg = flops_alg(wl)
+    b_alg = bytes_alg(wl)
+    tflops = f_alg / avg_launch_s / 1e12
+    gbs = b_alg / avg_launch_s / 1e9
+    if wl.dtype == "f32":
+        roof = {"bound": "mfma", "achieved": tflops, "peak": PEAK["mfma_f32_tflops"],
+                "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": gbs, "peak": PEAK["hbm_gbs"], "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = load_traffic(wl.name)
+
+    mfma_peak = PEAK["mfma_f32_tflops"] if wl.dtype == "f32" else PEAK["mfma_bf16_tflops"]
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "combines/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic (seeded Haar-orthogonal x diag x Haar-orthogonal interface "
+                "Jacobians; no dataset or checkpoint)",
+        "config": {"workload": wl.name, "B": wl.B, "K": wl.K, "r": wl.r,
+                   "storage": wl.dtype, "affine": wl.affine,
+                   "widths": "cyclic 32/64/128" if wl.widths else "uniform",
+                   "parallelism": "single GPU, one workgroup per chain"},
+        "roofline": roof,
+        "extra": {
+            "alg_tflops": tflops,
+            "pct_of_mfma_peak": 100.0 * tflops / mfma_peak,
+            "alg_hbm_gbs": gbs,
+            "pct_of_hbm_peak": 100.0 * gbs / PEAK["hbm_gbs"],
+            "avg_launch_ms": avg_launch_s * 1e3,
+            "min_launch_ms": min(per_launch_ms),
+            "work_inflation_vs_sequential": f_alg / flops_seq(wl),
+            "alg_flops_per_launch": f_alg,
+            "alg_bytes_per_launch": b_alg,
+            "input_copies_rotated": ncopy,
+            "wall_s_timed_region": t_wall,
+        },
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle baseline", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(x)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

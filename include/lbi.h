@@ -1,0 +1,132 @@
+/*
+ * lbi.h -- C-ABI of the MI355X (gfx950) interface-adjoint scan of LBI
+ * ("LBI: Parallel Scan Backpropagation via Latent Bounded Interfaces").
+ *
+ * The operation.  A bounded-interface model joins K regions by interface
+ * states m_0 .. m_K; J_k = d m_{k+1} / d m_k is the interface Jacobian
+ * (Section "Implementation Details": an r_{k+1} x r_k matrix).  Theorem
+ * "Bounded-Interface Backpropagation" gives the interface adjoints as
+ * mbar_k = J_k^T mbar_{k+1} = (J_k^T ... J_{K-1}^T) mbar_K, and Proposition
+ * "Scan Formulation of Backpropagation" computes the products by an
+ * associative suffix scan.  This library adds the affine term b_k (the direct
+ * gradient of any loss term that reads m_k) and returns every adjoint of
+ *
+ *     lambda_j = A_j lambda_{j+1} + b_j,   j = K-1 .. 0,   A_j = J_j^T,
+ *
+ * for B independent chains, by scanning the slots under the combine
+ *
+ *     (A, b) o (A', b') = (A A', A b' + b)
+ *
+ * (left operand = lower slot) into the suffix composites
+ * (P_j, c_j) = (A_j, b_j) o ... o (A_{K-1}, b_{K-1}) and applying them:
+ * lambda_j = P_j lambda_K + c_j.  With b absent this is exactly the paper's
+ * Phase 2 of Algorithm "Bounded-Interface Backpropagation".
+ *
+ * Conventions shared by every entry point:
+ *   - Pointers to tensors are DEVICE pointers on the current HIP device,
+ *     allocated and owned by the caller.  The library never allocates, frees
+ *     or synchronizes, and keeps no pointer after a call returns.
+ *   - Calls are asynchronous: work is enqueued on `stream` (NULL = the null
+ *     stream) and results are valid once the caller synchronizes it.
+ *   - Argument errors are reported synchronously, before anything is
+ *     enqueued, and leave every buffer untouched.  A failed launch returns
+ *     LBI_ERR_HIP.  A device fault surfaces at the caller's next sync.
+ *   - Layout is C-contiguous row-major; every base pointer is 16-byte aligned.
+ *   - bf16 is the upper half of an IEEE binary32 (torch.bfloat16).
+ *   - Non-finite inputs propagate; nothing is checked for them.
+ *   - Thread-safe: no mutable global state.
+ */
+#ifndef LBI_H
+#define LBI_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* HIP stream handle (the same type as hipStream_t). */
+typedef struct ihipStream_t *lbi_stream_t;
+
+#define LBI_ABI_VERSION 1
+
+/* Largest K for which a widths hint is used (longer chains run unhinted,
+ * which gives identical results). */
+#define LBI_MAX_HINT_K 2047
+
+typedef enum {
+    LBI_F32 = 0,  /* A, b, lambda_K stored as float32; float32 arithmetic   */
+    LBI_BF16 = 1  /* stored as bfloat16; bf16 MFMA products, fp32 sums      */
+} lbi_dtype;
+
+typedef enum {
+    LBI_OK = 0,
+    LBI_ERR_NULL = 1,          /* a required pointer is NULL                */
+    LBI_ERR_SHAPE = 2,         /* B < 0, K < 1, size overflow, bad widths   */
+    LBI_ERR_DTYPE = 3,         /* dtype not an lbi_dtype                    */
+    LBI_ERR_UNSUPPORTED_R = 4, /* r not in {16, 32, 64, 128}                */
+    LBI_ERR_WORKSPACE = 5,     /* workspace missing or too small            */
+    LBI_ERR_HIP = 6,           /* the HIP runtime refused the launch        */
+    LBI_ERR_ALIGN = 7,         /* a pointer is not 16-byte aligned          */
+    LBI_ERR_ALIAS = 8          /* lambda overlaps an input                  */
+} lbi_status;
+
+/*
+ * Bytes of device workspace that lbi_scan_backward needs for (B, K, r, dt).
+ * 0 means the call needs none (workspace may then be NULL).  Returns 0 for
+ * arguments the scan would reject.
+ */
+size_t lbi_scan_backward_workspace_bytes(int64_t B, int64_t K, int32_t r, lbi_dtype dt);
+
+/*
+ * Every interface adjoint of B independent chains.
+ *
+ *   A         [B][K][r][r]  A[beta][j] = J_j^T, r_j rows x r_{j+1} columns,
+ *                           zero-padded to r x r; row-major.
+ *   b         [B][K][r]     affine terms, or NULL for b = 0.
+ *   lambda_K  [B][r]        terminal adjoints mbar_K.
+ *   lambda    [B][K][r]     OUTPUT, float32 for both dtypes; slot j holds
+ *                           lambda_j for j = 0..K-1 (lambda_K is the input).
+ *                           Must not overlap A, b or lambda_K.
+ *   B >= 0 (B = 0 is a no-op that returns LBI_OK), K >= 1,
+ *   r in {16, 32, 64, 128}, dt an lbi_dtype.
+ *   workspace / workspace_bytes: device scratch of at least
+ *                           lbi_scan_backward_workspace_bytes(B, K, r, dt).
+ *   stream: the HIP stream to enqueue on.
+ *
+ * Precision: LBI_F32 composes and applies in float32 throughout.  LBI_BF16
+ * multiplies bf16 operands on the matrix cores with float32 accumulation; the
+ * running float32 composite is fed back as a two-term bf16 split (hi + lo),
+ * so only the inputs are bf16-rounded.  Results are bitwise reproducible run
+ * to run for a given (B, K, r, dt).
+ */
+lbi_status lbi_scan_backward(const void *A, const void *b, const void *lambda_K,
+                             float *lambda, int64_t B, int64_t K, int32_t r, lbi_dtype dt,
+                             void *workspace, size_t workspace_bytes, lbi_stream_t stream);
+
+/*
+ * As lbi_scan_backward, for chains whose interfaces have widths
+ * r_0 .. r_K <= r (the paper's "variable-width case", Section "Scan Parallel
+ * Backpropagation").  widths_host is a HOST array of K+1 entries in [1, r],
+ * or NULL (then this is lbi_scan_backward).  The caller zero-pads A, b and
+ * lambda_K to r; the hint only lets the kernels skip all-zero tiles, so the
+ * results equal the unhinted call's.  For K > LBI_MAX_HINT_K the hint is
+ * ignored.  Padded output lanes (rows >= r_j of lambda_j) are exactly 0.
+ */
+lbi_status lbi_scan_backward_widths(const void *A, const void *b, const void *lambda_K,
+                                    float *lambda, int64_t B, int64_t K, int32_t r,
+                                    lbi_dtype dt, void *workspace, size_t workspace_bytes,
+                                    lbi_stream_t stream, const int32_t *widths_host);
+
+/* A static, human-readable name for a status code. */
+const char *lbi_status_string(lbi_status s);
+
+/* LBI_ABI_VERSION of the built library. */
+int lbi_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LBI_H */

@@ -1,0 +1,142 @@
+"""Python binding of the C-ABI in ``include/lbi.h`` (argument marshalling only).
+
+Every function has the name of the C entry point it calls.  Tensors are torch
+tensors on the current GPU; torch provides device memory and the stream (the
+current torch stream unless one is given).  All arithmetic runs in the HIP
+library; if the library is not built, the first call raises ``RuntimeError``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "_lib", "liblbi.so")
+
+LBI_F32 = 0
+LBI_BF16 = 1
+LBI_OK = 0
+LBI_MAX_HINT_K = 2047
+
+_DTYPES = {torch.float32: LBI_F32, torch.bfloat16: LBI_BF16}
+
+_lib = None
+
+
+class LbiError(RuntimeError):
+    """A non-OK lbi_status from the library."""
+
+    def __init__(self, status: int, message: str):
+        super().__init__(message)
+        self.status = status
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load() -> ctypes.CDLL:
+    """Load the HIP library (raises RuntimeError when it is not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError(
+            f"HIP library not built: {_LIB_PATH} is missing "
+            "(run `python -m paper_2605_09204_amd.build`)")
+    lib = ctypes.CDLL(_LIB_PATH)
+    vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    lib.lbi_scan_backward_workspace_bytes.argtypes = [i64, i64, i32, ctypes.c_int]
+    lib.lbi_scan_backward_workspace_bytes.restype = sz
+    lib.lbi_scan_backward.argtypes = [vp, vp, vp, vp, i64, i64, i32, ctypes.c_int, vp, sz, vp]
+    lib.lbi_scan_backward.restype = ctypes.c_int
+    lib.lbi_scan_backward_widths.argtypes = [vp, vp, vp, vp, i64, i64, i32, ctypes.c_int, vp,
+                                             sz, vp, ctypes.POINTER(ctypes.c_int32)]
+    lib.lbi_scan_backward_widths.restype = ctypes.c_int
+    lib.lbi_status_string.argtypes = [ctypes.c_int]
+    lib.lbi_status_string.restype = ctypes.c_char_p
+    lib.lbi_abi_version.argtypes = []
+    lib.lbi_abi_version.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def lbi_status_string(status: int) -> str:
+    return load().lbi_status_string(int(status)).decode()
+
+
+def lbi_abi_version() -> int:
+    return int(load().lbi_abi_version())
+
+
+def lbi_scan_backward_workspace_bytes(B: int, K: int, r: int, dt: int) -> int:
+    return int(load().lbi_scan_backward_workspace_bytes(int(B), int(K), int(r), int(dt)))
+
+
+def _check(status: int) -> None:
+    if status != LBI_OK:
+        raise LbiError(status, lbi_status_string(status))
+
+
+def _marshal(A: torch.Tensor, b: Optional[torch.Tensor], lambda_K: torch.Tensor,
+             lam: Optional[torch.Tensor], workspace: Optional[torch.Tensor], stream):
+    if A.dim() != 4 or A.shape[2] != A.shape[3]:
+        raise ValueError(f"A must be [B, K, r, r], got {tuple(A.shape)}")
+    B, K, r = int(A.shape[0]), int(A.shape[1]), int(A.shape[2])
+    if A.dtype not in _DTYPES:
+        raise TypeError(f"A must be float32 or bfloat16, got {A.dtype}")
+    dt = _DTYPES[A.dtype]
+    for name, t, shape in (("b", b, (B, K, r)), ("lambda_K", lambda_K, (B, r))):
+        if t is None:
+            continue
+        if tuple(t.shape) != shape or t.dtype != A.dtype or t.device != A.device:
+            raise ValueError(f"{name} must be {shape} {A.dtype} on {A.device}")
+    tensors = [A, lambda_K] + ([b] if b is not None else [])
+    if not A.is_cuda:
+        raise ValueError("tensors must be on a GPU device")
+    if not all(t.is_contiguous() for t in tensors):
+        raise ValueError("tensors must be contiguous")
+    if lam is None:
+        lam = torch.empty((B, K, r), dtype=torch.float32, device=A.device)
+    elif tuple(lam.shape) != (B, K, r) or lam.dtype != torch.float32 or not lam.is_contiguous() \
+            or lam.device != A.device:
+        raise ValueError("lambda must be a contiguous float32 [B, K, r] tensor on A's device")
+    need = lbi_scan_backward_workspace_bytes(B, K, r, dt)
+    if workspace is None and need > 0:
+        workspace = torch.empty((need,), dtype=torch.uint8, device=A.device)
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    if stream is None:
+        stream = torch.cuda.current_stream(A.device)
+    s_ptr = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    args = (A.data_ptr(), b.data_ptr() if b is not None else None, lambda_K.data_ptr(),
+            lam.data_ptr(), B, K, r, dt, ws_ptr, ws_bytes, s_ptr)
+    return lam, args
+
+
+def lbi_scan_backward(A: torch.Tensor, b: Optional[torch.Tensor], lambda_K: torch.Tensor,
+                      lam: Optional[torch.Tensor] = None,
+                      workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """lambda[B, K, r] (float32) = every interface adjoint; see include/lbi.h."""
+    lam, args = _marshal(A, b, lambda_K, lam, workspace, stream)
+    _check(load().lbi_scan_backward(*args))
+    return lam
+
+
+def lbi_scan_backward_widths(A: torch.Tensor, b: Optional[torch.Tensor],
+                             lambda_K: torch.Tensor, widths: Optional[Sequence[int]],
+                             lam: Optional[torch.Tensor] = None,
+                             workspace: Optional[torch.Tensor] = None,
+                             stream=None) -> torch.Tensor:
+    """As lbi_scan_backward with the interface widths r_0..r_K as a hint."""
+    lam, args = _marshal(A, b, lambda_K, lam, workspace, stream)
+    wptr = None
+    if widths is not None:
+        if len(widths) != int(A.shape[1]) + 1:
+            raise ValueError("widths must hold K+1 entries")
+        warr = (ctypes.c_int32 * len(widths))(*[int(x) for x in widths])
+        wptr = ctypes.cast(warr, ctypes.POINTER(ctypes.c_int32))
+    _check(load().lbi_scan_backward_widths(*args, wptr))
+    return lam

@@ -14,8 +14,8 @@ Layout (row-major, C-contiguous):
   * ``b[beta, j]`` has r_j meaningful entries, ``lambda_K[beta]`` has r_K.
 
 Recipes (each a workload of the paper's r = 64 setting or its variants):
-  * ``uniform``: A = Q1 diag(s) Q2 with Q1, Q2 Haar-orthogonal (QR of a Gaussian
-    matrix with the sign of diag(R) folded into Q, Mezzadri 2007) and
+  * ``uniform``: A = Q1 diag(s) Q2 with Q1, Q2 Haar-orthogonal (the Q of the
+    QR factorisation of a Gaussian matrix with positive diag(R), Mezzadri 2007) and
     s ~ U[0.9, 1.1].
   * ``concentrated``: the same factors with a spectrum shaped like the trained
     Mamba-3 interface Jacobians of the spectral-structure appendix (leading
@@ -124,12 +124,30 @@ def _chunk_seed(seed: int, chunk: int) -> int:
 
 
 def _haar(n: int, d: int, gen: torch.Generator, device) -> torch.Tensor:
-    """n Haar-distributed d x d orthogonal matrices (float64)."""
+    """n Haar-distributed d x d orthogonal matrices (float64).
+
+    The Q of the QR factorisation G = QR of a Gaussian G with diag(R) > 0,
+    which is unique and Haar-distributed (Mezzadri 2007).  On the CPU it comes
+    from LAPACK's QR with the signs of diag(R) folded into Q; on a GPU from
+    classical Gram-Schmidt with one re-orthogonalisation pass (CGS2), which
+    produces the same positive-diagonal factor as batched matrix products.
+    """
     G = torch.randn((n, d, d), generator=gen, device=device, dtype=torch.float64)
-    Q, R = torch.linalg.qr(G)
-    sgn = torch.sign(torch.diagonal(R, dim1=-2, dim2=-1))
-    sgn = torch.where(sgn == 0, torch.ones_like(sgn), sgn)
-    return Q * sgn.unsqueeze(-2)
+    if G.device.type == "cpu":
+        Q, R = torch.linalg.qr(G)
+        sgn = torch.sign(torch.diagonal(R, dim1=-2, dim2=-1))
+        sgn = torch.where(sgn == 0, torch.ones_like(sgn), sgn)
+        return Q * sgn.unsqueeze(-2)
+    Q = torch.empty_like(G)
+    for k in range(d):
+        v = G[:, :, k:k + 1].clone()
+        if k > 0:
+            Qk = Q[:, :, :k]
+            QkT = Qk.transpose(1, 2).contiguous()
+            for _ in range(2):
+                v = v - torch.bmm(Qk, torch.bmm(QkT, v))
+        Q[:, :, k:k + 1] = v / torch.linalg.vector_norm(v, dim=1, keepdim=True)
+    return Q
 
 
 def _spectrum(n: int, k: int, kind: str, gen: torch.Generator, device) -> torch.Tensor:

@@ -1,0 +1,96 @@
+"""The C-ABI library loads, exports what include/lbi.h declares, and rejects
+bad arguments before touching the GPU (runs without a GPU: no call here
+reaches a HIP API)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2605_09204_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lbi.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(binding.library_path()),
+                                reason="library not built")
+
+# fake device addresses: never dereferenced, only validated
+PA, PB, PL, POUT = 0x10000000, 0x20000000, 0x30000000, 0x40000000
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lbi_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_entry_points():
+    names = declared_functions()
+    assert names == sorted(["lbi_scan_backward_workspace_bytes", "lbi_scan_backward",
+                            "lbi_scan_backward_widths", "lbi_status_string",
+                            "lbi_abi_version"])
+
+
+def test_library_exports_every_declared_symbol():
+    lib = binding.load()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", binding.library_path()],
+                         capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r"\b(lbi_[a-z_]+)\b", out))
+    assert set(declared_functions()) <= exported
+
+
+def test_header_compiles_as_c():
+    src = '#include "lbi.h"\nint main(void){return lbi_abi_version()==LBI_ABI_VERSION?0:1;}\n'
+    res = subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-fsyntax-only",
+                          f"-I{os.path.join(ROOT, 'include')}", "-x", "c", "-"],
+                         input=src, capture_output=True, text=True)
+    assert res.returncode == 0, res.stderr
+
+
+def test_version_and_status_strings():
+    assert binding.lbi_abi_version() == 1
+    assert binding.lbi_status_string(0) == "LBI_OK"
+    for code in range(1, 9):
+        assert binding.lbi_status_string(code).startswith("LBI_ERR_")
+    assert "unknown" in binding.lbi_status_string(99)
+
+
+def call(A=PA, b=PB, L=PL, out=POUT, B=2, K=3, r=64, dt=0, ws=None, wsb=0, widths=None):
+    lib = binding.load()
+    if widths is None:
+        return lib.lbi_scan_backward(A, b, L, out, B, K, r, dt, ws, wsb, None)
+    arr = (ctypes.c_int32 * len(widths))(*widths)
+    return lib.lbi_scan_backward_widths(A, b, L, out, B, K, r, dt, ws, wsb, None,
+                                        ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32)))
+
+
+def test_argument_errors():
+    assert call(dt=7) == 3                      # LBI_ERR_DTYPE
+    for r in (0, 8, 48, 96, 256):
+        assert call(r=r) == 4                   # LBI_ERR_UNSUPPORTED_R
+    assert call(K=0) == 2 and call(B=-1) == 2   # LBI_ERR_SHAPE
+    assert call(B=2**40, K=2**20) == 2          # size overflow
+    assert call(A=None) == 1 and call(L=None) == 1 and call(out=None) == 1
+    assert call(A=PA + 4) == 7 and call(out=POUT + 8) == 7 and call(b=PB + 2) == 7
+    # lambda overlapping A / b / lambda_K
+    assert call(out=PA + 256) == 8
+    assert call(out=PB) == 8
+    assert call(out=PL - 16) == 8
+    # widths out of range
+    assert call(widths=[64, 64, 0, 64]) == 2
+    assert call(widths=[64, 65, 64, 64]) == 2
+
+
+def test_empty_batch_is_a_noop():
+    # B = 0 succeeds without touching pointers or the GPU
+    assert call(B=0, A=None, L=None, out=None) == 0
+
+
+def test_workspace_query():
+    for r in (16, 32, 64, 128):
+        for dt in (0, 1):
+            assert binding.lbi_scan_backward_workspace_bytes(4, 8, r, dt) == 0

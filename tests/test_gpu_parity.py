@@ -1,0 +1,208 @@
+"""Parity of the HIP scan with the CPU oracle, through the C-ABI (needs a GPU).
+
+Tolerances (relative Frobenius over the compared output):
+  * float32 storage: 1e-5; bf16 storage with fp32 accumulation: 2e-2.
+  * bf16 runs also check 1e-3, well above what the hi/lo feedback of the
+    composite leaves (about 1e-5), to catch a lost low part.
+  * chains whose products do not contract (orthogonal A over many slots)
+    carry fp32 rounding as a random walk: relative error ~ c sqrt(K r) u with
+    u = 2^-24, so their bound is 8 sqrt(K r) u.
+Integer/permutation inputs, where every intermediate is exact in fp32, must
+match bit for bit.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2605_09204_amd import binding, synth
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+BF16_EXPECTED = 1e-3
+U32 = 2.0 ** -24
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def run_gpu(x: synth.Inputs, widths=None, stream=None):
+    dev = torch.device("cuda:0")
+    A = x.A.to(dev)
+    b = None if x.b is None else x.b.to(dev)
+    lk = x.lamK.to(dev)
+    if widths is None:
+        lam = binding.lbi_scan_backward(A, b, lk, stream=stream)
+    else:
+        lam = binding.lbi_scan_backward_widths(A, b, lk, widths, stream=stream)
+    torch.cuda.synchronize()
+    return lam
+
+
+def ref(x: synth.Inputs, idx=None):
+    if idx is not None:
+        x = x.chains(idx)
+    return oracle.recurrence(x.A, x.b, x.lamK)
+
+
+def assert_close(got, want, tol, what=""):
+    got = np.asarray(got, dtype=np.float64)
+    err = oracle.rel_frobenius(got, want)
+    per = oracle.per_chain_rel_frobenius(got, want)
+    _say(f"  {what}: rel-Frobenius {err:.3e}, worst chain {per.max():.3e}")
+    assert err <= tol, f"{what}: relative Frobenius error {err:.3e} > {tol:.1e}"
+    # element by element: no entry off by more than tol x the chain's max
+    scale = np.abs(want).reshape(want.shape[0], -1).max(axis=1)
+    diff = np.abs(got - want).reshape(want.shape[0], -1).max(axis=1)
+    bad = diff > 4 * tol * np.maximum(scale, 1e-30)
+    assert not bad.any(), f"{what}: elementwise error in chains {np.nonzero(bad)[0][:8]}"
+    return err
+
+
+def sample_chains(B, n=48, seed=0):
+    if B <= n:
+        return torch.arange(B)
+    g = torch.Generator().manual_seed(seed)
+    mid = torch.randperm(B - 2, generator=g)[: n - 2] + 1
+    return torch.cat([torch.tensor([0, B - 1]), mid]).sort().values
+
+
+# ----------------------------------------------------------------------------
+# the five workloads at full size, in the launch configuration of the bench
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", synth.WORKLOAD_ORDER)
+def test_workload_parity_full_size(name):
+    wl = synth.WORKLOADS[name]
+    _say(f"[parity] workload {name}: B={wl.B} K={wl.K} r={wl.r} {wl.dtype}")
+    x = synth.generate(wl, device="cuda:0")
+    hint = wl.widths
+    lam = run_gpu(x, widths=hint)
+    idx = sample_chains(wl.B)
+    xh = x.to("cpu")
+    want = ref(xh, idx)
+    got = lam[idx.to(lam.device)].cpu().numpy()
+    err = assert_close(got, want, TOL[wl.dtype], name)
+    if wl.dtype == "bf16":
+        assert err <= BF16_EXPECTED
+    if hint is not None:
+        # padded output lanes are exactly zero
+        for j in range(wl.K):
+            if hint[j] < wl.r:
+                assert float(lam[:, j, hint[j]:].abs().max()) == 0.0
+
+
+# ----------------------------------------------------------------------------
+# shapes off the workload grid: ragged K, single chains, every tile width
+# ----------------------------------------------------------------------------
+
+STRESS = [(B, K, r) for r in (16, 32, 64, 128) for (B, K) in
+          ((1, 1), (3, 2), (2, 3), (5, 31), (4, 33), (1, 130))]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("B,K,r", STRESS)
+def test_stress_shapes(B, K, r, dtype):
+    _say(f"[stress] B={B} K={K} r={r} {dtype}")
+    for affine in (True, False):
+        x = synth.random_chain(B, K, r, dtype=dtype, seed=K * 7 + r, affine=affine)
+        lam = run_gpu(x)
+        assert_close(lam.cpu().numpy(), ref(x), TOL[dtype] if dtype == "f32" else BF16_EXPECTED,
+                     f"B{B} K{K} r{r} {dtype} affine={affine}")
+
+
+def test_long_contracting_chain_r16():
+    x = synth.random_chain(2, 2049, 16, dtype="f32", seed=3, spectrum="concentrated")
+    _say("[stress] K=2049 r=16 concentrated")
+    assert_close(run_gpu(x).cpu().numpy(), ref(x), TOL["f32"], "K2049")
+
+
+@pytest.mark.parametrize("r", [16, 32, 64, 128])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_permutation_chains_bit_exact(r, dtype):
+    _say(f"[exact] permutation r={r} {dtype}")
+    for K in (1, 7, 40):
+        x = synth.permutation_chain(3, K, r, dtype=dtype, seed=K + r)
+        got = run_gpu(x).cpu().numpy().astype(np.float64)
+        assert np.array_equal(got, ref(x)), f"K={K}"
+
+
+def test_orthogonal_long_chain_carries_norm():
+    """s == 1, b = 0, K = 512: nothing decays, so every slot tests the carry."""
+    K, r = 512, 64
+    _say("[stress] orthogonal K=512 r=64")
+    x = synth.random_chain(4, K, r, dtype="f32", seed=9, spectrum="orthogonal", affine=False)
+    lam = run_gpu(x).cpu().numpy().astype(np.float64)
+    tol = 8 * math.sqrt(K * r) * U32
+    assert_close(lam, ref(x), tol, "orthogonal K512")
+    ratio = np.linalg.norm(lam, axis=-1) / np.linalg.norm(x.lamK.double().numpy(), axis=-1)[:, None]
+    assert np.allclose(ratio, 1.0, atol=tol * 4)
+
+
+# ----------------------------------------------------------------------------
+# API behaviour
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_null_b_equals_zero_b(dtype):
+    x = synth.random_chain(8, 20, 64, dtype=dtype, seed=1, affine=False)
+    none = run_gpu(x)
+    zero = synth.Inputs(x.A, torch.zeros(x.A.shape[:3], dtype=x.A.dtype), x.lamK, x.widths,
+                        x.workload)
+    assert torch.equal(none, run_gpu(zero))
+
+
+def test_bitwise_deterministic():
+    x = synth.generate(synth.WORKLOADS["paper_width"], device="cuda:0")
+    a = run_gpu(x)
+    b = run_gpu(x)
+    assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_widths_hint_matches_unhinted(dtype):
+    widths = synth.cyclic_widths(23)
+    x = synth.random_chain(6, 23, 128, dtype=dtype, seed=2, widths=widths)
+    plain = run_gpu(x)
+    hinted = run_gpu(x, widths=widths)
+    assert torch.equal(plain, hinted)
+    for j in range(23):
+        if widths[j] < 128:
+            assert float(hinted[:, j, widths[j]:].abs().max()) == 0.0
+    assert_close(hinted.cpu().numpy(), ref(x), BF16_EXPECTED if dtype == "bf16" else TOL["f32"],
+                 f"hinted {dtype}")
+
+
+def test_runs_on_the_given_stream():
+    x = synth.generate(synth.WORKLOADS["tiny"], device="cuda:0")
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        lam = binding.lbi_scan_backward(x.A, x.b, x.lamK)
+    s.synchronize()
+    assert_close(lam.cpu().numpy(), ref(x.to("cpu")), TOL["f32"], "side stream")
+
+
+def test_empty_batch_and_argument_errors_on_gpu():
+    A = torch.zeros((0, 4, 64, 64), device="cuda:0")
+    lk = torch.zeros((0, 64), device="cuda:0")
+    assert binding.lbi_scan_backward(A, None, lk).shape == (0, 4, 64)
+    A = torch.zeros((2, 4, 48, 48), device="cuda:0")
+    with pytest.raises(binding.LbiError) as e:
+        binding.lbi_scan_backward(A, None, torch.zeros((2, 48), device="cuda:0"))
+    assert e.value.status == 4
+
+
+def test_nan_propagates():
+    x = synth.random_chain(2, 6, 64, dtype="f32", seed=4)
+    lk = x.lamK.clone()
+    lk[1, 5] = float("nan")
+    y = synth.Inputs(x.A, x.b, lk, x.widths, x.workload)
+    lam = run_gpu(y).cpu()
+    assert torch.isnan(lam[1]).all()
+    assert torch.isfinite(lam[0]).all()
