@@ -95,6 +95,58 @@ def source_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
+def _counter_rows(path):
+    """(kernel name, counter name, value) per dispatch of a rocprofv3
+    counter-collection CSV."""
+    import csv
+    rows = []
+    with open(path, newline="") as f:
+        for rec in csv.DictReader(f):
+            name = rec.get("Kernel_Name") or rec.get("Kernel-Name") or ""
+            cname = rec.get("Counter_Name") or rec.get("Counter-Name") or ""
+            val = rec.get("Counter_Value") or rec.get("Counter-Value") or "nan"
+            rows.append((name, cname, float(val)))
+    return rows
+
+
+def record_traffic(workload: str, fetch_csv: str, write_csv: str, copy_mib: int) -> dict:
+    """HBM bytes per launch of the scan kernel from two rocprofv3 PMC runs
+    (FETCH_SIZE, then WRITE_SIZE, in KiB per dispatch), each scaled by what the
+    same counter reads for the calibration copy kernel of known size."""
+    copy_bytes = float(copy_mib << 20)
+    out = {"workload": workload, "source_sha256_16": source_hash(),
+           "calibration_copy_bytes": copy_bytes}
+    for tag, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"),
+                               ("write", write_csv, "WRITE_SIZE")):
+        rows = [r for r in _counter_rows(path) if r[1] == counter]
+        scan = [v for n, _, v in rows if "scan_chain_kernel" in n]
+        copy = [v for n, _, v in rows if "neg_kernel" in n]
+        if not scan or not copy:
+            raise SystemExit(f"{path}: no {counter} rows for the scan or the copy kernel")
+        kib_scan = sum(scan) / len(scan)
+        kib_copy = sum(copy) / len(copy)
+        factor = copy_bytes / (kib_copy * 1024.0)
+        out[f"{tag}_kib_per_dispatch"] = kib_scan
+        out[f"{tag}_copy_kib_per_dispatch"] = kib_copy
+        out[f"{tag}_scale"] = factor
+        out[f"{tag}_bytes_per_launch"] = kib_scan * 1024.0 * factor
+        out[f"{tag}_dispatches"] = len(scan)
+    out["hbm_bytes_per_launch"] = out["fetch_bytes_per_launch"] + out["write_bytes_per_launch"]
+    wl_bytes = None
+    try:
+        from paper_2605_09204_amd import synth
+        wl_bytes = bytes_alg(synth.WORKLOADS[workload])
+    except Exception:
+        pass
+    out["alg_bytes_per_launch"] = wl_bytes
+    os.makedirs(TRAFFIC_DIR, exist_ok=True)
+    path = os.path.join(TRAFFIC_DIR, f"traffic_{workload}.json")
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    return out
+
+
 def load_traffic(workload: str):
     """Measured HBM bytes per launch from the rocprofv3 PMC runs, if they were
     taken on the current kernel source; else None."""
@@ -159,7 +211,21 @@ def main(argv=None) -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="also run a plain device copy of this many MiB (for PMC scaling)")
+    ap.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write profiles/traffic_<workload>.json from two rocprofv3 "
+                         "counter-collection CSVs (FETCH_SIZE, WRITE_SIZE) of a run with "
+                         "--copy-calibration MIB, then exit")
     args = ap.parse_args(argv)
+
+    if args.record_traffic:
+        if args.copy_calibration <= 0:
+            print("--record-traffic needs the --copy-calibration MIB of the PMC runs",
+                  file=sys.stderr)
+            return 2
+        rec = record_traffic(args.workload, args.record_traffic[0], args.record_traffic[1],
+                             args.copy_calibration)
+        print(json.dumps(rec))
+        return 0
 
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -203,11 +269,14 @@ def main(argv=None) -> int:
             binding.lbi_scan_backward_widths(c.A, c.b, c.lamK, hint, lam=lam)
 
     if args.copy_calibration > 0:
-        n = args.copy_calibration << 20
-        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        # A plain streaming kernel of known size (torch's elementwise negation:
+        # reads and writes MiB << 20 bytes each) against which the PMC byte
+        # counters of the scan kernel are scaled.
+        n = (args.copy_calibration << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
         for _ in range(3):
-            dst.copy_(src)
+            torch.neg(src, out=dst)
         torch.cuda.synchronize()
         del src, dst
 
