@@ -7,7 +7,7 @@ line.  Default workload: ``long_chain`` (B=512 chains, K=512 regions, r=64,
 fp32), the largest batched r=64 workload.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                  [--no-cpu-baseline] [--copy-calibration MiB]
+                  [--math split|mfma] [--no-cpu-baseline] [--copy-calibration MiB]
 
 Accounting (flop = 2 per multiply-add; the paper counts r^3 per r x r
 product, i.e. one per multiply-add, in its scan-negligibility estimate):
@@ -17,6 +17,12 @@ product, i.e. one per multiply-add, in its scan-negligibility estimate):
   algorithmic flops = B [sum_{j<K-1} combine_j + sum_j apply_j],
   algorithmic bytes = A (true-width tiles), b, lambda_K read once, lambda
   written once (fp32, padded rows included).
+
+Roofline: the kernel's ideal time is the larger of (algorithmic bytes / HBM
+peak) and (matrix-core flops it executes / the peak of the MFMA type it uses);
+the larger one names the bound.  Executed matrix-core flops per combine: 2 r^3
+for fp32 on the fp32 matrix cores, 4 r^3 for bf16 storage (hi + lo parts of the
+composite), 12 r^3 for fp32 as three-part bf16 splits (six partial products).
 """
 from __future__ import annotations
 
@@ -83,6 +89,38 @@ def bytes_alg(wl, padded: bool = False) -> int:
     lk = R if padded else w[wl.K]
     out = wl.K * R * 4
     return wl.B * ((a + bb + lk) * e + out)
+
+
+def mfma_flops_executed(wl, math: str) -> int:
+    """Matrix-core flops one launch executes, at the shapes the kernel runs:
+    r x r tiles, or with the widths hint the slot's row and k blocks rounded
+    up to 16 x a power of two and the r_K columns rounded up to 16; bf16
+    products take k in blocks of 32."""
+    w = widths_of(wl)
+    rK = w[wl.K]
+    mode = mode_of(wl, math)
+    reps = {"f32-mfma": 1, "bf16": 2, "f32-split": 6}[mode]
+
+    def blk(x):
+        return 16 * (1 << max(0, (-(-x // 16) - 1).bit_length()))
+
+    cols = 16 * -(-rK // 16) if wl.widths else wl.r
+    per_chain = 0
+    for j in range(wl.K - 1):
+        rows = blk(w[j]) if wl.widths else wl.r
+        ks = blk(w[j + 1]) if wl.widths else wl.r
+        if mode != "f32-mfma":
+            ks = 32 * -(-ks // 32)
+        per_chain += 2 * rows * ks * cols
+    return wl.B * per_chain * reps
+
+
+def mode_of(wl, math: str) -> str:
+    if wl.dtype == "bf16":
+        return "bf16"
+    if math == "split" and wl.r <= 64:
+        return "f32-split"
+    return "f32-mfma"
 
 
 def scan_payload_bytes(K: int, r: int, elem: int) -> int:
@@ -208,6 +246,9 @@ def main(argv=None) -> int:
     ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="long_chain")
+    ap.add_argument("--math", choices=["split", "mfma"], default="split",
+                    help="float32 arithmetic: three-part bf16 splits on the bf16 matrix "
+                         "cores (the library default) or the fp32 matrix cores")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="also run a plain device copy of this many MiB (for PMC scaling)")
@@ -261,12 +302,11 @@ def main(argv=None) -> int:
     lam = torch.empty((wl.B, wl.K, wl.r), dtype=torch.float32, device=dev)
     hint = wl.widths
 
+    math = binding.LBI_MATH_F32_SPLIT if args.math == "split" else binding.LBI_MATH_F32_MFMA
+
     def step(i):
         c = copies[i % ncopy]
-        if hint is None:
-            binding.lbi_scan_backward(c.A, c.b, c.lamK, lam=lam)
-        else:
-            binding.lbi_scan_backward_widths(c.A, c.b, c.lamK, hint, lam=lam)
+        binding.lbi_scan_backward_ex(c.A, c.b, c.lamK, hint, math, lam=lam)
 
     if args.copy_calibration > 0:
         # A plain streaming kernel of known size (torch's elementwise negation:
@@ -305,15 +345,21 @@ def main(argv=None) -> int:
     b_alg = bytes_alg(wl)
     tflops = f_alg / avg_launch_s / 1e12
     gbs = b_alg / avg_launch_s / 1e9
-    if wl.dtype == "f32":
-        roof = {"bound": "mfma", "achieved": tflops, "peak": PEAK["mfma_f32_tflops"],
-                "unit": "TFLOP/s"}
+    mode = mode_of(wl, args.math)
+    f_exec = mfma_flops_executed(wl, args.math)
+    mfma_peak = PEAK["mfma_f32_tflops"] if mode == "f32-mfma" else PEAK["mfma_bf16_tflops"]
+    t_mfma = f_exec / (mfma_peak * 1e12)
+    t_hbm = b_alg / (PEAK["hbm_gbs"] * 1e9)
+    if t_mfma >= t_hbm:
+        # matrix-core bound: algorithmic flops against the fp32 peak when the
+        # products run on the fp32 matrix cores, else executed bf16 flops
+        # against the bf16 peak
+        ach = tflops if mode == "f32-mfma" else f_exec / avg_launch_s / 1e12
+        roof = {"bound": "mfma", "achieved": ach, "peak": mfma_peak, "unit": "TFLOP/s"}
     else:
         roof = {"bound": "hbm", "achieved": gbs, "peak": PEAK["hbm_gbs"], "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = load_traffic(wl.name)
-
-    mfma_peak = PEAK["mfma_f32_tflops"] if wl.dtype == "f32" else PEAK["mfma_bf16_tflops"]
+    roof["traffic"] = load_traffic(wl.name) if args.math == "split" or wl.dtype == "bf16" else None
     out = {
         "metric": METRIC,
         "value": value,
@@ -329,13 +375,17 @@ def main(argv=None) -> int:
         "data": "synthetic (seeded Haar-orthogonal x diag x Haar-orthogonal interface "
                 "Jacobians; no dataset or checkpoint)",
         "config": {"workload": wl.name, "B": wl.B, "K": wl.K, "r": wl.r,
-                   "storage": wl.dtype, "affine": wl.affine,
+                   "storage": wl.dtype, "affine": wl.affine, "arithmetic": mode,
                    "widths": "cyclic 32/64/128" if wl.widths else "uniform",
                    "parallelism": "single GPU, one workgroup per chain"},
         "roofline": roof,
         "extra": {
             "alg_tflops": tflops,
-            "pct_of_mfma_peak": 100.0 * tflops / mfma_peak,
+            "pct_of_fp32_mfma_peak": 100.0 * tflops / PEAK["mfma_f32_tflops"],
+            "executed_mfma_tflops": f_exec / avg_launch_s / 1e12,
+            "executed_mfma_peak_tflops": mfma_peak,
+            "ideal_ms_hbm": t_hbm * 1e3,
+            "ideal_ms_mfma": t_mfma * 1e3,
             "alg_hbm_gbs": gbs,
             "pct_of_hbm_peak": 100.0 * gbs / PEAK["hbm_gbs"],
             "avg_launch_ms": avg_launch_s * 1e3,

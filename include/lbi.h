@@ -49,7 +49,7 @@ extern "C" {
 /* HIP stream handle (the same type as hipStream_t). */
 typedef struct ihipStream_t *lbi_stream_t;
 
-#define LBI_ABI_VERSION 1
+#define LBI_ABI_VERSION 2
 
 /* Largest K for which a widths hint is used (longer chains run unhinted,
  * which gives identical results). */
@@ -60,11 +60,23 @@ typedef enum {
     LBI_BF16 = 1  /* stored as bfloat16; bf16 MFMA products, fp32 sums      */
 } lbi_dtype;
 
+/* How float32 inputs are multiplied (lbi_scan_backward_ex).  bf16 inputs
+ * always use the bf16 matrix cores. */
+typedef enum {
+    LBI_MATH_DEFAULT = 0,   /* the library's choice: LBI_MATH_F32_SPLIT          */
+    LBI_MATH_F32_MFMA = 1,  /* fp32 products on the fp32 matrix cores            */
+    LBI_MATH_F32_SPLIT = 2  /* fp32 products from exact three-part bf16 splits
+                             * of both operands on the bf16 matrix cores (the
+                             * six partial products down to 2^-16 of the leading
+                             * one), fp32 accumulation                           */
+} lbi_math;
+
 typedef enum {
     LBI_OK = 0,
     LBI_ERR_NULL = 1,          /* a required pointer is NULL                */
     LBI_ERR_SHAPE = 2,         /* B < 0, K < 1, size overflow, bad widths   */
-    LBI_ERR_DTYPE = 3,         /* dtype not an lbi_dtype                    */
+    LBI_ERR_DTYPE = 3,         /* dtype not an lbi_dtype, or math not an    *
+                                * lbi_math                                  */
     LBI_ERR_UNSUPPORTED_R = 4, /* r not in {16, 32, 64, 128}                */
     LBI_ERR_WORKSPACE = 5,     /* workspace missing or too small            */
     LBI_ERR_HIP = 6,           /* the HIP runtime refused the launch        */
@@ -95,11 +107,12 @@ size_t lbi_scan_backward_workspace_bytes(int64_t B, int64_t K, int32_t r, lbi_dt
  *                           lbi_scan_backward_workspace_bytes(B, K, r, dt).
  *   stream: the HIP stream to enqueue on.
  *
- * Precision: LBI_F32 composes and applies in float32 throughout.  LBI_BF16
- * multiplies bf16 operands on the matrix cores with float32 accumulation; the
- * running float32 composite is fed back as a two-term bf16 split (hi + lo),
- * so only the inputs are bf16-rounded.  Results are bitwise reproducible run
- * to run for a given (B, K, r, dt).
+ * Precision: LBI_F32 composes and applies in float32 throughout; its matrix
+ * products are formed as LBI_MATH_DEFAULT says (see lbi_scan_backward_ex).
+ * LBI_BF16 multiplies bf16 operands on the matrix cores with float32
+ * accumulation; the running float32 composite is fed back as a two-term bf16
+ * split (hi + lo), so only the inputs are bf16-rounded.  Results are bitwise
+ * reproducible run to run for a given (B, K, r, dt, math).
  */
 lbi_status lbi_scan_backward(const void *A, const void *b, const void *lambda_K,
                              float *lambda, int64_t B, int64_t K, int32_t r, lbi_dtype dt,
@@ -118,6 +131,18 @@ lbi_status lbi_scan_backward_widths(const void *A, const void *b, const void *la
                                     float *lambda, int64_t B, int64_t K, int32_t r,
                                     lbi_dtype dt, void *workspace, size_t workspace_bytes,
                                     lbi_stream_t stream, const int32_t *widths_host);
+
+/*
+ * As lbi_scan_backward_widths (widths_host may be NULL), with the arithmetic
+ * for float32 inputs chosen by `math`; for LBI_BF16 inputs `math` must still
+ * be a valid lbi_math and has no effect.  LBI_MATH_F32_MFMA and
+ * LBI_MATH_F32_SPLIT agree to float32 rounding (both accumulate in float32);
+ * they are not bitwise equal.
+ */
+lbi_status lbi_scan_backward_ex(const void *A, const void *b, const void *lambda_K,
+                                float *lambda, int64_t B, int64_t K, int32_t r, lbi_dtype dt,
+                                void *workspace, size_t workspace_bytes, lbi_stream_t stream,
+                                const int32_t *widths_host, lbi_math math);
 
 /* A static, human-readable name for a status code. */
 const char *lbi_status_string(lbi_status s);

@@ -19,6 +19,9 @@ LBI_F32 = 0
 LBI_BF16 = 1
 LBI_OK = 0
 LBI_MAX_HINT_K = 2047
+LBI_MATH_DEFAULT = 0
+LBI_MATH_F32_MFMA = 1
+LBI_MATH_F32_SPLIT = 2
 
 _DTYPES = {torch.float32: LBI_F32, torch.bfloat16: LBI_BF16}
 
@@ -55,6 +58,9 @@ def load() -> ctypes.CDLL:
     lib.lbi_scan_backward_widths.argtypes = [vp, vp, vp, vp, i64, i64, i32, ctypes.c_int, vp,
                                              sz, vp, ctypes.POINTER(ctypes.c_int32)]
     lib.lbi_scan_backward_widths.restype = ctypes.c_int
+    lib.lbi_scan_backward_ex.argtypes = [vp, vp, vp, vp, i64, i64, i32, ctypes.c_int, vp, sz,
+                                         vp, ctypes.POINTER(ctypes.c_int32), ctypes.c_int]
+    lib.lbi_scan_backward_ex.restype = ctypes.c_int
     lib.lbi_status_string.argtypes = [ctypes.c_int]
     lib.lbi_status_string.restype = ctypes.c_char_p
     lib.lbi_abi_version.argtypes = []
@@ -125,6 +131,15 @@ def lbi_scan_backward(A: torch.Tensor, b: Optional[torch.Tensor], lambda_K: torc
     return lam
 
 
+def _widths_arg(widths, K):
+    if widths is None:
+        return None, None
+    if len(widths) != K + 1:
+        raise ValueError("widths must hold K+1 entries")
+    warr = (ctypes.c_int32 * len(widths))(*[int(x) for x in widths])
+    return warr, ctypes.cast(warr, ctypes.POINTER(ctypes.c_int32))
+
+
 def lbi_scan_backward_widths(A: torch.Tensor, b: Optional[torch.Tensor],
                              lambda_K: torch.Tensor, widths: Optional[Sequence[int]],
                              lam: Optional[torch.Tensor] = None,
@@ -132,11 +147,17 @@ def lbi_scan_backward_widths(A: torch.Tensor, b: Optional[torch.Tensor],
                              stream=None) -> torch.Tensor:
     """As lbi_scan_backward with the interface widths r_0..r_K as a hint."""
     lam, args = _marshal(A, b, lambda_K, lam, workspace, stream)
-    wptr = None
-    if widths is not None:
-        if len(widths) != int(A.shape[1]) + 1:
-            raise ValueError("widths must hold K+1 entries")
-        warr = (ctypes.c_int32 * len(widths))(*[int(x) for x in widths])
-        wptr = ctypes.cast(warr, ctypes.POINTER(ctypes.c_int32))
+    warr, wptr = _widths_arg(widths, int(A.shape[1]))
     _check(load().lbi_scan_backward_widths(*args, wptr))
+    return lam
+
+
+def lbi_scan_backward_ex(A: torch.Tensor, b: Optional[torch.Tensor], lambda_K: torch.Tensor,
+                         widths: Optional[Sequence[int]] = None, math: int = LBI_MATH_DEFAULT,
+                         lam: Optional[torch.Tensor] = None,
+                         workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """As lbi_scan_backward_widths, with the float32 arithmetic chosen by ``math``."""
+    lam, args = _marshal(A, b, lambda_K, lam, workspace, stream)
+    warr, wptr = _widths_arg(widths, int(A.shape[1]))
+    _check(load().lbi_scan_backward_ex(*args, wptr, int(math)))
     return lam

@@ -21,15 +21,26 @@
 //   * Work is the algorithmic minimum: the K-1 combines of a right-to-left
 //     inclusive scan; the B independent chains fill the GPU.
 //   * A_j tiles stream HBM -> registers (buffer loads NPF slots ahead, 16
-//     bytes per lane, branch-free) -> LDS (padded rows: conflict-free MFMA
-//     operand reads), one barrier per slot.
+//     bytes per lane, branch-free) -> LDS, one barrier per slot.  While a tile
+//     is staged from registers, the same registers give the affine update
+//     c_j = A_j c_{j+1} + b_j (partial dot products reduced across the lanes
+//     that share a row), so A is never re-read for it.
 //   * The apply of slot j+1 (P_{j+1} lambda_K: per-wave partial sums reduced
 //     by a DPP butterfly, then across waves through LDS) is issued between
 //     the MFMAs that form P_j, so VALU and matrix-core work overlap;
-//     c_j = A_j c_{j+1} + b_j runs on the VALU with rows split over the
-//     workgroup; lambda_j is stored once, coalesced, by one wave in turn.
-//   * bf16: A tiles are bf16 MFMA operands; the fp32 composite is fed back as
-//     bf16 hi + lo (two MFMAs), so the only bf16 rounding is the inputs'.
+//     lambda_j is stored once, coalesced, by one wave in turn.
+//   * Three arithmetic modes:
+//       kF32   fp32 storage, v_mfma_f32_16x16x4_f32;
+//       kBF16  bf16 storage, v_mfma_f32_16x16x32_bf16; the fp32 composite is
+//              fed back as bf16 hi + lo (two MFMAs), so the only bf16
+//              rounding is the inputs';
+//       kF32X  fp32 storage on the bf16 matrix cores: A_j and P are each cut
+//              into three bf16 parts whose sum is exactly the fp32 value
+//              (truncated high part, then the remainder twice), and the
+//              product keeps the six partial products down to 2^-16 of the
+//              leading one, accumulated in fp32.  Error matches fp32 MFMA.
+//     bf16 tiles sit in LDS with each 32-wide k block stored in MFMA operand
+//     order, so one 16-byte LDS read yields a lane's 8 operand values.
 //   * Widths hint: loads of all-zero tile regions are skipped (out-of-range
 //     buffer offsets return zero without touching memory) and the combine
 //     runs a shape specialised to the slot's row and k blocks.
@@ -46,27 +57,39 @@ namespace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-enum : int { kF32 = 0, kBF16 = 1 };
+enum : int { kF32 = 0, kBF16 = 1, kF32X = 2 };
 
-template <int DT> struct Elem;
-template <> struct Elem<kF32> {
-    typedef float T;
-    static constexpr int kPad = 4;  // LDS row pitch R + 4 floats
+// E: storage element; L: LDS element of the staged A tile; PLANES: LDS
+// copies of the tile (three bf16 parts for kF32X); PAD: row padding in L.
+template <int M> struct Mode;
+template <> struct Mode<kF32> {
+    typedef float E;
+    typedef float L;
+    static constexpr int PLANES = 1, PAD = 4;
 };
-template <> struct Elem<kBF16> {
-    typedef __bf16 T;
-    static constexpr int kPad = 8;  // LDS row pitch R + 8 bf16
+template <> struct Mode<kBF16> {
+    typedef __bf16 E;
+    typedef __bf16 L;
+    static constexpr int PLANES = 1, PAD = 8;
+};
+template <> struct Mode<kF32X> {
+    typedef float E;
+    typedef __bf16 L;
+    static constexpr int PLANES = 3, PAD = 8;
 };
 
 constexpr int waves_for(int R) { return R == 16 ? 1 : (R == 32 ? 2 : 4); }
+constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x / 2); }
 
 // Buffer resource word 3 for raw (untyped) buffer loads on gfx9-family GPUs.
 constexpr int kBufferWord3 = 0x00020000;
 // A per-lane offset past every tile: the load returns zero, no memory access.
 constexpr int kOutOfRange = 0x40000000;
+constexpr uint32_t kHighHalf = 0xFFFF0000u;
 
 struct ScanArgs {
     const void *A;
@@ -99,40 +122,77 @@ template <int CTRL> __device__ __forceinline__ float dpp(float x)
     return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, false));
 }
 
-// One butterfly stage over N live values: lanes whose bit BIT is 0 keep the
-// lower half (summed with the partner's lower half), the others the upper.
-template <int N, int CTRL, int BIT, int V>
-__device__ __forceinline__ void bfly_split(float (&q)[V], int li)
+// The value of lane (this lane ^ MASK); MASK 7 stands in for 4 (it flips the
+// same top bit of an 8-lane group, and together with 2 and 1 it still spans
+// every lane of the group).
+template <int MASK> __device__ __forceinline__ float xchg(float x)
 {
-    const bool upper = (li >> BIT) & 1;
-#pragma unroll
-    for (int i = 0; i < N / 2; ++i) {
-        const float keep = upper ? q[i + N / 2] : q[i];
-        const float send = upper ? q[i] : q[i + N / 2];
-        q[i] = keep + dpp<CTRL>(send);
+    if constexpr (MASK == 1) return dpp<kDppXor1>(x);
+    else if constexpr (MASK == 2) return dpp<kDppXor2>(x);
+    else if constexpr (MASK == 7) return dpp<kDppXor7>(x);
+    else if constexpr (MASK == 8) return dpp<kDppXor8>(x);
+    else {
+        static_assert(MASK == 16, "lane exchange");
+        return __shfl_xor(x, 16);
     }
 }
 
-// Sum V values per lane over the 16 lanes of a row.  The partner masks
-// 8, 7, 2, 1 span GF(2)^4, so after the four stages lane li holds the full
-// sums of original indices (li >> SHIFT) * VF + e, e < VF, where
-// VF = max(1, V / 16) and SHIFT = log2(16 / V) for V < 16.
-template <int V> __device__ __forceinline__ void row_reduce(float (&q)[V], int li)
+// Sum LIVE values per lane over an aligned group of N lanes (gi = lane index
+// in the group).  Each stage either halves the live values (lanes whose bit
+// BIT is 0 keep the lower half, summed with the partner's lower half, the
+// others the upper) or, with one value left, adds the partner's.  Afterwards
+// lane gi holds, in q[e] for e < max(1, LIVE / N), the full group sum of
+// original index (gi >> S) * max(1, LIVE / N) + e with
+// S = log2(N) - log2(min(LIVE, N)).
+template <int N, int LIVE, int V> __device__ __forceinline__ void group_reduce(float (&q)[V], int gi)
 {
-    static_assert(V == 4 || V == 8 || V == 16 || V == 32, "unsupported width");
-    bfly_split<V, kDppXor8, 3>(q, li);
-    if constexpr (V >= 4) bfly_split<V / 2, kDppXor7, 2>(q, li);
-    else q[0] += dpp<kDppXor7>(q[0]);
-    if constexpr (V >= 8) bfly_split<V / 4, kDppXor2, 1>(q, li);
-    else q[0] += dpp<kDppXor2>(q[0]);
-    if constexpr (V >= 16) bfly_split<V / 8, kDppXor1, 0>(q, li);
-    else q[0] += dpp<kDppXor1>(q[0]);
+    if constexpr (N > 1) {
+        constexpr int MASK = N == 32 ? 16 : (N == 16 ? 8 : (N == 8 ? 7 : (N == 4 ? 2 : 1)));
+        constexpr int BIT = ilog2(N) - 1;
+        if constexpr (LIVE >= 2) {
+            const bool upper = (gi >> BIT) & 1;
+#pragma unroll
+            for (int i = 0; i < LIVE / 2; ++i) {
+                const float keep = upper ? q[i + LIVE / 2] : q[i];
+                const float send = upper ? q[i] : q[i + LIVE / 2];
+                q[i] = keep + xchg<MASK>(send);
+            }
+            group_reduce<N / 2, LIVE / 2>(q, gi);
+        } else {
+            q[0] += xchg<MASK>(q[0]);
+            group_reduce<N / 2, 1>(q, gi);
+        }
+    }
 }
 
 template <typename T> __device__ __forceinline__ float to_f32(T x) { return (float)x; }
 
+__device__ __forceinline__ uint32_t fbits(float x) { return __float_as_uint(x); }
+__device__ __forceinline__ float bitsf(uint32_t u) { return __uint_as_float(u); }
+
+// Upper halves of two words, packed: the bf16 pair (lo, hi).
+__device__ __forceinline__ uint32_t pack_hi(uint32_t lo, uint32_t hi)
+{
+    return __builtin_amdgcn_perm(hi, lo, 0x07060302u);
+}
+
+// Three bf16 parts of two fp32 values with h + m + l == x exactly (for
+// normal x): h keeps the top 8 significant bits, m the next 8 of the
+// remainder, l the rest, which has at most 8 significant bits.
+struct Split2 {
+    uint32_t h, m, l;
+};
+__device__ __forceinline__ Split2 split_pair(float x0, float x1)
+{
+    const uint32_t h0 = fbits(x0) & kHighHalf, h1 = fbits(x1) & kHighHalf;
+    const float r0 = x0 - bitsf(h0), r1 = x1 - bitsf(h1);
+    const uint32_t m0 = fbits(r0) & kHighHalf, m1 = fbits(r1) & kHighHalf;
+    const float l0 = r0 - bitsf(m0), l1 = r1 - bitsf(m1);
+    return {pack_hi(h0, h1), pack_hi(m0, m1), pack_hi(fbits(l0), fbits(l1))};
+}
+
 // Geometry shared by the kernel and its pieces.
-template <int R, int DT, int NCA> struct Geo {
+template <int R, int M, int NCA> struct Geo {
     static constexpr int NW = waves_for(R);
     static constexpr int T = 64 * NW;
     static constexpr int NRB = R / 16;    // 16-row blocks
@@ -140,36 +200,67 @@ template <int R, int DT, int NCA> struct Geo {
     static constexpr int V = 4 * NRB;     // values per lane in the apply
     static constexpr int VF = V >= 16 ? V / 16 : 1;
     static constexpr int SHIFT = V >= 16 ? 0 : (V == 8 ? 1 : 2);
-    using E = typename Elem<DT>::T;
+    using E = typename Mode<M>::E;
+    using L = typename Mode<M>::L;
+    static constexpr int PLANES = Mode<M>::PLANES;
     static constexpr int ESZ = sizeof(E);
-    static constexpr int PITCH = R + Elem<DT>::kPad;
-    static constexpr int EPC = 16 / ESZ;                   // elements per 16-byte chunk
+    static constexpr int PITCH = R + Mode<M>::PAD;               // LDS row pitch in L
+    static constexpr bool PERM = sizeof(L) == 2 && R >= 32;      // k blocks in operand order
+    static constexpr int EPC = 16 / ESZ;                         // elements per 16-byte chunk
     static constexpr int TILE_CHUNKS = R * R / EPC;
-    static constexpr int CPT = (TILE_CHUNKS + T - 1) / T;  // chunks per thread
-    static constexpr int BCH = R / EPC;                    // chunks of one b row
-    static constexpr int TPR = T / R;                      // threads per row (c update)
-    static constexpr int CPR = R / TPR;                    // columns per thread
-    static constexpr int NPF = (DT == kBF16 && R <= 64) ? 3 : 2;  // slots prefetched
-    static constexpr int WPF = R > 64 ? R / 64 : 1;        // waves per finalize
-    static constexpr int NWF = NW / WPF;                   // finalizing wave groups
-    static_assert(NCA % NW == 0 && CB >= 1 && (TPR == 2 || TPR == 4), "tile geometry");
+    static constexpr int CPT = (TILE_CHUNKS + T - 1) / T;        // chunks per thread
+    static constexpr int LPR = R / EPC;                          // staging lanes per tile row
+    static constexpr int RPI = T / LPR;                          // tile rows per chunk index
+    static constexpr int SHIFT_S = ilog2(LPR) - ilog2(CPT);      // staging reduce layout
+    static constexpr int NPF = (M == kBF16 && R <= 64) ? 3 : 2;  // slots prefetched
+    static constexpr int WPF = R > 64 ? R / 64 : 1;              // waves per finalize
+    static constexpr int NWF = NW / WPF;                         // finalizing wave groups
+    static_assert(NCA % NW == 0 && CB >= 1, "tile geometry");
+    static_assert(CPT <= LPR && (T * EPC) % R == 0, "staging geometry");
 };
+
+// LDS column of tile column col (col % 4 == 0) in a k-permuted bf16 row: in
+// each 32-wide block, operand lane group g reads k = 4g..4g+3 and
+// 16+4g..16+4g+3 as its 8 consecutive values.
+template <bool PERM> __device__ __forceinline__ int lds_col(int col)
+{
+    if constexpr (!PERM) {
+        return col;
+    } else {
+        const int q = col & 31;
+        return (col & ~31) + (((q & 15) >> 2) << 3) + ((q >> 4) << 2);
+    }
+}
+
+// A operand (8 bf16 values) of row block I, k pair p, from one LDS plane.
+template <int R, int PITCH>
+__device__ __forceinline__ bf16x8 a_operand(const __bf16 *plane, int I, int p, int li, int g)
+{
+    if constexpr (R >= 32) {
+        return *(const bf16x8 *)&plane[(16 * I + li) * PITCH + 32 * p + 8 * g];
+    } else {
+        const bf16x4 a0 = *(const bf16x4 *)&plane[li * PITCH + 4 * g];
+        const bf16x4 z = {};
+        return __builtin_shufflevector(a0, z, 0, 1, 2, 3, 4, 5, 6, 7);
+    }
+}
 
 // Pn = A_j * P on the matrix cores, for the first NR row blocks and NK k blocks
 // (the rest of A_j is zero); rows past NR come out zero.
-template <int R, int DT, int NCA, int NR, int NK>
+template <int R, int M, int NCA, int NR, int NK>
 __device__ __forceinline__ void combine(f4 (&Pn)[R / 16][NCA / waves_for(R)],
                                         const f4 (&P)[R / 16][NCA / waves_for(R)],
-                                        const typename Elem<DT>::T *sAbuf, int li, int g)
+                                        const typename Mode<M>::L *sAbuf, int li, int g)
 {
-    using G = Geo<R, DT, NCA>;
+    using G = Geo<R, M, NCA>;
     constexpr int NRB = G::NRB, CB = G::CB, PITCH = G::PITCH;
+    constexpr int PLANE = R * PITCH;
 #pragma unroll
     for (int I = 0; I < NRB; ++I)
 #pragma unroll
         for (int t = 0; t < CB; ++t)
             Pn[I][t] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-    if constexpr (DT == kF32) {
+    if constexpr (M == kF32) {
 #pragma unroll
         for (int Ik = 0; Ik < NK; ++Ik) {
             f4 a[NR];
@@ -186,38 +277,117 @@ __device__ __forceinline__ void combine(f4 (&Pn)[R / 16][NCA / waves_for(R)],
                                                                          Pn[I][t], 0, 0, 0);
         }
     } else {
-        // k runs over pairs of 16-row blocks of P; a missing second block
-        // (one 16-block only) is zero in both operands.
+        // k runs over pairs of 16-row blocks of P (operand value e < 4 from
+        // the first block, e >= 4 from the second); a missing second block is
+        // zero in both operands.
         constexpr int NKP = (NK + 1) / 2;
+        constexpr bool kPairs = NRB >= 2;
 #pragma unroll
         for (int p = 0; p < NKP; ++p) {
-            constexpr bool kPairs = NRB >= 2;
-            bf16x8 bh[CB], bl[CB];
+            float x[CB][8];
 #pragma unroll
-            for (int t = 0; t < CB; ++t) {
+            for (int t = 0; t < CB; ++t)
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
-                    const float x0 = P[2 * p][t][v];
-                    const float x1 = kPairs ? P[kPairs ? 2 * p + 1 : 0][t][v] : 0.0f;
-                    const __bf16 h0 = (__bf16)x0, h1 = (__bf16)x1;
-                    bh[t][v] = h0;
-                    bh[t][v + 4] = h1;
-                    bl[t][v] = (__bf16)(x0 - (float)h0);
-                    bl[t][v + 4] = (__bf16)(x1 - (float)h1);
+                    x[t][v] = P[2 * p][t][v];
+                    x[t][v + 4] = kPairs ? P[kPairs ? 2 * p + 1 : 0][t][v] : 0.0f;
                 }
-            }
+            if constexpr (M == kBF16) {
+                // P = hi + lo (RNE hi, exact remainder, RNE lo)
+                bf16x8 bh[CB], bl[CB];
 #pragma unroll
-            for (int I = 0; I < NR; ++I) {
-                const typename Elem<DT>::T *rowp = &sAbuf[(16 * I + li) * PITCH + 32 * p + 4 * g];
-                const bf16x4 a0 = *(const bf16x4 *)rowp;
-                bf16x4 a1 = {};
-                if constexpr (kPairs)
-                    a1 = *(const bf16x4 *)(rowp + 16);
-                const bf16x8 a = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+                for (int t = 0; t < CB; ++t)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const __bf16 h = (__bf16)x[t][e];
+                        bh[t][e] = h;
+                        bl[t][e] = (__bf16)(x[t][e] - (float)h);
+                    }
+#pragma unroll
+                for (int I = 0; I < NR; ++I) {
+                    const bf16x8 a = a_operand<R, PITCH>(sAbuf, I, p, li, g);
+#pragma unroll
+                    for (int t = 0; t < CB; ++t) {
+                        Pn[I][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bh[t], Pn[I][t], 0, 0, 0);
+                        Pn[I][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bl[t], Pn[I][t], 0, 0, 0);
+                    }
+                }
+            } else {
+                bf16x8 bh[CB], bm[CB], bl[CB];
 #pragma unroll
                 for (int t = 0; t < CB; ++t) {
-                    Pn[I][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bh[t], Pn[I][t], 0, 0, 0);
-                    Pn[I][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bl[t], Pn[I][t], 0, 0, 0);
+                    u4 hh, mm, ll;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const Split2 s = split_pair(x[t][2 * e], x[t][2 * e + 1]);
+                        hh[e] = s.h;
+                        mm[e] = s.m;
+                        ll[e] = s.l;
+                    }
+                    bh[t] = __builtin_bit_cast(bf16x8, hh);
+                    bm[t] = __builtin_bit_cast(bf16x8, mm);
+                    bl[t] = __builtin_bit_cast(bf16x8, ll);
+                }
+                // the six partial products that reach 2^-16 of the leading one
+                auto terms = [&](const bf16x8 &ah, const bf16x8 &am, const bf16x8 &al, f4 &acc,
+                                 int t) {
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bh[t], acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bm[t], acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, bh[t], acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bl[t], acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bh[t], acc, 0, 0, 0);
+                    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, bm[t], acc, 0, 0, 0);
+                };
+                if constexpr (NR <= 4) {
+                    // all operands first, then the products interleaved over
+                    // the independent accumulators
+                    bf16x8 ah[NR], am[NR], al[NR];
+#pragma unroll
+                    for (int I = 0; I < NR; ++I) {
+                        ah[I] = a_operand<R, PITCH>(sAbuf, I, p, li, g);
+                        am[I] = a_operand<R, PITCH>(sAbuf + PLANE, I, p, li, g);
+                        al[I] = a_operand<R, PITCH>(sAbuf + 2 * PLANE, I, p, li, g);
+                    }
+#pragma unroll
+                    for (int t = 0; t < CB; ++t)
+#pragma unroll
+                        for (int I = 0; I < NR; ++I)
+                            Pn[I][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[I], bh[t], Pn[I][t], 0, 0, 0);
+#pragma unroll
+                    for (int t = 0; t < CB; ++t)
+#pragma unroll
+                        for (int I = 0; I < NR; ++I)
+                            Pn[I][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[I], bm[t], Pn[I][t], 0, 0, 0);
+#pragma unroll
+                    for (int t = 0; t < CB; ++t)
+#pragma unroll
+                        for (int I = 0; I < NR; ++I)
+                            Pn[I][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am[I], bh[t], Pn[I][t], 0, 0, 0);
+#pragma unroll
+                    for (int t = 0; t < CB; ++t)
+#pragma unroll
+                        for (int I = 0; I < NR; ++I)
+                            Pn[I][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[I], bl[t], Pn[I][t], 0, 0, 0);
+#pragma unroll
+                    for (int t = 0; t < CB; ++t)
+#pragma unroll
+                        for (int I = 0; I < NR; ++I)
+                            Pn[I][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[I], bh[t], Pn[I][t], 0, 0, 0);
+#pragma unroll
+                    for (int t = 0; t < CB; ++t)
+#pragma unroll
+                        for (int I = 0; I < NR; ++I)
+                            Pn[I][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am[I], bm[t], Pn[I][t], 0, 0, 0);
+                } else {
+#pragma unroll
+                    for (int I = 0; I < NR; ++I) {
+                        const bf16x8 ah = a_operand<R, PITCH>(sAbuf, I, p, li, g);
+                        const bf16x8 am = a_operand<R, PITCH>(sAbuf + PLANE, I, p, li, g);
+                        const bf16x8 al = a_operand<R, PITCH>(sAbuf + 2 * PLANE, I, p, li, g);
+#pragma unroll
+                        for (int t = 0; t < CB; ++t)
+                            terms(ah, am, al, Pn[I][t], t);
+                    }
                 }
             }
         }
@@ -226,47 +396,48 @@ __device__ __forceinline__ void combine(f4 (&Pn)[R / 16][NCA / waves_for(R)],
 
 // Runtime (row blocks, k blocks) of a hinted slot -> the specialised combine
 // for the next powers of two (extra blocks multiply zeros).
-template <int R, int DT, int NCA, int NR>
+template <int R, int M, int NCA, int NR>
 __device__ __forceinline__ void combine_k(int nk, f4 (&Pn)[R / 16][NCA / waves_for(R)],
                                           const f4 (&P)[R / 16][NCA / waves_for(R)],
-                                          const typename Elem<DT>::T *sAbuf, int li, int g)
+                                          const typename Mode<M>::L *sAbuf, int li, int g)
 {
     constexpr int NRB = R / 16;
-    if (nk <= 1 || NRB == 1) { combine<R, DT, NCA, NR, 1>(Pn, P, sAbuf, li, g); return; }
-    if constexpr (NRB >= 2) if (nk <= 2) { combine<R, DT, NCA, NR, 2>(Pn, P, sAbuf, li, g); return; }
-    if constexpr (NRB >= 4) if (nk <= 4) { combine<R, DT, NCA, NR, 4>(Pn, P, sAbuf, li, g); return; }
-    if constexpr (NRB >= 8) combine<R, DT, NCA, NR, 8>(Pn, P, sAbuf, li, g);
+    if (nk <= 1 || NRB == 1) { combine<R, M, NCA, NR, 1>(Pn, P, sAbuf, li, g); return; }
+    if constexpr (NRB >= 2) if (nk <= 2) { combine<R, M, NCA, NR, 2>(Pn, P, sAbuf, li, g); return; }
+    if constexpr (NRB >= 4) if (nk <= 4) { combine<R, M, NCA, NR, 4>(Pn, P, sAbuf, li, g); return; }
+    if constexpr (NRB >= 8) combine<R, M, NCA, NR, 8>(Pn, P, sAbuf, li, g);
 }
 
-template <int R, int DT, int NCA>
+template <int R, int M, int NCA>
 __device__ __forceinline__ void combine_shape(int nr, int nk, f4 (&Pn)[R / 16][NCA / waves_for(R)],
                                               const f4 (&P)[R / 16][NCA / waves_for(R)],
-                                              const typename Elem<DT>::T *sAbuf, int li, int g)
+                                              const typename Mode<M>::L *sAbuf, int li, int g)
 {
     constexpr int NRB = R / 16;
-    if (nr <= 1 || NRB == 1) { combine_k<R, DT, NCA, 1>(nk, Pn, P, sAbuf, li, g); return; }
-    if constexpr (NRB >= 2) if (nr <= 2) { combine_k<R, DT, NCA, 2>(nk, Pn, P, sAbuf, li, g); return; }
-    if constexpr (NRB >= 4) if (nr <= 4) { combine_k<R, DT, NCA, 4>(nk, Pn, P, sAbuf, li, g); return; }
-    if constexpr (NRB >= 8) combine_k<R, DT, NCA, 8>(nk, Pn, P, sAbuf, li, g);
+    if (nr <= 1 || NRB == 1) { combine_k<R, M, NCA, 1>(nk, Pn, P, sAbuf, li, g); return; }
+    if constexpr (NRB >= 2) if (nr <= 2) { combine_k<R, M, NCA, 2>(nk, Pn, P, sAbuf, li, g); return; }
+    if constexpr (NRB >= 4) if (nr <= 4) { combine_k<R, M, NCA, 4>(nk, Pn, P, sAbuf, li, g); return; }
+    if constexpr (NRB >= 8) combine_k<R, M, NCA, 8>(nk, Pn, P, sAbuf, li, g);
 }
 
-template <int R, int DT, bool AFF, bool HINT, int NCA>
+template <int R, int M, bool AFF, bool HINT, int NCA>
 __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const ScanArgs args)
 {
-    using G = Geo<R, DT, NCA>;
+    using G = Geo<R, M, NCA>;
     using E = typename G::E;
+    using L = typename G::L;
     constexpr int NW = G::NW, T = G::T, NRB = G::NRB, CB = G::CB, V = G::V, VF = G::VF;
     constexpr int SHIFT = G::SHIFT, PITCH = G::PITCH, EPC = G::EPC, CPT = G::CPT;
-    constexpr int TILE_CHUNKS = G::TILE_CHUNKS, BCH = G::BCH, TPR = G::TPR, CPR = G::CPR;
-    static_assert(BCH <= T, "b row fits one chunk per thread");
+    constexpr int TILE_CHUNKS = G::TILE_CHUNKS, LPR = G::LPR, RPI = G::RPI;
+    constexpr int SHIFT_S = G::SHIFT_S, PLANES = G::PLANES;
+    constexpr bool PERM = G::PERM;
     constexpr int NPF = G::NPF, WPF = G::WPF, NWF = G::NWF;
     constexpr int TILE_BYTES = R * R * G::ESZ;
+    constexpr int PLANE = R * PITCH;
 
-    __shared__ __attribute__((aligned(16))) E sA[2][R * PITCH];
-    // b_j as loaded: one raw 16-byte chunk per thread (threads < BCH hold b),
-    // stored unconditionally so the store needs no branch
-    __shared__ __attribute__((aligned(16))) u4 sB[AFF ? 2 : 1][T];
-    __shared__ __attribute__((aligned(16))) float sC[AFF ? 3 : 1][R];
+    __shared__ __attribute__((aligned(16))) L sA[2][PLANES * PLANE];
+    // c_s in a ring of four, indexed (K - s) mod 4
+    __shared__ __attribute__((aligned(16))) float sC[AFF ? 4 : 1][R];
     __shared__ __attribute__((aligned(16))) float sPart[2][NW][R];
 
     const int tid = threadIdx.x;
@@ -279,6 +450,16 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
     const E *A = (const E *)args.A + beta * K * (int64_t)(R * R);
     const E *bv = AFF ? (const E *)args.b + beta * K * (int64_t)R : nullptr;
     float *lam = args.lam + beta * K * (int64_t)R;
+    auto ring = [&](int64_t s) { return (int)((K - s) & 3); };
+
+    // staging lane roles: chunk i of this thread covers tile row
+    // i * RPI + srow, columns scol .. scol + EPC - 1; after the row reduce,
+    // this lane owns the affine sum of row orow (if oown)
+    const int sgi = tid % LPR;
+    const int srow = tid / LPR;
+    const int scol = sgi * EPC;
+    const int orow = (sgi >> SHIFT_S) * RPI + srow;
+    const bool oown = (sgi & ((1 << SHIFT_S) - 1)) == 0 && orow < R;
 
     // ---- staging: HBM -> registers -> LDS -------------------------------------
     // Loads are issued unconditionally (a slot that does not exist gets only
@@ -301,29 +482,83 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
             dst[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, ok ? c * 16 : kOutOfRange, 0, 0);
         }
     };
-    auto store_tile = [&](const u4 (&src)[CPT], int buf) {
-#pragma unroll
-        for (int i = 0; i < CPT; ++i) {
-            const int c = i * T + tid;
-            if (TILE_CHUNKS % T == 0 || c < TILE_CHUNKS) {
-                const int e = c * EPC;
-                *(u4 *)&sA[buf][(e / R) * PITCH + (e % R)] = src[i];
-            }
-        }
-    };
-    auto load_b = [&](u4 &dst, int64_t j, bool valid) {
+    // b_j at the row this lane owns after the staging reduce (raw bits)
+    auto load_b = [&](int64_t j, bool valid) -> uint32_t {
         if constexpr (AFF) {
             const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
                 (void *)(bv + (valid ? j : 0) * (int64_t)R), 0, R * G::ESZ, kBufferWord3);
-            dst = __builtin_amdgcn_raw_buffer_load_b128(
-                rs, (valid && tid < BCH) ? tid * 16 : kOutOfRange, 0, 0);
+            const int off = (valid && oown) ? orow * G::ESZ : kOutOfRange;
+            if constexpr (G::ESZ == 4)
+                return __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0);
+            else
+                return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rs, off, 0, 0) << 16;
+        } else {
+            return 0u;
         }
     };
-    auto store_b = [&](const u4 &src, int buf) {
-        if constexpr (AFF)
-            sB[buf][tid] = src;
+    // Tile j from registers into LDS buffer buf, and (affine) c_j = A_j c_{j+1}
+    // + b_j from the same registers (c_{j+1} = 0 for the first slot).
+    auto stage = [&](const u4 (&src)[CPT], int buf, uint32_t braw, int64_t j, bool first) {
+        float cv[EPC];
+        if constexpr (AFF) {
+#pragma unroll
+            for (int e = 0; e < EPC; e += 4) {
+                const f4 c4 = first ? f4{0.0f, 0.0f, 0.0f, 0.0f}
+                                    : *(const f4 *)&sC[ring(j + 1)][scol + e];
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    cv[e + u] = c4[u];
+            }
+        }
+        float part[CPT];
+#pragma unroll
+        for (int i = 0; i < CPT; ++i) {
+            const int c = i * T + tid;
+            const int row = i * RPI + srow;
+            float x[EPC];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                if constexpr (G::ESZ == 4) {
+                    x[e] = bitsf(src[i][e]);
+                } else {
+                    x[2 * e] = bitsf(src[i][e] << 16);
+                    x[2 * e + 1] = bitsf(src[i][e] & kHighHalf);
+                }
+            }
+            if constexpr (AFF) {
+                float s = x[0] * cv[0];
+#pragma unroll
+                for (int e = 1; e < EPC; ++e)
+                    s += x[e] * cv[e];
+                part[i] = s;
+            }
+            if (TILE_CHUNKS % T == 0 || c < TILE_CHUNKS) {
+                L *dst = &sA[buf][row * PITCH];
+                if constexpr (M == kF32) {
+                    *(u4 *)&dst[scol] = src[i];
+                } else if constexpr (M == kBF16) {
+                    if constexpr (PERM) {
+                        *(u2 *)&dst[lds_col<PERM>(scol)] = u2{src[i][0], src[i][1]};
+                        *(u2 *)&dst[lds_col<PERM>(scol + 4)] = u2{src[i][2], src[i][3]};
+                    } else {
+                        *(u4 *)&dst[scol] = src[i];
+                    }
+                } else {
+                    const Split2 s01 = split_pair(x[0], x[1]);
+                    const Split2 s23 = split_pair(x[2], x[3]);
+                    const int pos = lds_col<PERM>(scol);
+                    *(u2 *)&dst[pos] = u2{s01.h, s23.h};
+                    *(u2 *)&dst[PLANE + pos] = u2{s01.m, s23.m};
+                    *(u2 *)&dst[2 * PLANE + pos] = u2{s01.l, s23.l};
+                }
+            }
+        }
+        if constexpr (AFF) {
+            group_reduce<LPR, CPT>(part, sgi);
+            if (oown)
+                sC[ring(j)][orow] = part[0] + bitsf(braw);
+        }
     };
-    auto b_at = [&](int buf, int m) { return to_f32(((const E *)&sB[buf][0])[m]); };
 
     // ---- per-lane constants ---------------------------------------------------
     float lk[CB];
@@ -344,7 +579,7 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
                     s += P[I][t][v] * lk[t];
                 q[4 * I + v] = s;
             }
-        row_reduce<V>(q, li);
+        group_reduce<16, V>(q, li);
         if ((li & ((1 << SHIFT) - 1)) == 0) {
 #pragma unroll
             for (int e = 0; e < VF; ++e) {
@@ -359,7 +594,7 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
     // get an out-of-range offset, which the buffer store drops; every wave
     // then issues the same memory instructions, which keeps the compiler's
     // count of outstanding loads exact.
-    auto finalize = [&](int64_t s, bool valid, int pbuf, int cring) {
+    auto finalize = [&](int64_t s, bool valid, int pbuf) {
         const int64_t ss = valid ? s : 0;
         const int fw = (int)((uint64_t)ss % NWF);
         const int ft = tid - fw * 64 * WPF;
@@ -370,45 +605,26 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
         for (int ww = 1; ww < NW; ++ww)
             acc += sPart[pbuf][ww][fi];
         if constexpr (AFF)
-            acc += sC[cring][fi];
+            acc += sC[ring(ss)][fi];
         const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
             (void *)(lam + ss * R), 0, R * (int)sizeof(float), kBufferWord3);
         __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc), rs,
                                               mine ? fi * (int)sizeof(float) : kOutOfRange, 0, 0);
     };
-    // ---- c_j = A_j c_{j+1} + b_j ------------------------------------------------
-    auto affine_update = [&](int buf, int cprev, int ccur) {
-        if constexpr (AFF) {
-            const int m = tid / TPR, qq = tid % TPR;
-            const E *arow = &sA[buf][m * PITCH + qq * CPR];
-            const float *cp = &sC[cprev][qq * CPR];
-            float acc = 0.0f;
-#pragma unroll
-            for (int k = 0; k < CPR; ++k)
-                acc += to_f32(arow[k]) * cp[k];
-            acc += dpp<kDppXor1>(acc);
-            if constexpr (TPR == 4)
-                acc += dpp<kDppXor2>(acc);
-            if (qq == 0)
-                sC[ccur][m] = acc + b_at(buf, m);
-        }
-    };
 
     // ---- slot K-1: P = A_{K-1}, c = b_{K-1} -----------------------------------
     u4 pf[NPF][CPT];
-    u4 pfb[NPF];
+    uint32_t pfb[NPF];
     {
         u4 first[CPT];
-        u4 firstb;
-        load_b(firstb, K - 1, true);
+        const uint32_t firstb = load_b(K - 1, true);
         load_tile(first, K - 1, true);
 #pragma unroll
         for (int s = 0; s < NPF; ++s) {
-            load_b(pfb[s], K - 2 - s, K - 2 - s >= 0);
+            pfb[s] = load_b(K - 2 - s, K - 2 - s >= 0);
             load_tile(pf[s], K - 2 - s, K - 2 - s >= 0);
         }
-        store_tile(first, 0);
-        store_b(firstb, 0);
+        stage(first, 0, firstb, K - 1, true);
     }
     __syncthreads();
 
@@ -418,42 +634,42 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
 #pragma unroll
         for (int t = 0; t < CB; ++t)
 #pragma unroll
-            for (int v = 0; v < 4; ++v)
-                P[I][t][v] = to_f32(sA[0][(16 * I + 4 * g + v) * PITCH + 16 * (w + NW * t) + li]);
-    if constexpr (AFF) {
-        if (tid < R)
-            sC[0][tid] = b_at(0, tid);
-    }
+            for (int v = 0; v < 4; ++v) {
+                const int row = 16 * I + 4 * g + v, col = 16 * (w + NW * t) + li;
+                const int pos = row * PITCH + lds_col<PERM>(col & ~3) + (col & 3);
+                if constexpr (M == kF32X)
+                    P[I][t][v] = (to_f32(sA[0][pos]) + to_f32(sA[0][PLANE + pos])) +
+                                 to_f32(sA[0][2 * PLANE + pos]);
+                else
+                    P[I][t][v] = to_f32(sA[0][pos]);
+            }
 
     // ---- slots K-2 .. 0 ---------------------------------------------------------
-    // Iteration j: stage A_j, then [finalize slot j+2 | MFMA P_j = A_j P_{j+1} |
-    // apply slot j+1 | c_j].  Buffers: A, b by slot parity; partials by slot
-    // parity; c in a ring of 3.
+    // Iteration j: stage A_j (and c_j), then [finalize slot j+2 | MFMA
+    // P_j = A_j P_{j+1} | apply slot j+1].  A by slot parity; partials by slot
+    // parity; c in a ring of 4 (c_j overwrites c_{j+4}, whose last reader ran
+    // before the previous iteration's barrier).
     for (int64_t base = K - 2; base >= 0; base -= NPF) {
 #pragma unroll
         for (int s = 0; s < NPF; ++s) {
             const int64_t j = base - s;
             if (j < 0)
                 break;
-            const uint32_t step = (uint32_t)(K - 1 - j);  // slots done before j
-            const int buf = (int)(step & 1);
-            const int cc = (int)(step % 3), cp = (int)((step + 2) % 3), cf = (int)((step + 1) % 3);
-            store_tile(pf[s], buf);
-            store_b(pfb[s], buf);
-            load_b(pfb[s], j - NPF, j - NPF >= 0);
+            const int buf = (int)((uint32_t)(K - 1 - j) & 1);
+            stage(pf[s], buf, pfb[s], j, false);
+            pfb[s] = load_b(j - NPF, j - NPF >= 0);
             load_tile(pf[s], j - NPF, j - NPF >= 0);
             __syncthreads();
-            finalize(j + 2, j + 2 <= K - 1, (int)((j + 2) & 1), cf);
+            finalize(j + 2, j + 2 <= K - 1, (int)((j + 2) & 1));
             f4 Pn[NRB][CB];
             if constexpr (HINT) {
                 const int nr = pow2_at_least(width_blocks(args, j));
                 const int nk = pow2_at_least(width_blocks(args, j + 1));
-                combine_shape<R, DT, NCA>(nr, nk, Pn, P, sA[buf], li, g);
+                combine_shape<R, M, NCA>(nr, nk, Pn, P, sA[buf], li, g);
             } else {
-                combine<R, DT, NCA, NRB, NRB>(Pn, P, sA[buf], li, g);
+                combine<R, M, NCA, NRB, NRB>(Pn, P, sA[buf], li, g);
             }
             apply_partial(P, (int)((j + 1) & 1));
-            affine_update(buf, cp, cc);
 #pragma unroll
             for (int I = 0; I < NRB; ++I)
 #pragma unroll
@@ -465,51 +681,51 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
     __syncthreads();
     apply_partial(P, 0);
     __syncthreads();
-    {
-        // c_0 sits at ring index (K-1) % 3 and c_1 at (K-2) % 3
-        const uint32_t last = (uint32_t)(K - 1);
-        finalize(1, K >= 2, 1, (int)((last + 2) % 3));
-        finalize(0, true, 0, (int)(last % 3));
-    }
+    finalize(1, K >= 2, 1);
+    finalize(0, true, 0);
 }
 
 // ---- host side ------------------------------------------------------------
 
 bool supported_r(int32_t r) { return r == 16 || r == 32 || r == 64 || r == 128; }
 
-template <int R, int DT, bool AFF, bool HINT, int NCA>
+template <int R, int M, bool AFF, bool HINT, int NCA>
 hipError_t launch(const ScanArgs &a, int64_t B, hipStream_t stream)
 {
     void *params[] = {(void *)&a};
-    return hipLaunchKernel((const void *)&scan_chain_kernel<R, DT, AFF, HINT, NCA>,
+    return hipLaunchKernel((const void *)&scan_chain_kernel<R, M, AFF, HINT, NCA>,
                            dim3((unsigned)B), dim3(64 * waves_for(R)), params, 0, stream);
 }
 
-template <int DT, bool AFF, bool HINT>
+template <int M, bool AFF, bool HINT>
 hipError_t dispatch_r(int32_t r, int ncol, const ScanArgs &a, int64_t B, hipStream_t s)
 {
     switch (r) {
-    case 16: return launch<16, DT, AFF, HINT, 1>(a, B, s);
-    case 32: return launch<32, DT, AFF, HINT, 2>(a, B, s);
-    case 64: return launch<64, DT, AFF, HINT, 4>(a, B, s);
-    default:
+    case 16: return launch<16, M, AFF, HINT, 1>(a, B, s);
+    case 32: return launch<32, M, AFF, HINT, 2>(a, B, s);
+    case 64: return launch<64, M, AFF, HINT, 4>(a, B, s);
+    default: {
+        // Three bf16 planes of a 128-wide tile do not fit LDS twice over, so
+        // fp32 at r = 128 multiplies on the fp32 matrix cores.
+        constexpr int M128 = M == kF32X ? kF32 : M;
         // With a hint whose r_K <= 64 only the first four column blocks of P
         // can be nonzero.
         if (HINT && ncol <= 4)
-            return launch<128, DT, AFF, HINT, 4>(a, B, s);
-        return launch<128, DT, AFF, HINT, 8>(a, B, s);
+            return launch<128, M128, AFF, HINT, 4>(a, B, s);
+        return launch<128, M128, AFF, HINT, 8>(a, B, s);
+    }
     }
 }
 
-template <int DT>
+template <int M>
 hipError_t dispatch(bool aff, bool hint, int32_t r, int ncol, const ScanArgs &a, int64_t B,
                     hipStream_t s)
 {
     if (aff)
-        return hint ? dispatch_r<DT, true, true>(r, ncol, a, B, s)
-                    : dispatch_r<DT, true, false>(r, ncol, a, B, s);
-    return hint ? dispatch_r<DT, false, true>(r, ncol, a, B, s)
-                : dispatch_r<DT, false, false>(r, ncol, a, B, s);
+        return hint ? dispatch_r<M, true, true>(r, ncol, a, B, s)
+                    : dispatch_r<M, true, false>(r, ncol, a, B, s);
+    return hint ? dispatch_r<M, false, true>(r, ncol, a, B, s)
+                : dispatch_r<M, false, false>(r, ncol, a, B, s);
 }
 
 bool overlaps(const void *p, size_t pn, const void *q, size_t qn)
@@ -524,9 +740,11 @@ bool misaligned(const void *p) { return p && ((uintptr_t)p & 15u); }
 
 lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam, int64_t B,
                      int64_t K, int32_t r, lbi_dtype dt, void *ws, size_t ws_bytes,
-                     lbi_stream_t stream, const int32_t *widths)
+                     lbi_stream_t stream, const int32_t *widths, lbi_math math)
 {
     if (dt != LBI_F32 && dt != LBI_BF16)
+        return LBI_ERR_DTYPE;
+    if (math != LBI_MATH_DEFAULT && math != LBI_MATH_F32_MFMA && math != LBI_MATH_F32_SPLIT)
         return LBI_ERR_DTYPE;
     if (!supported_r(r))
         return LBI_ERR_UNSUPPORTED_R;
@@ -574,8 +792,14 @@ lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam,
         }
     }
     hipStream_t s = (hipStream_t)stream;
-    const hipError_t e = dt == LBI_F32 ? dispatch<kF32>(b != nullptr, hinted, r, ncol, a, B, s)
-                                       : dispatch<kBF16>(b != nullptr, hinted, r, ncol, a, B, s);
+    const bool aff = b != nullptr;
+    hipError_t e;
+    if (dt == LBI_BF16)
+        e = dispatch<kBF16>(aff, hinted, r, ncol, a, B, s);
+    else if (math == LBI_MATH_F32_MFMA)
+        e = dispatch<kF32>(aff, hinted, r, ncol, a, B, s);
+    else
+        e = dispatch<kF32X>(aff, hinted, r, ncol, a, B, s);
     return e == hipSuccess ? LBI_OK : LBI_ERR_HIP;
 }
 
@@ -597,7 +821,7 @@ lbi_status lbi_scan_backward(const void *A, const void *b, const void *lambda_K,
                              size_t workspace_bytes, lbi_stream_t stream)
 {
     return scan_impl(A, b, lambda_K, lambda, B, K, r, dt, workspace, workspace_bytes, stream,
-                     nullptr);
+                     nullptr, LBI_MATH_DEFAULT);
 }
 
 lbi_status lbi_scan_backward_widths(const void *A, const void *b, const void *lambda_K,
@@ -606,7 +830,16 @@ lbi_status lbi_scan_backward_widths(const void *A, const void *b, const void *la
                                     const int32_t *widths_host)
 {
     return scan_impl(A, b, lambda_K, lambda, B, K, r, dt, workspace, workspace_bytes, stream,
-                     widths_host);
+                     widths_host, LBI_MATH_DEFAULT);
+}
+
+lbi_status lbi_scan_backward_ex(const void *A, const void *b, const void *lambda_K,
+                                float *lambda, int64_t B, int64_t K, int32_t r, lbi_dtype dt,
+                                void *workspace, size_t workspace_bytes, lbi_stream_t stream,
+                                const int32_t *widths_host, lbi_math math)
+{
+    return scan_impl(A, b, lambda_K, lambda, B, K, r, dt, workspace, workspace_bytes, stream,
+                     widths_host, math);
 }
 
 const char *lbi_status_string(lbi_status s)
@@ -615,7 +848,7 @@ const char *lbi_status_string(lbi_status s)
     case LBI_OK: return "LBI_OK";
     case LBI_ERR_NULL: return "LBI_ERR_NULL: a required pointer is NULL";
     case LBI_ERR_SHAPE: return "LBI_ERR_SHAPE: bad B, K, size or widths";
-    case LBI_ERR_DTYPE: return "LBI_ERR_DTYPE: unknown dtype";
+    case LBI_ERR_DTYPE: return "LBI_ERR_DTYPE: unknown dtype or math mode";
     case LBI_ERR_UNSUPPORTED_R: return "LBI_ERR_UNSUPPORTED_R: r must be 16, 32, 64 or 128";
     case LBI_ERR_WORKSPACE: return "LBI_ERR_WORKSPACE: workspace missing or too small";
     case LBI_ERR_HIP: return "LBI_ERR_HIP: the HIP runtime refused the launch";

@@ -29,8 +29,8 @@ def declared_functions():
 def test_header_declares_entry_points():
     names = declared_functions()
     assert names == sorted(["lbi_scan_backward_workspace_bytes", "lbi_scan_backward",
-                            "lbi_scan_backward_widths", "lbi_status_string",
-                            "lbi_abi_version"])
+                            "lbi_scan_backward_widths", "lbi_scan_backward_ex",
+                            "lbi_status_string", "lbi_abi_version"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -52,15 +52,18 @@ def test_header_compiles_as_c():
 
 
 def test_version_and_status_strings():
-    assert binding.lbi_abi_version() == 1
+    assert binding.lbi_abi_version() == 2
     assert binding.lbi_status_string(0) == "LBI_OK"
     for code in range(1, 9):
         assert binding.lbi_status_string(code).startswith("LBI_ERR_")
     assert "unknown" in binding.lbi_status_string(99)
 
 
-def call(A=PA, b=PB, L=PL, out=POUT, B=2, K=3, r=64, dt=0, ws=None, wsb=0, widths=None):
+def call(A=PA, b=PB, L=PL, out=POUT, B=2, K=3, r=64, dt=0, ws=None, wsb=0, widths=None,
+         math=None):
     lib = binding.load()
+    if math is not None:
+        return lib.lbi_scan_backward_ex(A, b, L, out, B, K, r, dt, ws, wsb, None, None, math)
     if widths is None:
         return lib.lbi_scan_backward(A, b, L, out, B, K, r, dt, ws, wsb, None)
     arr = (ctypes.c_int32 * len(widths))(*widths)
@@ -70,6 +73,7 @@ def call(A=PA, b=PB, L=PL, out=POUT, B=2, K=3, r=64, dt=0, ws=None, wsb=0, width
 
 def test_argument_errors():
     assert call(dt=7) == 3                      # LBI_ERR_DTYPE
+    assert call(math=3) == 3 and call(math=-1) == 3 and call(dt=1, math=9) == 3
     for r in (0, 8, 48, 96, 256):
         assert call(r=r) == 4                   # LBI_ERR_UNSUPPORTED_R
     assert call(K=0) == 2 and call(B=-1) == 2   # LBI_ERR_SHAPE

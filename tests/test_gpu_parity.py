@@ -9,6 +9,11 @@ Tolerances (relative Frobenius over the compared output):
     u = 2^-24, so their bound is 8 sqrt(K r) u.
 Integer/permutation inputs, where every intermediate is exact in fp32, must
 match bit for bit.
+
+float32 inputs run under both arithmetic modes of the library: products on the
+fp32 matrix cores (LBI_MATH_F32_MFMA) and products from exact three-part bf16
+splits on the bf16 matrix cores (LBI_MATH_F32_SPLIT, the default); both must
+meet the fp32 tolerance.
 """
 import math
 import sys
@@ -32,12 +37,20 @@ def _say(msg):
     sys.stdout.flush()
 
 
-def run_gpu(x: synth.Inputs, widths=None, stream=None):
+MATH = {"split": binding.LBI_MATH_F32_SPLIT, "mfma": binding.LBI_MATH_F32_MFMA}
+# (storage dtype, float32 arithmetic) pairs every shape test runs under
+MODES = [("f32", "split"), ("f32", "mfma"), ("bf16", None)]
+MODE_IDS = ["f32-split", "f32-mfma", "bf16"]
+
+
+def run_gpu(x: synth.Inputs, widths=None, stream=None, math=None):
     dev = torch.device("cuda:0")
     A = x.A.to(dev)
     b = None if x.b is None else x.b.to(dev)
     lk = x.lamK.to(dev)
-    if widths is None:
+    if math is not None:
+        lam = binding.lbi_scan_backward_ex(A, b, lk, widths, MATH[math], stream=stream)
+    elif widths is None:
         lam = binding.lbi_scan_backward(A, b, lk, stream=stream)
     else:
         lam = binding.lbi_scan_backward_widths(A, b, lk, widths, stream=stream)
@@ -84,6 +97,13 @@ def test_workload_parity_full_size(name):
     x = synth.generate(wl, device="cuda:0")
     hint = wl.widths
     lam = run_gpu(x, widths=hint)
+    if wl.dtype == "f32":
+        # the default arithmetic is the split one; the fp32 matrix cores agree
+        native = run_gpu(x, widths=hint, math="mfma")
+        assert torch.equal(lam, run_gpu(x, widths=hint, math="split"))
+        idx0 = sample_chains(wl.B)
+        assert_close(native[idx0.to(native.device)].cpu().numpy(),
+                     ref(x.to("cpu"), idx0), TOL["f32"], f"{name} fp32 MFMA")
     idx = sample_chains(wl.B)
     xh = x.to("cpu")
     want = ref(xh, idx)
@@ -106,39 +126,41 @@ STRESS = [(B, K, r) for r in (16, 32, 64, 128) for (B, K) in
           ((1, 1), (3, 2), (2, 3), (5, 31), (4, 33), (1, 130))]
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("dtype,arith", MODES, ids=MODE_IDS)
 @pytest.mark.parametrize("B,K,r", STRESS)
-def test_stress_shapes(B, K, r, dtype):
-    _say(f"[stress] B={B} K={K} r={r} {dtype}")
+def test_stress_shapes(B, K, r, dtype, arith):
+    _say(f"[stress] B={B} K={K} r={r} {dtype} {arith}")
     for affine in (True, False):
         x = synth.random_chain(B, K, r, dtype=dtype, seed=K * 7 + r, affine=affine)
-        lam = run_gpu(x)
+        lam = run_gpu(x, math=arith)
         assert_close(lam.cpu().numpy(), ref(x), TOL[dtype] if dtype == "f32" else BF16_EXPECTED,
-                     f"B{B} K{K} r{r} {dtype} affine={affine}")
+                     f"B{B} K{K} r{r} {dtype} {arith} affine={affine}")
 
 
-def test_long_contracting_chain_r16():
+@pytest.mark.parametrize("arith", ["split", "mfma"])
+def test_long_contracting_chain_r16(arith):
     x = synth.random_chain(2, 2049, 16, dtype="f32", seed=3, spectrum="concentrated")
-    _say("[stress] K=2049 r=16 concentrated")
-    assert_close(run_gpu(x).cpu().numpy(), ref(x), TOL["f32"], "K2049")
+    _say(f"[stress] K=2049 r=16 concentrated {arith}")
+    assert_close(run_gpu(x, math=arith).cpu().numpy(), ref(x), TOL["f32"], "K2049")
 
 
 @pytest.mark.parametrize("r", [16, 32, 64, 128])
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_permutation_chains_bit_exact(r, dtype):
-    _say(f"[exact] permutation r={r} {dtype}")
+@pytest.mark.parametrize("dtype,arith", MODES, ids=MODE_IDS)
+def test_permutation_chains_bit_exact(r, dtype, arith):
+    _say(f"[exact] permutation r={r} {dtype} {arith}")
     for K in (1, 7, 40):
         x = synth.permutation_chain(3, K, r, dtype=dtype, seed=K + r)
-        got = run_gpu(x).cpu().numpy().astype(np.float64)
+        got = run_gpu(x, math=arith).cpu().numpy().astype(np.float64)
         assert np.array_equal(got, ref(x)), f"K={K}"
 
 
-def test_orthogonal_long_chain_carries_norm():
+@pytest.mark.parametrize("arith", ["split", "mfma"])
+def test_orthogonal_long_chain_carries_norm(arith):
     """s == 1, b = 0, K = 512: nothing decays, so every slot tests the carry."""
     K, r = 512, 64
-    _say("[stress] orthogonal K=512 r=64")
+    _say(f"[stress] orthogonal K=512 r=64 {arith}")
     x = synth.random_chain(4, K, r, dtype="f32", seed=9, spectrum="orthogonal", affine=False)
-    lam = run_gpu(x).cpu().numpy().astype(np.float64)
+    lam = run_gpu(x, math=arith).cpu().numpy().astype(np.float64)
     tol = 8 * math.sqrt(K * r) * U32
     assert_close(lam, ref(x), tol, "orthogonal K512")
     ratio = np.linalg.norm(lam, axis=-1) / np.linalg.norm(x.lamK.double().numpy(), axis=-1)[:, None]
@@ -158,22 +180,35 @@ def test_null_b_equals_zero_b(dtype):
     assert torch.equal(none, run_gpu(zero))
 
 
-def test_bitwise_deterministic():
+@pytest.mark.parametrize("arith", ["split", "mfma"])
+def test_bitwise_deterministic(arith):
     x = synth.generate(synth.WORKLOADS["paper_width"], device="cuda:0")
-    a = run_gpu(x)
-    b = run_gpu(x)
+    a = run_gpu(x, math=arith)
+    b = run_gpu(x, math=arith)
     assert torch.equal(a, b)
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_widths_hint_matches_unhinted(dtype):
-    widths = synth.cyclic_widths(23)
-    x = synth.random_chain(6, 23, 128, dtype=dtype, seed=2, widths=widths)
-    plain = run_gpu(x)
-    hinted = run_gpu(x, widths=widths)
+def test_split_arithmetic_matches_fp32_matrix_cores():
+    """Both float32 modes sit within a few fp32 roundings of each other."""
+    x = synth.random_chain(16, 64, 64, dtype="f32", seed=11)
+    a = run_gpu(x, math="split").cpu().numpy().astype(np.float64)
+    b = run_gpu(x, math="mfma").cpu().numpy().astype(np.float64)
+    want = ref(x)
+    ea, eb = oracle.rel_frobenius(a, want), oracle.rel_frobenius(b, want)
+    _say(f"  split {ea:.3e}, fp32 MFMA {eb:.3e}")
+    assert ea <= 4 * eb + 1e-7 and eb <= 4 * ea + 1e-7
+
+
+@pytest.mark.parametrize("r", [64, 128])
+@pytest.mark.parametrize("dtype,arith", MODES, ids=MODE_IDS)
+def test_widths_hint_matches_unhinted(dtype, arith, r):
+    widths = synth.cyclic_widths(23, (16, 32, 64) if r == 64 else (32, 64, 128))
+    x = synth.random_chain(6, 23, r, dtype=dtype, seed=2, widths=widths)
+    plain = run_gpu(x, math=arith)
+    hinted = run_gpu(x, widths=widths, math=arith)
     assert torch.equal(plain, hinted)
     for j in range(23):
-        if widths[j] < 128:
+        if widths[j] < r:
             assert float(hinted[:, j, widths[j]:].abs().max()) == 0.0
     assert_close(hinted.cpu().numpy(), ref(x), BF16_EXPECTED if dtype == "bf16" else TOL["f32"],
                  f"hinted {dtype}")
