@@ -32,6 +32,9 @@ def compile_flags():
         f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
         "-Wall", "-Wextra", "-Wno-unused-parameter",
         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+        # MFMA accumulators in ordinary VGPRs: no copies between register
+        # files around the VALU work on the running composite
+        "-mllvm", "-amdgpu-mfma-vgpr-form=1",
         f"-I{INCLUDE}",
     ]
 

@@ -117,9 +117,11 @@ constexpr int kDppXor2 = 0x4E;   // quad_perm [2,3,0,1]
 constexpr int kDppXor7 = 0x141;  // row_half_mirror: lane i <- i ^ 7
 constexpr int kDppXor8 = 0x128;  // row_ror:8:       lane i <- i ^ 8
 
+// (bound_ctrl set, all rows and banks enabled: the compiler can fold the move
+// into the instruction that consumes it)
 template <int CTRL> __device__ __forceinline__ float dpp(float x)
 {
-    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, false));
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, true));
 }
 
 // The value of lane (this lane ^ MASK); MASK 7 stands in for 4 (it flips the
@@ -612,7 +614,9 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
                                               mine ? fi * (int)sizeof(float) : kOutOfRange, 0, 0);
     };
 
-    // ---- slot K-1: P = A_{K-1}, c = b_{K-1} -----------------------------------
+    // ---- slot K-1: P = A_{K-1}, c = b_{K-1}; then stage slot K-2 --------------
+    // Slot x is prefetched into register set (K-1-x) mod NPF and staged into
+    // LDS buffer (K-1-x) mod 2.
     u4 pf[NPF][CPT];
     uint32_t pfb[NPF];
     {
@@ -620,9 +624,9 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
         const uint32_t firstb = load_b(K - 1, true);
         load_tile(first, K - 1, true);
 #pragma unroll
-        for (int s = 0; s < NPF; ++s) {
-            pfb[s] = load_b(K - 2 - s, K - 2 - s >= 0);
-            load_tile(pf[s], K - 2 - s, K - 2 - s >= 0);
+        for (int q = 1; q <= NPF; ++q) {
+            pfb[q % NPF] = load_b(K - 1 - q, K - 1 - q >= 0);
+            load_tile(pf[q % NPF], K - 1 - q, K - 1 - q >= 0);
         }
         stage(first, 0, firstb, K - 1, true);
     }
@@ -643,12 +647,19 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
                 else
                     P[I][t][v] = to_f32(sA[0][pos]);
             }
+    if (K >= 2) {
+        stage(pf[1 % NPF], 1, pfb[1 % NPF], K - 2, false);
+        pfb[1 % NPF] = load_b(K - 2 - NPF, K - 2 - NPF >= 0);
+        load_tile(pf[1 % NPF], K - 2 - NPF, K - 2 - NPF >= 0);
+    }
 
     // ---- slots K-2 .. 0 ---------------------------------------------------------
-    // Iteration j: stage A_j (and c_j), then [finalize slot j+2 | MFMA
-    // P_j = A_j P_{j+1} | apply slot j+1].  A by slot parity; partials by slot
-    // parity; c in a ring of 4 (c_j overwrites c_{j+4}, whose last reader ran
-    // before the previous iteration's barrier).
+    // Iteration j (A_j and c_j staged before its barrier): finalize slot j+2,
+    // then the MFMAs of P_j = A_j P_{j+1} with, in their shadow, the staging
+    // of slot j-1 (into the other LDS buffer; c_{j-1} from c_j) and the apply
+    // of slot j+1.  One barrier per slot: the buffer staged here was last
+    // read by the previous iteration's MFMAs, and c_{j-1} overwrites c_{j+3}
+    // in the ring of four, whose readers all ran before this barrier.
     for (int64_t base = K - 2; base >= 0; base -= NPF) {
 #pragma unroll
         for (int s = 0; s < NPF; ++s) {
@@ -656,9 +667,7 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
             if (j < 0)
                 break;
             const int buf = (int)((uint32_t)(K - 1 - j) & 1);
-            stage(pf[s], buf, pfb[s], j, false);
-            pfb[s] = load_b(j - NPF, j - NPF >= 0);
-            load_tile(pf[s], j - NPF, j - NPF >= 0);
+            const int nx = (s + 2) % NPF;  // register set of slot j-1 (constant once unrolled)
             __syncthreads();
             finalize(j + 2, j + 2 <= K - 1, (int)((j + 2) & 1));
             f4 Pn[NRB][CB];
@@ -669,6 +678,13 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
             } else {
                 combine<R, M, NCA, NRB, NRB>(Pn, P, sA[buf], li, g);
             }
+            // Unconditional, so that the scheduler can spread it between the
+            // MFMAs: at j = 0 it stages the all-zero registers of the
+            // nonexistent slot -1 into a buffer nothing reads again, and its
+            // c lands in ring entry (K + 1) mod 4, which no later reader uses.
+            stage(pf[nx], buf ^ 1, pfb[nx], j - 1, false);
+            pfb[nx] = load_b(j - 1 - NPF, j - 1 - NPF >= 0);
+            load_tile(pf[nx], j - 1 - NPF, j - 1 - NPF >= 0);
             apply_partial(P, (int)((j + 1) & 1));
 #pragma unroll
             for (int I = 0; I < NRB; ++I)
