@@ -249,6 +249,10 @@ def main(argv=None) -> int:
     ap.add_argument("--math", choices=["split", "mfma"], default="split",
                     help="float32 arithmetic: three-part bf16 splits on the bf16 matrix "
                          "cores (the library default) or the fp32 matrix cores")
+    ap.add_argument("--algo", choices=["auto", "chain", "two_level"], default="auto",
+                    help="scan algorithm (auto: the library's choice)")
+    ap.add_argument("--B", type=int, default=0, help="override the workload's chain count")
+    ap.add_argument("--K", type=int, default=0, help="override the workload's slot count")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="also run a plain device copy of this many MiB (for PMC scaling)")
@@ -286,6 +290,12 @@ def main(argv=None) -> int:
               file=sys.stderr)
         return 2
     wl = synth.WORKLOADS[args.workload]
+    if args.B or args.K:
+        if wl.widths is not None:
+            print("--B/--K apply to uniform-width workloads only", file=sys.stderr)
+            return 2
+        wl = wl.with_(B=args.B or wl.B, K=args.K or wl.K, name=f"{wl.name}_B{args.B or wl.B}"
+                      f"_K{args.K or wl.K}")
     dev = torch.device("cuda:0")
     print(f"[bench] generating {wl.name}: B={wl.B} K={wl.K} r={wl.r} {wl.dtype}",
           file=sys.stderr, flush=True)
@@ -303,10 +313,15 @@ def main(argv=None) -> int:
     hint = wl.widths
 
     math = binding.LBI_MATH_F32_SPLIT if args.math == "split" else binding.LBI_MATH_F32_MFMA
+    algo = {"auto": binding.LBI_ALGO_AUTO, "chain": binding.LBI_ALGO_CHAIN,
+            "two_level": binding.LBI_ALGO_TWO_LEVEL}[args.algo]
+    need = binding.lbi_scan_backward_workspace_bytes_ex(wl.B, wl.K, wl.r,
+                                                         0 if wl.dtype == "f32" else 1, algo)
+    ws = torch.empty((need,), dtype=torch.uint8, device=dev) if need else None
 
     def step(i):
         c = copies[i % ncopy]
-        binding.lbi_scan_backward_ex(c.A, c.b, c.lamK, hint, math, lam=lam)
+        binding.lbi_scan_backward_ex(c.A, c.b, c.lamK, hint, math, algo, lam=lam, workspace=ws)
 
     if args.copy_calibration > 0:
         # A plain streaming kernel of known size (torch's elementwise negation:
@@ -376,8 +391,10 @@ def main(argv=None) -> int:
                 "Jacobians; no dataset or checkpoint)",
         "config": {"workload": wl.name, "B": wl.B, "K": wl.K, "r": wl.r,
                    "storage": wl.dtype, "affine": wl.affine, "arithmetic": mode,
+                   "algorithm": args.algo, "workspace_bytes": need,
                    "widths": "cyclic 32/64/128" if wl.widths else "uniform",
-                   "parallelism": "single GPU, one workgroup per chain"},
+                   "parallelism": "1 GPU, " + ("two-level scan (segments in parallel)" if need
+                                               else "one workgroup per chain")},
         "roofline": roof,
         "extra": {
             "alg_tflops": tflops,

@@ -49,7 +49,7 @@ extern "C" {
 /* HIP stream handle (the same type as hipStream_t). */
 typedef struct ihipStream_t *lbi_stream_t;
 
-#define LBI_ABI_VERSION 2
+#define LBI_ABI_VERSION 3
 
 /* Largest K for which a widths hint is used (longer chains run unhinted,
  * which gives identical results). */
@@ -60,36 +60,67 @@ typedef enum {
     LBI_BF16 = 1  /* stored as bfloat16; bf16 MFMA products, fp32 sums      */
 } lbi_dtype;
 
-/* How float32 inputs are multiplied (lbi_scan_backward_ex).  bf16 inputs
- * always use the bf16 matrix cores. */
+/* How float32 inputs are multiplied (lbi_scan_backward_ex,
+ * lbi_scan_suffix_products).  bf16 inputs always use the bf16 matrix cores. */
 typedef enum {
-    LBI_MATH_DEFAULT = 0,   /* the library's choice: LBI_MATH_F32_SPLIT          */
+    LBI_MATH_DEFAULT = 0,   /* the library's choice: LBI_MATH_F32_SPLIT for
+                             * r <= 64, LBI_MATH_F32_MFMA for r = 128           */
     LBI_MATH_F32_MFMA = 1,  /* fp32 products on the fp32 matrix cores            */
     LBI_MATH_F32_SPLIT = 2  /* fp32 products from exact three-part bf16 splits
                              * of both operands on the bf16 matrix cores (the
                              * six partial products down to 2^-16 of the leading
-                             * one), fp32 accumulation                           */
+                             * one), fp32 accumulation; r = 128 falls back to
+                             * LBI_MATH_F32_MFMA                                 */
 } lbi_math;
+
+/* How the slots of a chain are scanned (lbi_scan_backward_ex). */
+typedef enum {
+    LBI_ALGO_AUTO = 0,      /* LBI_ALGO_TWO_LEVEL when the chains are too few to
+                             * fill the GPU (B * waves(r) <= 256, waves = 1, 2,
+                             * 4, 4 for r = 16, 32, 64, 128) and K >= 16, else
+                             * LBI_ALGO_CHAIN                                    */
+    LBI_ALGO_CHAIN = 1,     /* one workgroup folds each whole chain right to
+                             * left (K-1 combines, span K) and applies every
+                             * composite to lambda_K as it forms; no workspace */
+    LBI_ALGO_TWO_LEVEL = 2  /* each chain is cut into S ~ sqrt(8K) segments; a
+                             * workgroup per segment folds it into its local
+                             * composites (kept in the workspace), a carry pass
+                             * applies the segment aggregates right to left to
+                             * lambda_K, and an apply pass forms every
+                             * lambda_j = P_j carry + c_j at once (span K/S
+                             * combines + S matrix-vector products); needs
+                             * workspace, B * K < 2^31                           */
+} lbi_algo;
 
 typedef enum {
     LBI_OK = 0,
     LBI_ERR_NULL = 1,          /* a required pointer is NULL                */
     LBI_ERR_SHAPE = 2,         /* B < 0, K < 1, size overflow, bad widths   */
-    LBI_ERR_DTYPE = 3,         /* dtype not an lbi_dtype, or math not an    *
-                                * lbi_math                                  */
+    LBI_ERR_DTYPE = 3,         /* dtype not an lbi_dtype, math not an       *
+                                * lbi_math, or algo not an lbi_algo         */
     LBI_ERR_UNSUPPORTED_R = 4, /* r not in {16, 32, 64, 128}                */
     LBI_ERR_WORKSPACE = 5,     /* workspace missing or too small            */
     LBI_ERR_HIP = 6,           /* the HIP runtime refused the launch        */
     LBI_ERR_ALIGN = 7,         /* a pointer is not 16-byte aligned          */
-    LBI_ERR_ALIAS = 8          /* lambda overlaps an input                  */
+    LBI_ERR_ALIAS = 8          /* an output (or the workspace) overlaps an  *
+                                * input                                     */
 } lbi_status;
 
 /*
- * Bytes of device workspace that lbi_scan_backward needs for (B, K, r, dt).
- * 0 means the call needs none (workspace may then be NULL).  Returns 0 for
- * arguments the scan would reject.
+ * Bytes of device workspace that lbi_scan_backward (and
+ * lbi_scan_backward_widths) need for (B, K, r, dt): those of the algorithm
+ * LBI_ALGO_AUTO picks.  0 means the call needs none (workspace may then be
+ * NULL).  Returns 0 for arguments the scan would reject.
  */
 size_t lbi_scan_backward_workspace_bytes(int64_t B, int64_t K, int32_t r, lbi_dtype dt);
+
+/*
+ * As lbi_scan_backward_workspace_bytes, for a given algorithm: 0 for
+ * LBI_ALGO_CHAIN; for LBI_ALGO_TWO_LEVEL about 4 B K r (r + 1) bytes (the
+ * segment composites in float32, plus the carries).
+ */
+size_t lbi_scan_backward_workspace_bytes_ex(int64_t B, int64_t K, int32_t r, lbi_dtype dt,
+                                            lbi_algo algo);
 
 /*
  * Every interface adjoint of B independent chains.
@@ -104,7 +135,9 @@ size_t lbi_scan_backward_workspace_bytes(int64_t B, int64_t K, int32_t r, lbi_dt
  *   B >= 0 (B = 0 is a no-op that returns LBI_OK), K >= 1,
  *   r in {16, 32, 64, 128}, dt an lbi_dtype.
  *   workspace / workspace_bytes: device scratch of at least
- *                           lbi_scan_backward_workspace_bytes(B, K, r, dt).
+ *                           lbi_scan_backward_workspace_bytes(B, K, r, dt)
+ *                           bytes, 16-byte aligned, not overlapping any
+ *                           argument; its contents on entry do not matter.
  *   stream: the HIP stream to enqueue on.
  *
  * Precision: LBI_F32 composes and applies in float32 throughout; its matrix
@@ -134,15 +167,38 @@ lbi_status lbi_scan_backward_widths(const void *A, const void *b, const void *la
 
 /*
  * As lbi_scan_backward_widths (widths_host may be NULL), with the arithmetic
- * for float32 inputs chosen by `math`; for LBI_BF16 inputs `math` must still
- * be a valid lbi_math and has no effect.  LBI_MATH_F32_MFMA and
- * LBI_MATH_F32_SPLIT agree to float32 rounding (both accumulate in float32);
- * they are not bitwise equal.
+ * for float32 inputs chosen by `math` and the scan by `algo`; the workspace
+ * must hold lbi_scan_backward_workspace_bytes_ex(B, K, r, dt, algo) bytes.
+ * For LBI_BF16 inputs `math` must still be a valid lbi_math and has no
+ * effect.  All choices agree to float32 rounding (they accumulate in float32
+ * in different orders); they are not bitwise equal to each other.
  */
 lbi_status lbi_scan_backward_ex(const void *A, const void *b, const void *lambda_K,
                                 float *lambda, int64_t B, int64_t K, int32_t r, lbi_dtype dt,
                                 void *workspace, size_t workspace_bytes, lbi_stream_t stream,
-                                const int32_t *widths_host, lbi_math math);
+                                const int32_t *widths_host, lbi_math math, lbi_algo algo);
+
+/*
+ * The suffix composites themselves (Proposition "Scan Formulation of
+ * Backpropagation"; Algorithm "Bounded-Interface Backpropagation", Phase 2,
+ * first step): for every chain and slot j,
+ *
+ *     P_j = A_j A_{j+1} ... A_{K-1},   c_j = A_j c_{j+1} + b_j (c_K = 0),
+ *
+ * so that lambda_j = P_j lambda_K + c_j.  With b absent, P_j is the paper's
+ * suffix product of interface-Jacobian transposes and c_j = 0.
+ *
+ *   A, b, B, K, r, dt, widths_host, math: as for lbi_scan_backward_ex.
+ *   P   [B][K][r][r]  OUTPUT, float32, row-major (P_j has r_j rows and r_K
+ *                     columns of the padded r x r tile; the padding is 0).
+ *   c   [B][K][r]     OUTPUT, float32, or NULL (not written).  Zero when b is
+ *                     NULL.
+ *   P and c must not overlap A, b or each other.  No workspace.  One
+ *   workgroup folds each chain with the combine code of LBI_ALGO_CHAIN.
+ */
+lbi_status lbi_scan_suffix_products(const void *A, const void *b, float *P, float *c, int64_t B,
+                                    int64_t K, int32_t r, lbi_dtype dt, lbi_stream_t stream,
+                                    const int32_t *widths_host, lbi_math math);
 
 /* A static, human-readable name for a status code. */
 const char *lbi_status_string(lbi_status s);

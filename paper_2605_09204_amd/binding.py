@@ -22,6 +22,9 @@ LBI_MAX_HINT_K = 2047
 LBI_MATH_DEFAULT = 0
 LBI_MATH_F32_MFMA = 1
 LBI_MATH_F32_SPLIT = 2
+LBI_ALGO_AUTO = 0
+LBI_ALGO_CHAIN = 1
+LBI_ALGO_TWO_LEVEL = 2
 
 _DTYPES = {torch.float32: LBI_F32, torch.bfloat16: LBI_BF16}
 
@@ -53,14 +56,21 @@ def load() -> ctypes.CDLL:
     vp, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
     lib.lbi_scan_backward_workspace_bytes.argtypes = [i64, i64, i32, ctypes.c_int]
     lib.lbi_scan_backward_workspace_bytes.restype = sz
+    lib.lbi_scan_backward_workspace_bytes_ex.argtypes = [i64, i64, i32, ctypes.c_int,
+                                                         ctypes.c_int]
+    lib.lbi_scan_backward_workspace_bytes_ex.restype = sz
     lib.lbi_scan_backward.argtypes = [vp, vp, vp, vp, i64, i64, i32, ctypes.c_int, vp, sz, vp]
     lib.lbi_scan_backward.restype = ctypes.c_int
     lib.lbi_scan_backward_widths.argtypes = [vp, vp, vp, vp, i64, i64, i32, ctypes.c_int, vp,
                                              sz, vp, ctypes.POINTER(ctypes.c_int32)]
     lib.lbi_scan_backward_widths.restype = ctypes.c_int
     lib.lbi_scan_backward_ex.argtypes = [vp, vp, vp, vp, i64, i64, i32, ctypes.c_int, vp, sz,
-                                         vp, ctypes.POINTER(ctypes.c_int32), ctypes.c_int]
+                                         vp, ctypes.POINTER(ctypes.c_int32), ctypes.c_int,
+                                         ctypes.c_int]
     lib.lbi_scan_backward_ex.restype = ctypes.c_int
+    lib.lbi_scan_suffix_products.argtypes = [vp, vp, vp, vp, i64, i64, i32, ctypes.c_int, vp,
+                                             ctypes.POINTER(ctypes.c_int32), ctypes.c_int]
+    lib.lbi_scan_suffix_products.restype = ctypes.c_int
     lib.lbi_status_string.argtypes = [ctypes.c_int]
     lib.lbi_status_string.restype = ctypes.c_char_p
     lib.lbi_abi_version.argtypes = []
@@ -81,13 +91,25 @@ def lbi_scan_backward_workspace_bytes(B: int, K: int, r: int, dt: int) -> int:
     return int(load().lbi_scan_backward_workspace_bytes(int(B), int(K), int(r), int(dt)))
 
 
+def lbi_scan_backward_workspace_bytes_ex(B: int, K: int, r: int, dt: int, algo: int) -> int:
+    return int(load().lbi_scan_backward_workspace_bytes_ex(int(B), int(K), int(r), int(dt),
+                                                            int(algo)))
+
+
 def _check(status: int) -> None:
     if status != LBI_OK:
         raise LbiError(status, lbi_status_string(status))
 
 
+def _stream_ptr(stream, device):
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
 def _marshal(A: torch.Tensor, b: Optional[torch.Tensor], lambda_K: torch.Tensor,
-             lam: Optional[torch.Tensor], workspace: Optional[torch.Tensor], stream):
+             lam: Optional[torch.Tensor], workspace: Optional[torch.Tensor], stream,
+             algo: int = LBI_ALGO_AUTO):
     if A.dim() != 4 or A.shape[2] != A.shape[3]:
         raise ValueError(f"A must be [B, K, r, r], got {tuple(A.shape)}")
     B, K, r = int(A.shape[0]), int(A.shape[1]), int(A.shape[2])
@@ -109,14 +131,12 @@ def _marshal(A: torch.Tensor, b: Optional[torch.Tensor], lambda_K: torch.Tensor,
     elif tuple(lam.shape) != (B, K, r) or lam.dtype != torch.float32 or not lam.is_contiguous() \
             or lam.device != A.device:
         raise ValueError("lambda must be a contiguous float32 [B, K, r] tensor on A's device")
-    need = lbi_scan_backward_workspace_bytes(B, K, r, dt)
+    need = lbi_scan_backward_workspace_bytes_ex(B, K, r, dt, algo)
     if workspace is None and need > 0:
         workspace = torch.empty((need,), dtype=torch.uint8, device=A.device)
     ws_ptr = workspace.data_ptr() if workspace is not None else None
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
-    if stream is None:
-        stream = torch.cuda.current_stream(A.device)
-    s_ptr = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    s_ptr = _stream_ptr(stream, A.device)
     args = (A.data_ptr(), b.data_ptr() if b is not None else None, lambda_K.data_ptr(),
             lam.data_ptr(), B, K, r, dt, ws_ptr, ws_bytes, s_ptr)
     return lam, args
@@ -154,10 +174,41 @@ def lbi_scan_backward_widths(A: torch.Tensor, b: Optional[torch.Tensor],
 
 def lbi_scan_backward_ex(A: torch.Tensor, b: Optional[torch.Tensor], lambda_K: torch.Tensor,
                          widths: Optional[Sequence[int]] = None, math: int = LBI_MATH_DEFAULT,
-                         lam: Optional[torch.Tensor] = None,
+                         algo: int = LBI_ALGO_AUTO, lam: Optional[torch.Tensor] = None,
                          workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """As lbi_scan_backward_widths, with the float32 arithmetic chosen by ``math``."""
-    lam, args = _marshal(A, b, lambda_K, lam, workspace, stream)
+    """As lbi_scan_backward_widths, with the float32 arithmetic chosen by ``math``
+    and the scan by ``algo``."""
+    lam, args = _marshal(A, b, lambda_K, lam, workspace, stream, algo)
     warr, wptr = _widths_arg(widths, int(A.shape[1]))
-    _check(load().lbi_scan_backward_ex(*args, wptr, int(math)))
+    _check(load().lbi_scan_backward_ex(*args, wptr, int(math), int(algo)))
     return lam
+
+
+def lbi_scan_suffix_products(A: torch.Tensor, b: Optional[torch.Tensor],
+                             widths: Optional[Sequence[int]] = None,
+                             math: int = LBI_MATH_DEFAULT, P: Optional[torch.Tensor] = None,
+                             c: Optional[torch.Tensor] = None, want_c: bool = True,
+                             stream=None):
+    """(P[B, K, r, r], c[B, K, r] or None), float32: the suffix composites."""
+    if A.dim() != 4 or A.shape[2] != A.shape[3] or A.dtype not in _DTYPES or not A.is_cuda:
+        raise ValueError("A must be a [B, K, r, r] float32/bfloat16 GPU tensor")
+    if not A.is_contiguous() or (b is not None and not b.is_contiguous()):
+        raise ValueError("tensors must be contiguous")
+    B, K, r = int(A.shape[0]), int(A.shape[1]), int(A.shape[2])
+    if b is not None and (tuple(b.shape) != (B, K, r) or b.dtype != A.dtype
+                          or b.device != A.device):
+        raise ValueError(f"b must be {(B, K, r)} {A.dtype} on {A.device}")
+    if P is None:
+        P = torch.empty((B, K, r, r), dtype=torch.float32, device=A.device)
+    if want_c and c is None:
+        c = torch.empty((B, K, r), dtype=torch.float32, device=A.device)
+    for name, t, shape in (("P", P, (B, K, r, r)), ("c", c, (B, K, r))):
+        if t is not None and (tuple(t.shape) != shape or t.dtype != torch.float32
+                              or not t.is_contiguous() or t.device != A.device):
+            raise ValueError(f"{name} must be a contiguous float32 {shape} tensor on A's device")
+    warr, wptr = _widths_arg(widths, K)
+    _check(load().lbi_scan_suffix_products(
+        A.data_ptr(), b.data_ptr() if b is not None else None, P.data_ptr(),
+        c.data_ptr() if c is not None else None, B, K, r, _DTYPES[A.dtype],
+        _stream_ptr(stream, A.device), wptr, int(math)))
+    return P, c

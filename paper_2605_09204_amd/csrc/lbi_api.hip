@@ -1,0 +1,308 @@
+// Host side of the LBI scan library: argument validation, the choice between
+// the chain scan and the two-level scan, and the C-ABI of include/lbi.h.
+//
+// Chain scan (one launch): a workgroup folds a whole chain, K-1 combines, and
+// writes every lambda_j.  Span K combines per chain; the B chains run in
+// parallel.  Used when the chains alone fill the GPU.
+//
+// Two-level scan (three launches, workspace): the K slots of each chain are
+// cut into S segments of L slots.  (1) A workgroup per segment folds it into
+// its local suffix composites (K-S combines per chain in all, the same as
+// the chain scan) and writes them to the workspace; (2) the carry pass
+// applies the S segment aggregates right to left to lambda_K (S
+// matrix-vector products per chain) to get lambda at every segment end;
+// (3) the apply pass forms lambda_j = P_j carry + c_j for all slots at once.
+// Span L combines + S matrix-vector products, instead of K combines.  Used
+// when the chains are too few to fill the GPU.
+
+#include <math.h>
+#include <string.h>
+
+#include "lbi_internal.h"
+
+namespace {
+
+using namespace lbi;
+
+bool supported_r(int32_t r) { return r == 16 || r == 32 || r == 64 || r == 128; }
+int waves_for_r(int32_t r) { return r == 16 ? 1 : (r == 32 ? 2 : 4); }
+
+bool overlaps(const void *p, size_t pn, const void *q, size_t qn)
+{
+    if (!p || !q || pn == 0 || qn == 0)
+        return false;
+    const uintptr_t a = (uintptr_t)p, b = (uintptr_t)q;
+    return a < b + qn && b < a + pn;
+}
+
+bool misaligned(const void *p) { return p && ((uintptr_t)p & 15u); }
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Segments of the two-level scan: a segment costs about one chain-kernel slot
+// step per slot and a carry step costs about a tenth of that, so S ~ sqrt(8K)
+// balances the L = K/S fold steps against the S carry steps.
+struct TwoLevelPlan {
+    int64_t L;
+    int32_t S;
+    size_t offP, offc, offcarry, bytes;
+};
+
+TwoLevelPlan two_level_plan(int64_t B, int64_t K, int32_t r)
+{
+    TwoLevelPlan p;
+    int64_t S = (int64_t)ceil(sqrt(8.0 * (double)K));
+    if (S > K)
+        S = K;
+    if (S < 1)
+        S = 1;
+    p.L = (K + S - 1) / S;
+    p.S = (int32_t)((K + p.L - 1) / p.L);
+    const size_t nP = (size_t)B * K * r * r * sizeof(float);
+    const size_t nc = (size_t)B * K * r * sizeof(float);
+    const size_t ncar = (size_t)B * p.S * r * sizeof(float);
+    p.offP = 0;
+    p.offc = align256(nP);
+    p.offcarry = p.offc + align256(nc);
+    p.bytes = p.offcarry + align256(ncar);
+    return p;
+}
+
+// The grid of the apply pass is B*K workgroups.
+bool two_level_possible(int64_t B, int64_t K) { return B * K < ((int64_t)1 << 31) - 1; }
+
+lbi_algo resolve_algo(lbi_algo algo, int64_t B, int64_t K, int32_t r)
+{
+    if (algo == LBI_ALGO_CHAIN || algo == LBI_ALGO_TWO_LEVEL)
+        return algo;
+    // the chains leave most SIMDs idle and are long enough to split
+    if ((int64_t)waves_for_r(r) * B <= 256 && K >= 16 && two_level_possible(B, K))
+        return LBI_ALGO_TWO_LEVEL;
+    return LBI_ALGO_CHAIN;
+}
+
+lbi_status check_common(lbi_dtype dt, lbi_math math, int32_t r, int64_t B, int64_t K)
+{
+    if (dt != LBI_F32 && dt != LBI_BF16)
+        return LBI_ERR_DTYPE;
+    if (math != LBI_MATH_DEFAULT && math != LBI_MATH_F32_MFMA && math != LBI_MATH_F32_SPLIT)
+        return LBI_ERR_DTYPE;
+    if (!supported_r(r))
+        return LBI_ERR_UNSUPPORTED_R;
+    if (B < 0 || K < 1)
+        return LBI_ERR_SHAPE;
+    // sizes must fit comfortably in 64 bits and the launch grid
+    const int64_t kMax = (int64_t)1 << 40;
+    if (B > (int64_t)INT32_MAX || K > kMax / ((int64_t)r * r) || B > kMax / (K * (int64_t)r * r))
+        return LBI_ERR_SHAPE;
+    return LBI_OK;
+}
+
+// Fills the widths code of a launch; false for widths out of range.
+bool encode_widths(const int32_t *widths, int64_t K, int32_t r, ChainLaunch &c)
+{
+    c.hint = false;
+    c.ncol = r / 16;
+    if (!widths)
+        return true;
+    for (int64_t k = 0; k <= K; ++k)
+        if (widths[k] < 1 || widths[k] > r)
+            return false;
+    if (K <= LBI_MAX_HINT_K) {
+        c.hint = true;
+        for (int64_t k = 0; k <= K; ++k) {
+            const uint32_t code = (uint32_t)(widths[k] + 15) / 16;
+            c.args.wcode[k >> 3] |= code << ((k & 7) * 4);
+        }
+        c.ncol = (widths[K] + 15) / 16;
+    }
+    return true;
+}
+
+hipError_t launch_chain_mode(const ChainLaunch &c, lbi_dtype dt, lbi_math math)
+{
+    if (dt == LBI_BF16)
+        return launch_chain_bf16(c);
+    if (math == LBI_MATH_F32_MFMA || c.r == 128)
+        return launch_chain_f32(c);
+    return launch_chain_f32x(c);
+}
+
+lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam, int64_t B,
+                     int64_t K, int32_t r, lbi_dtype dt, void *ws, size_t ws_bytes,
+                     lbi_stream_t stream, const int32_t *widths, lbi_math math, lbi_algo algo)
+{
+    lbi_status st = check_common(dt, math, r, B, K);
+    if (st != LBI_OK)
+        return st;
+    if (algo != LBI_ALGO_AUTO && algo != LBI_ALGO_CHAIN && algo != LBI_ALGO_TWO_LEVEL)
+        return LBI_ERR_DTYPE;
+    if (algo == LBI_ALGO_TWO_LEVEL && !two_level_possible(B, K))
+        return LBI_ERR_SHAPE;
+    if (B == 0)
+        return LBI_OK;
+    if (!A || !lamK || !lam)
+        return LBI_ERR_NULL;
+    if (misaligned(A) || misaligned(b) || misaligned(lamK) || misaligned(lam) || misaligned(ws))
+        return LBI_ERR_ALIGN;
+    const size_t esz = dt == LBI_F32 ? 4 : 2;
+    const size_t nA = (size_t)B * K * r * r * esz, nb = b ? (size_t)B * K * r * esz : 0;
+    const size_t nl = (size_t)B * r * esz, nout = (size_t)B * K * r * sizeof(float);
+    if (overlaps(lam, nout, A, nA) || overlaps(lam, nout, b, nb) || overlaps(lam, nout, lamK, nl))
+        return LBI_ERR_ALIAS;
+    const lbi_algo use = resolve_algo(algo, B, K, r);
+    const size_t need = lbi_scan_backward_workspace_bytes_ex(B, K, r, dt, use);
+    if (need > 0 && (!ws || ws_bytes < need))
+        return LBI_ERR_WORKSPACE;
+    if (need > 0 && (overlaps(ws, need, A, nA) || overlaps(ws, need, b, nb) ||
+                     overlaps(ws, need, lamK, nl) || overlaps(ws, need, lam, nout)))
+        return LBI_ERR_ALIAS;
+
+    ChainLaunch c;
+    memset(&c, 0, sizeof c);
+    c.args.A = A;
+    c.args.b = b;
+    c.args.lamK = lamK;
+    c.args.K = K;
+    c.B = B;
+    c.r = r;
+    c.aff = b != nullptr;
+    c.stream = (hipStream_t)stream;
+    if (!encode_widths(widths, K, r, c))
+        return LBI_ERR_SHAPE;
+
+    if (use == LBI_ALGO_CHAIN) {
+        c.args.lam = lam;
+        c.args.L = K;
+        c.args.S = 1;
+        c.out = kOutLambda;
+        return launch_chain_mode(c, dt, math) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
+    }
+
+    const TwoLevelPlan p = two_level_plan(B, K, r);
+    char *w = (char *)ws;
+    float *Pc = (float *)(w + p.offP);
+    float *cc = b ? (float *)(w + p.offc) : nullptr;
+    float *carry = (float *)(w + p.offcarry);
+    c.args.Pout = Pc;
+    c.args.cout = cc;
+    c.args.L = p.L;
+    c.args.S = p.S;
+    c.out = kOutComposite;
+    c.ncol = r / 16;  // segment composites have the width of their segment's end
+    if (launch_chain_mode(c, dt, math) != hipSuccess)
+        return LBI_ERR_HIP;
+    if (launch_carry(Pc, cc, lamK, dt == LBI_BF16, carry, B, K, p.L, p.S, r, c.stream) !=
+        hipSuccess)
+        return LBI_ERR_HIP;
+    if (launch_apply(Pc, cc, carry, lam, B, K, p.L, p.S, r, c.stream) != hipSuccess)
+        return LBI_ERR_HIP;
+    return LBI_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t lbi_scan_backward_workspace_bytes_ex(int64_t B, int64_t K, int32_t r, lbi_dtype dt,
+                                            lbi_algo algo)
+{
+    if (check_common(dt, LBI_MATH_DEFAULT, r, B, K) != LBI_OK || B == 0)
+        return 0;
+    if (algo != LBI_ALGO_AUTO && algo != LBI_ALGO_CHAIN && algo != LBI_ALGO_TWO_LEVEL)
+        return 0;
+    if (resolve_algo(algo, B, K, r) != LBI_ALGO_TWO_LEVEL || !two_level_possible(B, K))
+        return 0;
+    return two_level_plan(B, K, r).bytes;
+}
+
+size_t lbi_scan_backward_workspace_bytes(int64_t B, int64_t K, int32_t r, lbi_dtype dt)
+{
+    return lbi_scan_backward_workspace_bytes_ex(B, K, r, dt, LBI_ALGO_AUTO);
+}
+
+lbi_status lbi_scan_backward(const void *A, const void *b, const void *lambda_K, float *lambda,
+                             int64_t B, int64_t K, int32_t r, lbi_dtype dt, void *workspace,
+                             size_t workspace_bytes, lbi_stream_t stream)
+{
+    return scan_impl(A, b, lambda_K, lambda, B, K, r, dt, workspace, workspace_bytes, stream,
+                     nullptr, LBI_MATH_DEFAULT, LBI_ALGO_AUTO);
+}
+
+lbi_status lbi_scan_backward_widths(const void *A, const void *b, const void *lambda_K,
+                                    float *lambda, int64_t B, int64_t K, int32_t r, lbi_dtype dt,
+                                    void *workspace, size_t workspace_bytes, lbi_stream_t stream,
+                                    const int32_t *widths_host)
+{
+    return scan_impl(A, b, lambda_K, lambda, B, K, r, dt, workspace, workspace_bytes, stream,
+                     widths_host, LBI_MATH_DEFAULT, LBI_ALGO_AUTO);
+}
+
+lbi_status lbi_scan_backward_ex(const void *A, const void *b, const void *lambda_K,
+                                float *lambda, int64_t B, int64_t K, int32_t r, lbi_dtype dt,
+                                void *workspace, size_t workspace_bytes, lbi_stream_t stream,
+                                const int32_t *widths_host, lbi_math math, lbi_algo algo)
+{
+    return scan_impl(A, b, lambda_K, lambda, B, K, r, dt, workspace, workspace_bytes, stream,
+                     widths_host, math, algo);
+}
+
+lbi_status lbi_scan_suffix_products(const void *A, const void *b, float *P, float *c, int64_t B,
+                                    int64_t K, int32_t r, lbi_dtype dt, lbi_stream_t stream,
+                                    const int32_t *widths_host, lbi_math math)
+{
+    lbi_status st = check_common(dt, math, r, B, K);
+    if (st != LBI_OK)
+        return st;
+    if (B == 0)
+        return LBI_OK;
+    if (!A || !P)
+        return LBI_ERR_NULL;
+    if (misaligned(A) || misaligned(b) || misaligned(P) || misaligned(c))
+        return LBI_ERR_ALIGN;
+    const size_t esz = dt == LBI_F32 ? 4 : 2;
+    const size_t nA = (size_t)B * K * r * r * esz, nb = b ? (size_t)B * K * r * esz : 0;
+    const size_t nP = (size_t)B * K * r * r * sizeof(float);
+    const size_t nc = c ? (size_t)B * K * r * sizeof(float) : 0;
+    if (overlaps(P, nP, A, nA) || overlaps(P, nP, b, nb) || overlaps(c, nc, A, nA) ||
+        overlaps(c, nc, b, nb) || overlaps(c, nc, P, nP))
+        return LBI_ERR_ALIAS;
+    ChainLaunch cl;
+    memset(&cl, 0, sizeof cl);
+    cl.args.A = A;
+    cl.args.b = b;
+    cl.args.Pout = P;
+    cl.args.cout = c;
+    cl.args.K = K;
+    cl.args.L = K;
+    cl.args.S = 1;
+    cl.B = B;
+    cl.r = r;
+    cl.aff = b != nullptr;
+    cl.out = kOutComposite;
+    cl.stream = (hipStream_t)stream;
+    if (!encode_widths(widths_host, K, r, cl))
+        return LBI_ERR_SHAPE;
+    cl.ncol = r / 16;
+    return launch_chain_mode(cl, dt, math) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
+}
+
+const char *lbi_status_string(lbi_status s)
+{
+    switch (s) {
+    case LBI_OK: return "LBI_OK";
+    case LBI_ERR_NULL: return "LBI_ERR_NULL: a required pointer is NULL";
+    case LBI_ERR_SHAPE: return "LBI_ERR_SHAPE: bad B, K, size or widths";
+    case LBI_ERR_DTYPE: return "LBI_ERR_DTYPE: unknown dtype, math mode or algorithm";
+    case LBI_ERR_UNSUPPORTED_R: return "LBI_ERR_UNSUPPORTED_R: r must be 16, 32, 64 or 128";
+    case LBI_ERR_WORKSPACE: return "LBI_ERR_WORKSPACE: workspace missing or too small";
+    case LBI_ERR_HIP: return "LBI_ERR_HIP: the HIP runtime refused the launch";
+    case LBI_ERR_ALIGN: return "LBI_ERR_ALIGN: a pointer is not 16-byte aligned";
+    case LBI_ERR_ALIAS: return "LBI_ERR_ALIAS: an output overlaps an input";
+    }
+    return "unknown lbi_status";
+}
+
+int lbi_abi_version(void) { return LBI_ABI_VERSION; }
+
+}  // extern "C"

@@ -1,0 +1,189 @@
+// Carry and apply passes of the two-level interface-adjoint scan (gfx950).
+//
+// The chain kernel folds each segment of Lseg slots into its local suffix
+// composites (P_j, c_j) = (A_j, b_j) o ... o (A_{e-1}, b_{e-1}), e the
+// segment's end (Proposition "Scan Formulation of Backpropagation": any
+// bracketing of the associative combine gives the same composites).  Then:
+//   carry: lambda at each segment end, right to left, from the segment
+//          aggregates (the composites at each segment's first slot):
+//          lambda_{e_{S-1}} = lambda_K, lambda_{s_d} = P_{s_d} lambda_{e_d} + c_{s_d};
+//   apply: lambda_j = P_j lambda_{e(j)} + c_j for every slot at once
+//          (Phase 2 of Algorithm "Bounded-Interface Backpropagation", with the
+//          segment's carry in place of mbar_K).
+// Both are matrix-vector work on fp32 composites: one 256-thread workgroup
+// per matrix, TPR lanes per row, each lane CPR consecutive columns (16-byte
+// loads), the row sum reduced by DPP within the lane group.
+
+#include "lbi_device.cuh"
+#include "lbi_internal.h"
+
+namespace lbi {
+namespace {
+
+constexpr int kThreads = 256;
+
+template <int R> struct MatVec {
+    static constexpr int TPR = kThreads / R;  // lanes per row
+    static constexpr int CPR = R / TPR;       // columns per lane
+    static_assert(TPR >= 2 && TPR <= 16 && (CPR % 4 == 0 || CPR == 1), "matvec geometry");
+};
+
+// Sum over this lane's columns of p[e] x[col0 + e], then over the row's lanes;
+// every lane of the group ends with the full row sum.
+template <int R>
+__device__ __forceinline__ float row_dot(const float (&p)[MatVec<R>::CPR], const float *x, int col0)
+{
+    constexpr int CPR = MatVec<R>::CPR, TPR = MatVec<R>::TPR;
+    float acc = 0.0f;
+    if constexpr (CPR >= 4) {
+#pragma unroll
+        for (int e = 0; e < CPR; e += 4) {
+            const f4 xv = *(const f4 *)&x[col0 + e];
+            acc += p[e] * xv[0] + p[e + 1] * xv[1] + p[e + 2] * xv[2] + p[e + 3] * xv[3];
+        }
+    } else {
+        acc = p[0] * x[col0];
+    }
+    float q[1] = {acc};
+    group_reduce<TPR, 1>(q, threadIdx.x % TPR);
+    return q[0];
+}
+
+// This lane's CPR columns of one row of a composite (16-byte loads).
+template <int R>
+__device__ __forceinline__ void load_row(float (&p)[MatVec<R>::CPR], const float *Prow)
+{
+    constexpr int CPR = MatVec<R>::CPR;
+    if constexpr (CPR >= 4) {
+#pragma unroll
+        for (int e = 0; e < CPR; e += 4) {
+            const f4 v = *(const f4 *)&Prow[e];
+            p[e] = v[0];
+            p[e + 1] = v[1];
+            p[e + 2] = v[2];
+            p[e + 3] = v[3];
+        }
+    } else {
+        p[0] = Prow[0];
+    }
+}
+
+template <int R, bool BF16>
+__global__ __launch_bounds__(kThreads) void carry_kernel(const float *Pc, const float *cc,
+                                                        const void *lamK, float *carry,
+                                                        int64_t K, int64_t Lseg, int32_t S)
+{
+    constexpr int TPR = MatVec<R>::TPR, CPR = MatVec<R>::CPR;
+    __shared__ __attribute__((aligned(16))) float sl[2][R];
+    const int tid = threadIdx.x;
+    const int64_t beta = blockIdx.x;
+    const int row = tid / TPR, col0 = (tid % TPR) * CPR;
+    const bool owner = tid % TPR == 0;
+    if (tid < R) {
+        const float v = BF16 ? (float)((const __bf16 *)lamK)[beta * R + tid]
+                             : ((const float *)lamK)[beta * R + tid];
+        sl[0][tid] = v;
+        carry[(beta * S + S - 1) * R + tid] = v;
+    }
+    // aggregates of segments d = S-1 .. 1, prefetched one step ahead
+    auto fetch = [&](int32_t d, float (&p)[CPR], float &c) {
+        if (d >= 1) {
+            const int64_t slot = beta * K + (int64_t)d * Lseg;  // first slot of segment d
+            load_row<R>(p, Pc + (slot * R + row) * R + col0);
+            c = cc && owner ? cc[slot * R + row] : 0.0f;
+        }
+    };
+    int cur = 0;
+    auto step = [&](int32_t d, const float (&p)[CPR], float c) {
+        const float sum = row_dot<R>(p, sl[cur], col0);
+        if (owner) {
+            const float v = sum + c;
+            sl[cur ^ 1][row] = v;
+            carry[(beta * S + d - 1) * R + row] = v;
+        }
+        __syncthreads();
+        cur ^= 1;
+    };
+    float p0[CPR], p1[CPR], c0 = 0.0f, c1 = 0.0f;
+    fetch(S - 1, p0, c0);
+    __syncthreads();
+    for (int32_t d = S - 1; d >= 1; d -= 2) {
+        fetch(d - 1, p1, c1);
+        step(d, p0, c0);
+        if (d - 1 >= 1) {
+            fetch(d - 2, p0, c0);
+            step(d - 1, p1, c1);
+        }
+    }
+}
+
+template <int R>
+__global__ __launch_bounds__(kThreads) void apply_kernel(const float *Pc, const float *cc,
+                                                        const float *carry, float *lam,
+                                                        int64_t K, int64_t Lseg, int32_t S)
+{
+    constexpr int TPR = MatVec<R>::TPR, CPR = MatVec<R>::CPR;
+    __shared__ __attribute__((aligned(16))) float sx[R];
+    const int tid = threadIdx.x;
+    const int64_t slot = blockIdx.x;  // global slot beta * K + j
+    const int64_t beta = slot / K, j = slot % K;
+    const int64_t d = j / Lseg;
+    if (tid < R)
+        sx[tid] = carry[(beta * S + d) * R + tid];
+    __syncthreads();
+    const int row = tid / TPR, col0 = (tid % TPR) * CPR;
+    float p[CPR];
+    load_row<R>(p, Pc + (slot * R + row) * R + col0);
+    const float sum = row_dot<R>(p, sx, col0);
+    if (tid % TPR == 0)
+        lam[slot * R + row] = sum + (cc ? cc[slot * R + row] : 0.0f);
+}
+
+template <int R>
+hipError_t carry_r(const float *Pc, const float *cc, const void *lamK, bool bf16, float *carry,
+                   int64_t B, int64_t K, int64_t Lseg, int32_t S, hipStream_t st)
+{
+    if (bf16)
+        hipLaunchKernelGGL((carry_kernel<R, true>), dim3((unsigned)B), dim3(kThreads), 0, st, Pc,
+                           cc, lamK, carry, K, Lseg, S);
+    else
+        hipLaunchKernelGGL((carry_kernel<R, false>), dim3((unsigned)B), dim3(kThreads), 0, st, Pc,
+                           cc, lamK, carry, K, Lseg, S);
+    return hipGetLastError();
+}
+
+template <int R>
+hipError_t apply_r(const float *Pc, const float *cc, const float *carry, float *lam, int64_t B,
+                   int64_t K, int64_t Lseg, int32_t S, hipStream_t st)
+{
+    hipLaunchKernelGGL((apply_kernel<R>), dim3((unsigned)(B * K)), dim3(kThreads), 0, st, Pc, cc,
+                       carry, lam, K, Lseg, S);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_carry(const float *Pc, const float *cc, const void *lamK, bool lamK_bf16,
+                        float *carry, int64_t B, int64_t K, int64_t L, int32_t S, int32_t r,
+                        hipStream_t stream)
+{
+    switch (r) {
+    case 16: return carry_r<16>(Pc, cc, lamK, lamK_bf16, carry, B, K, L, S, stream);
+    case 32: return carry_r<32>(Pc, cc, lamK, lamK_bf16, carry, B, K, L, S, stream);
+    case 64: return carry_r<64>(Pc, cc, lamK, lamK_bf16, carry, B, K, L, S, stream);
+    default: return carry_r<128>(Pc, cc, lamK, lamK_bf16, carry, B, K, L, S, stream);
+    }
+}
+
+hipError_t launch_apply(const float *Pc, const float *cc, const float *carry, float *lam,
+                        int64_t B, int64_t K, int64_t L, int32_t S, int32_t r, hipStream_t stream)
+{
+    switch (r) {
+    case 16: return apply_r<16>(Pc, cc, carry, lam, B, K, L, S, stream);
+    case 32: return apply_r<32>(Pc, cc, carry, lam, B, K, L, S, stream);
+    case 64: return apply_r<64>(Pc, cc, carry, lam, B, K, L, S, stream);
+    default: return apply_r<128>(Pc, cc, carry, lam, B, K, L, S, stream);
+    }
+}
+
+}  // namespace lbi

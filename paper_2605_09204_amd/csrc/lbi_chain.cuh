@@ -1,4 +1,4 @@
-// Interface-adjoint suffix scan of LBI on gfx950 (MI355X).
+// The chain kernel of the LBI interface-adjoint scan on gfx950 (MI355X).
 //
 // Computes, for B independent chains of K slots,
 //     (P_j, c_j) = (A_j, b_j) o (A_{j+1}, b_{j+1}) o ... o (A_{K-1}, b_{K-1}),
@@ -7,9 +7,12 @@
 // formulation (Proposition "Scan Formulation of Backpropagation"; Theorem
 // "Bounded-Interface Backpropagation" gives lambda_j = mbar_j when b = 0), and
 // Phase 2 of Algorithm "Bounded-Interface Backpropagation" (apply the suffix
-// products to mbar_K, every slot).
+// products to mbar_K, every slot).  A workgroup folds one segment of one
+// chain: the whole chain (then it writes every lambda_j), or, in the
+// two-level scan, a segment whose composites it writes for the carry and
+// apply passes.
 //
-// Kernel design (one workgroup per chain, NW waves):
+// Kernel design (one workgroup per chain segment, NW waves):
 //   * The running suffix composite P (R x R, fp32) is split by 16-column
 //     blocks across the waves; wave w keeps column blocks w, w+NW, ... in the
 //     accumulator layout of v_mfma_f32_16x16x*: lane l holds rows
@@ -24,7 +27,8 @@
 //     bytes per lane, branch-free) -> LDS, one barrier per slot.  While a tile
 //     is staged from registers, the same registers give the affine update
 //     c_j = A_j c_{j+1} + b_j (partial dot products reduced across the lanes
-//     that share a row), so A is never re-read for it.
+//     that share a row), so A is never re-read for it.  Slot j-1 is staged
+//     while the MFMAs of slot j run.
 //   * The apply of slot j+1 (P_{j+1} lambda_K: per-wave partial sums reduced
 //     by a DPP butterfly, then across waves through LDS) is issued between
 //     the MFMAs that form P_j, so VALU and matrix-core work overlap;
@@ -46,22 +50,14 @@
 //     runs a shape specialised to the slot's row and k blocks.
 //
 // All HIP code here is built with packed fp32 math disabled.
+#ifndef LBI_CHAIN_CUH
+#define LBI_CHAIN_CUH
 
-#include <hip/hip_runtime.h>
-#include <stdint.h>
-#include <string.h>
+#include "lbi_device.cuh"
+#include "lbi_internal.h"
 
-#include "lbi.h"
-
+namespace lbi {
 namespace {
-
-typedef float f4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-
-enum : int { kF32 = 0, kBF16 = 1, kF32X = 2 };
 
 // E: storage element; L: LDS element of the staged A tile; PLANES: LDS
 // copies of the tile (three bf16 parts for kF32X); PAD: row padding in L.
@@ -82,115 +78,9 @@ template <> struct Mode<kF32X> {
     static constexpr int PLANES = 3, PAD = 8;
 };
 
-constexpr int waves_for(int R) { return R == 16 ? 1 : (R == 32 ? 2 : 4); }
-constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x / 2); }
-
-// Buffer resource word 3 for raw (untyped) buffer loads on gfx9-family GPUs.
-constexpr int kBufferWord3 = 0x00020000;
-// A per-lane offset past every tile: the load returns zero, no memory access.
-constexpr int kOutOfRange = 0x40000000;
-constexpr uint32_t kHighHalf = 0xFFFF0000u;
-
-struct ScanArgs {
-    const void *A;
-    const void *b;
-    const void *lamK;
-    float *lam;
-    int64_t K;
-    // ceil(r_k / 16) for k = 0..K as 4-bit fields, 8 per word (hinted launches)
-    uint32_t wcode[(LBI_MAX_HINT_K + 1 + 7) / 8];
-};
-
 __device__ __forceinline__ int width_blocks(const ScanArgs &a, int64_t k)
 {
     return (int)((a.wcode[k >> 3] >> ((k & 7) * 4)) & 15u);
-}
-
-__device__ __forceinline__ int pow2_at_least(int x)
-{
-    return x <= 1 ? 1 : (x <= 2 ? 2 : (x <= 4 ? 4 : 8));
-}
-
-// DPP lane permutations within a 16-lane row (GFX9 encodings).
-constexpr int kDppXor1 = 0xB1;   // quad_perm [1,0,3,2]
-constexpr int kDppXor2 = 0x4E;   // quad_perm [2,3,0,1]
-constexpr int kDppXor7 = 0x141;  // row_half_mirror: lane i <- i ^ 7
-constexpr int kDppXor8 = 0x128;  // row_ror:8:       lane i <- i ^ 8
-
-// (bound_ctrl set, all rows and banks enabled: the compiler can fold the move
-// into the instruction that consumes it)
-template <int CTRL> __device__ __forceinline__ float dpp(float x)
-{
-    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, true));
-}
-
-// The value of lane (this lane ^ MASK); MASK 7 stands in for 4 (it flips the
-// same top bit of an 8-lane group, and together with 2 and 1 it still spans
-// every lane of the group).
-template <int MASK> __device__ __forceinline__ float xchg(float x)
-{
-    if constexpr (MASK == 1) return dpp<kDppXor1>(x);
-    else if constexpr (MASK == 2) return dpp<kDppXor2>(x);
-    else if constexpr (MASK == 7) return dpp<kDppXor7>(x);
-    else if constexpr (MASK == 8) return dpp<kDppXor8>(x);
-    else {
-        static_assert(MASK == 16, "lane exchange");
-        return __shfl_xor(x, 16);
-    }
-}
-
-// Sum LIVE values per lane over an aligned group of N lanes (gi = lane index
-// in the group).  Each stage either halves the live values (lanes whose bit
-// BIT is 0 keep the lower half, summed with the partner's lower half, the
-// others the upper) or, with one value left, adds the partner's.  Afterwards
-// lane gi holds, in q[e] for e < max(1, LIVE / N), the full group sum of
-// original index (gi >> S) * max(1, LIVE / N) + e with
-// S = log2(N) - log2(min(LIVE, N)).
-template <int N, int LIVE, int V> __device__ __forceinline__ void group_reduce(float (&q)[V], int gi)
-{
-    if constexpr (N > 1) {
-        constexpr int MASK = N == 32 ? 16 : (N == 16 ? 8 : (N == 8 ? 7 : (N == 4 ? 2 : 1)));
-        constexpr int BIT = ilog2(N) - 1;
-        if constexpr (LIVE >= 2) {
-            const bool upper = (gi >> BIT) & 1;
-#pragma unroll
-            for (int i = 0; i < LIVE / 2; ++i) {
-                const float keep = upper ? q[i + LIVE / 2] : q[i];
-                const float send = upper ? q[i] : q[i + LIVE / 2];
-                q[i] = keep + xchg<MASK>(send);
-            }
-            group_reduce<N / 2, LIVE / 2>(q, gi);
-        } else {
-            q[0] += xchg<MASK>(q[0]);
-            group_reduce<N / 2, 1>(q, gi);
-        }
-    }
-}
-
-template <typename T> __device__ __forceinline__ float to_f32(T x) { return (float)x; }
-
-__device__ __forceinline__ uint32_t fbits(float x) { return __float_as_uint(x); }
-__device__ __forceinline__ float bitsf(uint32_t u) { return __uint_as_float(u); }
-
-// Upper halves of two words, packed: the bf16 pair (lo, hi).
-__device__ __forceinline__ uint32_t pack_hi(uint32_t lo, uint32_t hi)
-{
-    return __builtin_amdgcn_perm(hi, lo, 0x07060302u);
-}
-
-// Three bf16 parts of two fp32 values with h + m + l == x exactly (for
-// normal x): h keeps the top 8 significant bits, m the next 8 of the
-// remainder, l the rest, which has at most 8 significant bits.
-struct Split2 {
-    uint32_t h, m, l;
-};
-__device__ __forceinline__ Split2 split_pair(float x0, float x1)
-{
-    const uint32_t h0 = fbits(x0) & kHighHalf, h1 = fbits(x1) & kHighHalf;
-    const float r0 = x0 - bitsf(h0), r1 = x1 - bitsf(h1);
-    const uint32_t m0 = fbits(r0) & kHighHalf, m1 = fbits(r1) & kHighHalf;
-    const float l0 = r0 - bitsf(m0), l1 = r1 - bitsf(m1);
-    return {pack_hi(h0, h1), pack_hi(m0, m1), pack_hi(fbits(l0), fbits(l1))};
 }
 
 // Geometry shared by the kernel and its pieces.
@@ -422,9 +312,10 @@ __device__ __forceinline__ void combine_shape(int nr, int nk, f4 (&Pn)[R / 16][N
     if constexpr (NRB >= 8) combine_k<R, M, NCA, 8>(nk, Pn, P, sAbuf, li, g);
 }
 
-template <int R, int M, bool AFF, bool HINT, int NCA>
+template <int R, int M, bool AFF, bool HINT, int NCA, int OUT>
 __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const ScanArgs args)
 {
+    static_assert(OUT == kOutLambda || NCA == R / 16, "composites are written whole");
     using G = Geo<R, M, NCA>;
     using E = typename G::E;
     using L = typename G::L;
@@ -440,18 +331,26 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
     __shared__ __attribute__((aligned(16))) L sA[2][PLANES * PLANE];
     // c_s in a ring of four, indexed (K - s) mod 4
     __shared__ __attribute__((aligned(16))) float sC[AFF ? 4 : 1][R];
-    __shared__ __attribute__((aligned(16))) float sPart[2][NW][R];
+    __shared__ __attribute__((aligned(16))) float sPart[OUT == kOutLambda ? 2 : 1][NW][R];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int w = tid >> 6;
     const int g = lane >> 4;
     const int li = lane & 15;
-    const int64_t K = args.K;
-    const int64_t beta = blockIdx.x;
-    const E *A = (const E *)args.A + beta * K * (int64_t)(R * R);
-    const E *bv = AFF ? (const E *)args.b + beta * K * (int64_t)R : nullptr;
-    float *lam = args.lam + beta * K * (int64_t)R;
+    // this workgroup's segment: slots s0 .. s0 + K - 1 of chain beta; below,
+    // slot indices are local to the segment
+    const int64_t beta = blockIdx.x / args.S;
+    const int64_t s0 = (int64_t)(blockIdx.x % args.S) * args.L;
+    const int64_t K = args.K - s0 < args.L ? args.K - s0 : args.L;
+    const int64_t first = beta * args.K + s0;  // global index of local slot 0
+    const E *A = (const E *)args.A + first * (int64_t)(R * R);
+    const E *bv = AFF ? (const E *)args.b + first * (int64_t)R : nullptr;
+    float *lam = OUT == kOutLambda ? args.lam + first * (int64_t)R : nullptr;
+    float *Pout = OUT == kOutComposite ? args.Pout + first * (int64_t)(R * R) : nullptr;
+    float *cout = OUT == kOutComposite ? args.cout : nullptr;  // NULL: not written
+    if (cout)
+        cout += first * (int64_t)R;
     auto ring = [&](int64_t s) { return (int)((K - s) & 3); };
 
     // staging lane roles: chunk i of this thread covers tile row
@@ -473,8 +372,8 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
             (void *)(A + jj * (int64_t)(R * R)), 0, TILE_BYTES, kBufferWord3);
         int rows = valid ? R : 0, cols = R;
         if constexpr (HINT) {
-            rows = valid ? 16 * width_blocks(args, jj) : 0;
-            cols = 16 * width_blocks(args, jj + 1);
+            rows = valid ? 16 * width_blocks(args, s0 + jj) : 0;
+            cols = 16 * width_blocks(args, s0 + jj + 1);
         }
 #pragma unroll
         for (int i = 0; i < CPT; ++i) {
@@ -566,7 +465,8 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
     float lk[CB];
 #pragma unroll
     for (int t = 0; t < CB; ++t)
-        lk[t] = to_f32(((const E *)args.lamK)[beta * R + 16 * (w + NW * t) + li]);
+        lk[t] = OUT == kOutLambda ? to_f32(((const E *)args.lamK)[beta * R + 16 * (w + NW * t) + li])
+                                  : 0.0f;
 
     // ---- the apply: partial P lambda_K over this wave's columns ---------------
     auto apply_partial = [&](const f4 (&P)[NRB][CB], int pbuf) {
@@ -612,6 +512,32 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
             (void *)(lam + ss * R), 0, R * (int)sizeof(float), kBufferWord3);
         __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc), rs,
                                               mine ? fi * (int)sizeof(float) : kOutOfRange, 0, 0);
+    };
+    // ---- the composite (P_s, c_s) of local slot s, to global memory -----------
+    // (branch-free buffer stores; each lane writes its rows of its columns)
+    auto store_composite = [&](const f4 (&P)[NRB][CB], int64_t s) {
+        if constexpr (OUT == kOutComposite) {
+            const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                (void *)(Pout + s * (int64_t)(R * R)), 0, R * R * (int)sizeof(float), kBufferWord3);
+#pragma unroll
+            for (int I = 0; I < NRB; ++I)
+#pragma unroll
+                for (int t = 0; t < CB; ++t)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const int row = 16 * I + 4 * g + v, col = 16 * (w + NW * t) + li;
+                        __builtin_amdgcn_raw_buffer_store_b32(fbits(P[I][t][v]), rs,
+                                                              (row * R + col) * (int)sizeof(float), 0, 0);
+                    }
+            if (cout) {
+                // c_s (zero without an affine term)
+                const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
+                    (void *)(cout + s * (int64_t)R), 0, R * (int)sizeof(float), kBufferWord3);
+                const float cv = AFF ? sC[AFF ? ring(s) : 0][tid < R ? tid : 0] : 0.0f;
+                __builtin_amdgcn_raw_buffer_store_b32(
+                    fbits(cv), rc, tid < R ? tid * (int)sizeof(float) : kOutOfRange, 0, 0);
+            }
+        }
     };
 
     // ---- slot K-1: P = A_{K-1}, c = b_{K-1}; then stage slot K-2 --------------
@@ -669,11 +595,12 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
             const int buf = (int)((uint32_t)(K - 1 - j) & 1);
             const int nx = (s + 2) % NPF;  // register set of slot j-1 (constant once unrolled)
             __syncthreads();
-            finalize(j + 2, j + 2 <= K - 1, (int)((j + 2) & 1));
+            if constexpr (OUT == kOutLambda)
+                finalize(j + 2, j + 2 <= K - 1, (int)((j + 2) & 1));
             f4 Pn[NRB][CB];
             if constexpr (HINT) {
-                const int nr = pow2_at_least(width_blocks(args, j));
-                const int nk = pow2_at_least(width_blocks(args, j + 1));
+                const int nr = pow2_at_least(width_blocks(args, s0 + j));
+                const int nk = pow2_at_least(width_blocks(args, s0 + j + 1));
                 combine_shape<R, M, NCA>(nr, nk, Pn, P, sA[buf], li, g);
             } else {
                 combine<R, M, NCA, NRB, NRB>(Pn, P, sA[buf], li, g);
@@ -685,7 +612,10 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
             stage(pf[nx], buf ^ 1, pfb[nx], j - 1, false);
             pfb[nx] = load_b(j - 1 - NPF, j - 1 - NPF >= 0);
             load_tile(pf[nx], j - 1 - NPF, j - 1 - NPF >= 0);
-            apply_partial(P, (int)((j + 1) & 1));
+            if constexpr (OUT == kOutLambda)
+                apply_partial(P, (int)((j + 1) & 1));
+            else
+                store_composite(P, j + 1);
 #pragma unroll
             for (int I = 0; I < NRB; ++I)
 #pragma unroll
@@ -693,187 +623,74 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
                     P[I][t] = Pn[I][t];
         }
     }
-    // slot 0's partials reuse the buffer finalize(2) read in the last iteration
-    __syncthreads();
-    apply_partial(P, 0);
-    __syncthreads();
-    finalize(1, K >= 2, 1);
-    finalize(0, true, 0);
-}
-
-// ---- host side ------------------------------------------------------------
-
-bool supported_r(int32_t r) { return r == 16 || r == 32 || r == 64 || r == 128; }
-
-template <int R, int M, bool AFF, bool HINT, int NCA>
-hipError_t launch(const ScanArgs &a, int64_t B, hipStream_t stream)
-{
-    void *params[] = {(void *)&a};
-    return hipLaunchKernel((const void *)&scan_chain_kernel<R, M, AFF, HINT, NCA>,
-                           dim3((unsigned)B), dim3(64 * waves_for(R)), params, 0, stream);
-}
-
-template <int M, bool AFF, bool HINT>
-hipError_t dispatch_r(int32_t r, int ncol, const ScanArgs &a, int64_t B, hipStream_t s)
-{
-    switch (r) {
-    case 16: return launch<16, M, AFF, HINT, 1>(a, B, s);
-    case 32: return launch<32, M, AFF, HINT, 2>(a, B, s);
-    case 64: return launch<64, M, AFF, HINT, 4>(a, B, s);
-    default: {
-        // Three bf16 planes of a 128-wide tile do not fit LDS twice over, so
-        // fp32 at r = 128 multiplies on the fp32 matrix cores.
-        constexpr int M128 = M == kF32X ? kF32 : M;
-        // With a hint whose r_K <= 64 only the first four column blocks of P
-        // can be nonzero.
-        if (HINT && ncol <= 4)
-            return launch<128, M128, AFF, HINT, 4>(a, B, s);
-        return launch<128, M128, AFF, HINT, 8>(a, B, s);
+    if constexpr (OUT == kOutLambda) {
+        // slot 0's partials reuse the buffer finalize(2) read in the last
+        // iteration
+        __syncthreads();
+        apply_partial(P, 0);
+        __syncthreads();
+        finalize(1, K >= 2, 1);
+        finalize(0, true, 0);
+    } else {
+        // c_0 was staged before the last barrier
+        store_composite(P, 0);
     }
+}
+
+
+// ---- launch -----------------------------------------------------------------
+
+template <int R, int M, bool AFF, bool HINT, int NCA, int OUT>
+hipError_t launch_kernel(const ChainLaunch &c)
+{
+    void *params[] = {(void *)&c.args};
+    const int64_t grid = c.B * c.args.S;
+    return hipLaunchKernel((const void *)&scan_chain_kernel<R, M, AFF, HINT, NCA, OUT>,
+                           dim3((unsigned)grid), dim3(64 * waves_for(R)), params, 0, c.stream);
+}
+
+template <int M, bool AFF, bool HINT, int OUT>
+hipError_t launch_r(const ChainLaunch &c)
+{
+    switch (c.r) {
+    case 16: return launch_kernel<16, M, AFF, HINT, 1, OUT>(c);
+    case 32: return launch_kernel<32, M, AFF, HINT, 2, OUT>(c);
+    case 64: return launch_kernel<64, M, AFF, HINT, 4, OUT>(c);
+    default:
+        if constexpr (M == kF32X) {
+            // three bf16 planes of a 128-wide tile do not fit LDS twice over;
+            // the host sends r = 128 fp32 work to the fp32 matrix cores
+            return hipErrorInvalidValue;
+        } else {
+            // With a hint whose r_K <= 64 only the first four column blocks
+            // of P can be nonzero (lambda output only).
+            if constexpr (OUT == kOutLambda && HINT) {
+                if (c.ncol <= 4)
+                    return launch_kernel<128, M, AFF, HINT, 4, OUT>(c);
+            }
+            return launch_kernel<128, M, AFF, HINT, 8, OUT>(c);
+        }
     }
 }
 
 template <int M>
-hipError_t dispatch(bool aff, bool hint, int32_t r, int ncol, const ScanArgs &a, int64_t B,
-                    hipStream_t s)
+hipError_t launch_chain(const ChainLaunch &c)
 {
-    if (aff)
-        return hint ? dispatch_r<M, true, true>(r, ncol, a, B, s)
-                    : dispatch_r<M, true, false>(r, ncol, a, B, s);
-    return hint ? dispatch_r<M, false, true>(r, ncol, a, B, s)
-                : dispatch_r<M, false, false>(r, ncol, a, B, s);
-}
-
-bool overlaps(const void *p, size_t pn, const void *q, size_t qn)
-{
-    if (!p || !q || pn == 0 || qn == 0)
-        return false;
-    const uintptr_t a = (uintptr_t)p, b = (uintptr_t)q;
-    return a < b + qn && b < a + pn;
-}
-
-bool misaligned(const void *p) { return p && ((uintptr_t)p & 15u); }
-
-lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam, int64_t B,
-                     int64_t K, int32_t r, lbi_dtype dt, void *ws, size_t ws_bytes,
-                     lbi_stream_t stream, const int32_t *widths, lbi_math math)
-{
-    if (dt != LBI_F32 && dt != LBI_BF16)
-        return LBI_ERR_DTYPE;
-    if (math != LBI_MATH_DEFAULT && math != LBI_MATH_F32_MFMA && math != LBI_MATH_F32_SPLIT)
-        return LBI_ERR_DTYPE;
-    if (!supported_r(r))
-        return LBI_ERR_UNSUPPORTED_R;
-    if (B < 0 || K < 1)
-        return LBI_ERR_SHAPE;
-    // sizes must fit comfortably in 64 bits and the launch grid
-    const int64_t kMax = (int64_t)1 << 40;
-    if (B > (int64_t)INT32_MAX || K > kMax / ((int64_t)r * r) || B > kMax / (K * (int64_t)r * r))
-        return LBI_ERR_SHAPE;
-    if (B == 0)
-        return LBI_OK;
-    if (!A || !lamK || !lam)
-        return LBI_ERR_NULL;
-    if (misaligned(A) || misaligned(b) || misaligned(lamK) || misaligned(lam))
-        return LBI_ERR_ALIGN;
-    const size_t esz = dt == LBI_F32 ? 4 : 2;
-    const size_t nA = (size_t)B * K * r * r * esz, nb = b ? (size_t)B * K * r * esz : 0;
-    const size_t nl = (size_t)B * r * esz, nout = (size_t)B * K * r * sizeof(float);
-    if (overlaps(lam, nout, A, nA) || overlaps(lam, nout, b, nb) || overlaps(lam, nout, lamK, nl))
-        return LBI_ERR_ALIAS;
-    const size_t need = lbi_scan_backward_workspace_bytes(B, K, r, dt);
-    if (need > 0 && (!ws || ws_bytes < need))
-        return LBI_ERR_WORKSPACE;
-
-    ScanArgs a;
-    memset(&a, 0, sizeof a);
-    a.A = A;
-    a.b = b;
-    a.lamK = lamK;
-    a.lam = lam;
-    a.K = K;
-    bool hinted = false;
-    int ncol = r / 16;
-    if (widths) {
-        for (int64_t k = 0; k <= K; ++k)
-            if (widths[k] < 1 || widths[k] > r)
-                return LBI_ERR_SHAPE;
-        if (K <= LBI_MAX_HINT_K) {
-            hinted = true;
-            for (int64_t k = 0; k <= K; ++k) {
-                const uint32_t code = (uint32_t)(widths[k] + 15) / 16;
-                a.wcode[k >> 3] |= code << ((k & 7) * 4);
-            }
-            ncol = (widths[K] + 15) / 16;
-        }
+    if (c.out == kOutComposite) {
+        if (c.aff)
+            return c.hint ? launch_r<M, true, true, kOutComposite>(c)
+                          : launch_r<M, true, false, kOutComposite>(c);
+        return c.hint ? launch_r<M, false, true, kOutComposite>(c)
+                      : launch_r<M, false, false, kOutComposite>(c);
     }
-    hipStream_t s = (hipStream_t)stream;
-    const bool aff = b != nullptr;
-    hipError_t e;
-    if (dt == LBI_BF16)
-        e = dispatch<kBF16>(aff, hinted, r, ncol, a, B, s);
-    else if (math == LBI_MATH_F32_MFMA)
-        e = dispatch<kF32>(aff, hinted, r, ncol, a, B, s);
-    else
-        e = dispatch<kF32X>(aff, hinted, r, ncol, a, B, s);
-    return e == hipSuccess ? LBI_OK : LBI_ERR_HIP;
+    if (c.aff)
+        return c.hint ? launch_r<M, true, true, kOutLambda>(c)
+                      : launch_r<M, true, false, kOutLambda>(c);
+    return c.hint ? launch_r<M, false, true, kOutLambda>(c)
+                  : launch_r<M, false, false, kOutLambda>(c);
 }
 
 }  // namespace
+}  // namespace lbi
 
-extern "C" {
-
-size_t lbi_scan_backward_workspace_bytes(int64_t B, int64_t K, int32_t r, lbi_dtype dt)
-{
-    (void)B;
-    (void)K;
-    (void)r;
-    (void)dt;
-    return 0;  // the chain scan keeps its state in registers and LDS
-}
-
-lbi_status lbi_scan_backward(const void *A, const void *b, const void *lambda_K, float *lambda,
-                             int64_t B, int64_t K, int32_t r, lbi_dtype dt, void *workspace,
-                             size_t workspace_bytes, lbi_stream_t stream)
-{
-    return scan_impl(A, b, lambda_K, lambda, B, K, r, dt, workspace, workspace_bytes, stream,
-                     nullptr, LBI_MATH_DEFAULT);
-}
-
-lbi_status lbi_scan_backward_widths(const void *A, const void *b, const void *lambda_K,
-                                    float *lambda, int64_t B, int64_t K, int32_t r, lbi_dtype dt,
-                                    void *workspace, size_t workspace_bytes, lbi_stream_t stream,
-                                    const int32_t *widths_host)
-{
-    return scan_impl(A, b, lambda_K, lambda, B, K, r, dt, workspace, workspace_bytes, stream,
-                     widths_host, LBI_MATH_DEFAULT);
-}
-
-lbi_status lbi_scan_backward_ex(const void *A, const void *b, const void *lambda_K,
-                                float *lambda, int64_t B, int64_t K, int32_t r, lbi_dtype dt,
-                                void *workspace, size_t workspace_bytes, lbi_stream_t stream,
-                                const int32_t *widths_host, lbi_math math)
-{
-    return scan_impl(A, b, lambda_K, lambda, B, K, r, dt, workspace, workspace_bytes, stream,
-                     widths_host, math);
-}
-
-const char *lbi_status_string(lbi_status s)
-{
-    switch (s) {
-    case LBI_OK: return "LBI_OK";
-    case LBI_ERR_NULL: return "LBI_ERR_NULL: a required pointer is NULL";
-    case LBI_ERR_SHAPE: return "LBI_ERR_SHAPE: bad B, K, size or widths";
-    case LBI_ERR_DTYPE: return "LBI_ERR_DTYPE: unknown dtype or math mode";
-    case LBI_ERR_UNSUPPORTED_R: return "LBI_ERR_UNSUPPORTED_R: r must be 16, 32, 64 or 128";
-    case LBI_ERR_WORKSPACE: return "LBI_ERR_WORKSPACE: workspace missing or too small";
-    case LBI_ERR_HIP: return "LBI_ERR_HIP: the HIP runtime refused the launch";
-    case LBI_ERR_ALIGN: return "LBI_ERR_ALIGN: a pointer is not 16-byte aligned";
-    case LBI_ERR_ALIAS: return "LBI_ERR_ALIAS: lambda overlaps an input";
-    }
-    return "unknown lbi_status";
-}
-
-int lbi_abi_version(void) { return LBI_ABI_VERSION; }
-
-}  // extern "C"
+#endif  // LBI_CHAIN_CUH

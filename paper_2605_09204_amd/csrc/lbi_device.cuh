@@ -1,0 +1,118 @@
+// Device helpers shared by the kernels of the LBI scan library: vector
+// types, lane exchanges within a wavefront, group reductions and the exact
+// three-part bf16 split of fp32 values.
+#ifndef LBI_DEVICE_CUH
+#define LBI_DEVICE_CUH
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lbi {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int waves_for(int R) { return R == 16 ? 1 : (R == 32 ? 2 : 4); }
+constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x / 2); }
+
+// Buffer resource word 3 for raw (untyped) buffer loads on gfx9-family GPUs.
+constexpr int kBufferWord3 = 0x00020000;
+// A per-lane offset past every tile: the load returns zero, no memory access.
+constexpr int kOutOfRange = 0x40000000;
+constexpr uint32_t kHighHalf = 0xFFFF0000u;
+
+__device__ __forceinline__ int pow2_at_least(int x)
+{
+    return x <= 1 ? 1 : (x <= 2 ? 2 : (x <= 4 ? 4 : 8));
+}
+
+// DPP lane permutations within a 16-lane row (GFX9 encodings).
+constexpr int kDppXor1 = 0xB1;   // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;   // quad_perm [2,3,0,1]
+constexpr int kDppXor7 = 0x141;  // row_half_mirror: lane i <- i ^ 7
+constexpr int kDppXor8 = 0x128;  // row_ror:8:       lane i <- i ^ 8
+
+// (bound_ctrl set, all rows and banks enabled: the compiler can fold the move
+// into the instruction that consumes it)
+template <int CTRL> __device__ __forceinline__ float dpp(float x)
+{
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, true));
+}
+
+// The value of lane (this lane ^ MASK); MASK 7 stands in for 4 (it flips the
+// same top bit of an 8-lane group, and together with 2 and 1 it still spans
+// every lane of the group).
+template <int MASK> __device__ __forceinline__ float xchg(float x)
+{
+    if constexpr (MASK == 1) return dpp<kDppXor1>(x);
+    else if constexpr (MASK == 2) return dpp<kDppXor2>(x);
+    else if constexpr (MASK == 7) return dpp<kDppXor7>(x);
+    else if constexpr (MASK == 8) return dpp<kDppXor8>(x);
+    else {
+        static_assert(MASK == 16, "lane exchange");
+        return __shfl_xor(x, 16);
+    }
+}
+
+// Sum LIVE values per lane over an aligned group of N lanes (gi = lane index
+// in the group).  Each stage either halves the live values (lanes whose bit
+// BIT is 0 keep the lower half, summed with the partner's lower half, the
+// others the upper) or, with one value left, adds the partner's.  Afterwards
+// lane gi holds, in q[e] for e < max(1, LIVE / N), the full group sum of
+// original index (gi >> S) * max(1, LIVE / N) + e with
+// S = log2(N) - log2(min(LIVE, N)).
+template <int N, int LIVE, int V> __device__ __forceinline__ void group_reduce(float (&q)[V], int gi)
+{
+    if constexpr (N > 1) {
+        constexpr int MASK = N == 32 ? 16 : (N == 16 ? 8 : (N == 8 ? 7 : (N == 4 ? 2 : 1)));
+        constexpr int BIT = ilog2(N) - 1;
+        if constexpr (LIVE >= 2) {
+            const bool upper = (gi >> BIT) & 1;
+#pragma unroll
+            for (int i = 0; i < LIVE / 2; ++i) {
+                const float keep = upper ? q[i + LIVE / 2] : q[i];
+                const float send = upper ? q[i] : q[i + LIVE / 2];
+                q[i] = keep + xchg<MASK>(send);
+            }
+            group_reduce<N / 2, LIVE / 2>(q, gi);
+        } else {
+            q[0] += xchg<MASK>(q[0]);
+            group_reduce<N / 2, 1>(q, gi);
+        }
+    }
+}
+
+template <typename T> __device__ __forceinline__ float to_f32(T x) { return (float)x; }
+
+__device__ __forceinline__ uint32_t fbits(float x) { return __float_as_uint(x); }
+__device__ __forceinline__ float bitsf(uint32_t u) { return __uint_as_float(u); }
+
+// Upper halves of two words, packed: the bf16 pair (lo, hi).
+__device__ __forceinline__ uint32_t pack_hi(uint32_t lo, uint32_t hi)
+{
+    return __builtin_amdgcn_perm(hi, lo, 0x07060302u);
+}
+
+// Three bf16 parts of two fp32 values with h + m + l == x exactly (for
+// normal x): h keeps the top 8 significant bits, m the next 8 of the
+// remainder, l the rest, which has at most 8 significant bits.
+struct Split2 {
+    uint32_t h, m, l;
+};
+__device__ __forceinline__ Split2 split_pair(float x0, float x1)
+{
+    const uint32_t h0 = fbits(x0) & kHighHalf, h1 = fbits(x1) & kHighHalf;
+    const float r0 = x0 - bitsf(h0), r1 = x1 - bitsf(h1);
+    const uint32_t m0 = fbits(r0) & kHighHalf, m1 = fbits(r1) & kHighHalf;
+    const float l0 = r0 - bitsf(m0), l1 = r1 - bitsf(m1);
+    return {pack_hi(h0, h1), pack_hi(m0, m1), pack_hi(fbits(l0), fbits(l1))};
+}
+
+}  // namespace
+}  // namespace lbi
+
+#endif  // LBI_DEVICE_CUH

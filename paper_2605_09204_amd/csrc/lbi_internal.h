@@ -1,0 +1,68 @@
+// Interfaces between the translation units of the LBI scan library (not part
+// of the public C-ABI in include/lbi.h).
+#ifndef LBI_INTERNAL_H
+#define LBI_INTERNAL_H
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "lbi.h"
+
+namespace lbi {
+
+// Arithmetic of the chain kernel: fp32 storage on the fp32 matrix cores; bf16
+// storage on the bf16 matrix cores; fp32 storage as exact three-part bf16
+// splits on the bf16 matrix cores.
+enum : int { kF32 = 0, kBF16 = 1, kF32X = 2 };
+
+// What the chain kernel writes: every adjoint lambda_j, or every suffix
+// composite (P_j, c_j) of its segment.
+enum : int { kOutLambda = 0, kOutComposite = 1 };
+
+struct ScanArgs {
+    const void *A;     // [B][K][R][R] storage dtype
+    const void *b;     // [B][K][R] storage dtype, or NULL
+    const void *lamK;  // [B][R] storage dtype (kOutLambda)
+    float *lam;        // [B][K][R] (kOutLambda)
+    float *Pout;       // [B][K][R][R] (kOutComposite)
+    float *cout;       // [B][K][R] (kOutComposite; NULL: not written)
+    int64_t K;         // slots per chain
+    int64_t L;         // slots per segment; workgroup (beta, d) folds slots
+                       // d*L .. min(K, (d+1)*L) - 1 into composites local to
+                       // the segment (L = K: whole chains)
+    int32_t S;         // segments per chain, ceil(K / L)
+    // ceil(r_k / 16) for k = 0..K as 4-bit fields, 8 per word (hinted launches)
+    uint32_t wcode[(LBI_MAX_HINT_K + 1 + 7) / 8];
+};
+
+struct ChainLaunch {
+    ScanArgs args;
+    int64_t B;       // chains
+    int32_t r;       // tile width R
+    bool aff;        // b present
+    bool hint;       // wcode valid
+    int ncol;        // 16-column blocks of the composite that can be nonzero
+    int out;         // kOutLambda or kOutComposite
+    hipStream_t stream;
+};
+
+// One chain-kernel launch of grid B * S workgroups, arithmetic by file.
+hipError_t launch_chain_f32(const ChainLaunch &c);
+hipError_t launch_chain_f32x(const ChainLaunch &c);
+hipError_t launch_chain_bf16(const ChainLaunch &c);
+
+// Segment carries of the two-level scan: carry[beta][d] is lambda at the end
+// of segment d (lambda_K for the last), obtained by applying the segment
+// aggregates (the composites at each segment's first slot) right to left.
+hipError_t launch_carry(const float *Pc, const float *cc, const void *lamK, bool lamK_bf16,
+                        float *carry, int64_t B, int64_t K, int64_t L, int32_t S, int32_t r,
+                        hipStream_t stream);
+
+// lambda_j = Pc_j carry[segment of j] + cc_j for every slot of every chain.
+hipError_t launch_apply(const float *Pc, const float *cc, const float *carry, float *lam,
+                        int64_t B, int64_t K, int64_t L, int32_t S, int32_t r,
+                        hipStream_t stream);
+
+}  // namespace lbi
+
+#endif  // LBI_INTERNAL_H

@@ -28,9 +28,11 @@ def declared_functions():
 
 def test_header_declares_entry_points():
     names = declared_functions()
-    assert names == sorted(["lbi_scan_backward_workspace_bytes", "lbi_scan_backward",
+    assert names == sorted(["lbi_scan_backward_workspace_bytes",
+                            "lbi_scan_backward_workspace_bytes_ex", "lbi_scan_backward",
                             "lbi_scan_backward_widths", "lbi_scan_backward_ex",
-                            "lbi_status_string", "lbi_abi_version"])
+                            "lbi_scan_suffix_products", "lbi_status_string",
+                            "lbi_abi_version"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -52,7 +54,7 @@ def test_header_compiles_as_c():
 
 
 def test_version_and_status_strings():
-    assert binding.lbi_abi_version() == 2
+    assert binding.lbi_abi_version() == 3
     assert binding.lbi_status_string(0) == "LBI_OK"
     for code in range(1, 9):
         assert binding.lbi_status_string(code).startswith("LBI_ERR_")
@@ -60,10 +62,11 @@ def test_version_and_status_strings():
 
 
 def call(A=PA, b=PB, L=PL, out=POUT, B=2, K=3, r=64, dt=0, ws=None, wsb=0, widths=None,
-         math=None):
+         math=None, algo=0):
     lib = binding.load()
-    if math is not None:
-        return lib.lbi_scan_backward_ex(A, b, L, out, B, K, r, dt, ws, wsb, None, None, math)
+    if math is not None or algo:
+        return lib.lbi_scan_backward_ex(A, b, L, out, B, K, r, dt, ws, wsb, None, None,
+                                        math or 0, algo)
     if widths is None:
         return lib.lbi_scan_backward(A, b, L, out, B, K, r, dt, ws, wsb, None)
     arr = (ctypes.c_int32 * len(widths))(*widths)
@@ -97,4 +100,40 @@ def test_empty_batch_is_a_noop():
 def test_workspace_query():
     for r in (16, 32, 64, 128):
         for dt in (0, 1):
+            # short chains: the chain scan, no workspace
             assert binding.lbi_scan_backward_workspace_bytes(4, 8, r, dt) == 0
+            # many chains: the chain scan fills the GPU by itself
+            assert binding.lbi_scan_backward_workspace_bytes(4096, 512, r, dt) == 0
+            assert binding.lbi_scan_backward_workspace_bytes_ex(4096, 64, r, dt, 1) == 0
+            # few long chains: the two-level scan keeps composites and carries
+            need = binding.lbi_scan_backward_workspace_bytes(2, 512, r, dt)
+            assert need >= 2 * 512 * r * (r + 1) * 4
+            assert binding.lbi_scan_backward_workspace_bytes_ex(2, 512, r, dt, 2) == need
+            assert binding.lbi_scan_backward_workspace_bytes_ex(2, 512, r, dt, 1) == 0
+            assert need <= 2 * 512 * r * (r + 1) * 4 + 2 * 64 * r * 4 + 3 * 256
+    assert binding.lbi_scan_backward_workspace_bytes_ex(2, 512, 64, 0, 7) == 0
+    assert binding.lbi_scan_backward_workspace_bytes(2, 512, 48, 0) == 0
+
+
+def test_two_level_needs_workspace():
+    # the two-level path checks its workspace before touching the GPU
+    assert call(B=2, K=512, algo=2) == 5                 # LBI_ERR_WORKSPACE
+    need = binding.lbi_scan_backward_workspace_bytes_ex(2, 512, 64, 0, 2)
+    assert call(B=2, K=512, algo=2, ws=0x50000000, wsb=need - 1) == 5
+    assert call(B=2, K=512, algo=2, ws=0x50000008, wsb=need) == 7  # misaligned
+    # workspace overlapping an input
+    assert call(B=2, K=512, algo=2, ws=PA + 64, wsb=need) == 8
+    assert call(B=2, K=512, algo=9) == 3
+
+
+def test_suffix_products_argument_errors():
+    lib = binding.load()
+    f = lib.lbi_scan_suffix_products
+    assert f(PA, PB, POUT, PL, 2, 3, 64, 7, None, None, 0) == 3
+    assert f(PA, PB, POUT, PL, 2, 3, 48, 0, None, None, 0) == 4
+    assert f(PA, PB, POUT, PL, 2, 0, 64, 0, None, None, 0) == 2
+    assert f(None, PB, POUT, PL, 2, 3, 64, 0, None, None, 0) == 1
+    assert f(PA, PB, None, PL, 2, 3, 64, 0, None, None, 0) == 1
+    assert f(PA, PB, POUT + 4, PL, 2, 3, 64, 0, None, None, 0) == 7
+    assert f(PA, PB, PA + 64, PL, 2, 3, 64, 0, None, None, 0) == 8
+    assert f(None, None, None, None, 0, 3, 64, 0, None, None, 0) == 0

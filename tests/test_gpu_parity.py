@@ -43,13 +43,18 @@ MODES = [("f32", "split"), ("f32", "mfma"), ("bf16", None)]
 MODE_IDS = ["f32-split", "f32-mfma", "bf16"]
 
 
-def run_gpu(x: synth.Inputs, widths=None, stream=None, math=None):
+ALGO = {"auto": binding.LBI_ALGO_AUTO, "chain": binding.LBI_ALGO_CHAIN,
+        "two_level": binding.LBI_ALGO_TWO_LEVEL}
+
+
+def run_gpu(x: synth.Inputs, widths=None, stream=None, math=None, algo=None):
     dev = torch.device("cuda:0")
     A = x.A.to(dev)
     b = None if x.b is None else x.b.to(dev)
     lk = x.lamK.to(dev)
-    if math is not None:
-        lam = binding.lbi_scan_backward_ex(A, b, lk, widths, MATH[math], stream=stream)
+    if math is not None or algo is not None:
+        lam = binding.lbi_scan_backward_ex(A, b, lk, widths, MATH[math] if math else 0,
+                                           ALGO[algo or "auto"], stream=stream)
     elif widths is None:
         lam = binding.lbi_scan_backward(A, b, lk, stream=stream)
     else:
@@ -126,31 +131,34 @@ STRESS = [(B, K, r) for r in (16, 32, 64, 128) for (B, K) in
           ((1, 1), (3, 2), (2, 3), (5, 31), (4, 33), (1, 130))]
 
 
+@pytest.mark.parametrize("algo", ["chain", "two_level"])
 @pytest.mark.parametrize("dtype,arith", MODES, ids=MODE_IDS)
 @pytest.mark.parametrize("B,K,r", STRESS)
-def test_stress_shapes(B, K, r, dtype, arith):
-    _say(f"[stress] B={B} K={K} r={r} {dtype} {arith}")
+def test_stress_shapes(B, K, r, dtype, arith, algo):
+    _say(f"[stress] B={B} K={K} r={r} {dtype} {arith} {algo}")
     for affine in (True, False):
         x = synth.random_chain(B, K, r, dtype=dtype, seed=K * 7 + r, affine=affine)
-        lam = run_gpu(x, math=arith)
+        lam = run_gpu(x, math=arith, algo=algo)
         assert_close(lam.cpu().numpy(), ref(x), TOL[dtype] if dtype == "f32" else BF16_EXPECTED,
-                     f"B{B} K{K} r{r} {dtype} {arith} affine={affine}")
+                     f"B{B} K{K} r{r} {dtype} {arith} {algo} affine={affine}")
 
 
+@pytest.mark.parametrize("algo", ["chain", "two_level"])
 @pytest.mark.parametrize("arith", ["split", "mfma"])
-def test_long_contracting_chain_r16(arith):
+def test_long_contracting_chain_r16(arith, algo):
     x = synth.random_chain(2, 2049, 16, dtype="f32", seed=3, spectrum="concentrated")
-    _say(f"[stress] K=2049 r=16 concentrated {arith}")
-    assert_close(run_gpu(x, math=arith).cpu().numpy(), ref(x), TOL["f32"], "K2049")
+    _say(f"[stress] K=2049 r=16 concentrated {arith} {algo}")
+    assert_close(run_gpu(x, math=arith, algo=algo).cpu().numpy(), ref(x), TOL["f32"], "K2049")
 
 
+@pytest.mark.parametrize("algo", ["chain", "two_level"])
 @pytest.mark.parametrize("r", [16, 32, 64, 128])
 @pytest.mark.parametrize("dtype,arith", MODES, ids=MODE_IDS)
-def test_permutation_chains_bit_exact(r, dtype, arith):
-    _say(f"[exact] permutation r={r} {dtype} {arith}")
+def test_permutation_chains_bit_exact(r, dtype, arith, algo):
+    _say(f"[exact] permutation r={r} {dtype} {arith} {algo}")
     for K in (1, 7, 40):
         x = synth.permutation_chain(3, K, r, dtype=dtype, seed=K + r)
-        got = run_gpu(x, math=arith).cpu().numpy().astype(np.float64)
+        got = run_gpu(x, math=arith, algo=algo).cpu().numpy().astype(np.float64)
         assert np.array_equal(got, ref(x)), f"K={K}"
 
 
@@ -160,7 +168,7 @@ def test_orthogonal_long_chain_carries_norm(arith):
     K, r = 512, 64
     _say(f"[stress] orthogonal K=512 r=64 {arith}")
     x = synth.random_chain(4, K, r, dtype="f32", seed=9, spectrum="orthogonal", affine=False)
-    lam = run_gpu(x, math=arith).cpu().numpy().astype(np.float64)
+    lam = run_gpu(x, math=arith, algo="chain").cpu().numpy().astype(np.float64)
     tol = 8 * math.sqrt(K * r) * U32
     assert_close(lam, ref(x), tol, "orthogonal K512")
     ratio = np.linalg.norm(lam, axis=-1) / np.linalg.norm(x.lamK.double().numpy(), axis=-1)[:, None]
@@ -171,13 +179,14 @@ def test_orthogonal_long_chain_carries_norm(arith):
 # API behaviour
 # ----------------------------------------------------------------------------
 
+@pytest.mark.parametrize("algo", ["chain", "two_level"])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_null_b_equals_zero_b(dtype):
+def test_null_b_equals_zero_b(dtype, algo):
     x = synth.random_chain(8, 20, 64, dtype=dtype, seed=1, affine=False)
-    none = run_gpu(x)
+    none = run_gpu(x, algo=algo)
     zero = synth.Inputs(x.A, torch.zeros(x.A.shape[:3], dtype=x.A.dtype), x.lamK, x.widths,
                         x.workload)
-    assert torch.equal(none, run_gpu(zero))
+    assert torch.equal(none, run_gpu(zero, algo=algo))
 
 
 @pytest.mark.parametrize("arith", ["split", "mfma"])
@@ -186,6 +195,9 @@ def test_bitwise_deterministic(arith):
     a = run_gpu(x, math=arith)
     b = run_gpu(x, math=arith)
     assert torch.equal(a, b)
+    y = synth.random_chain(3, 300, 64, dtype="f32", seed=7)
+    assert torch.equal(run_gpu(y, math=arith, algo="two_level"),
+                       run_gpu(y, math=arith, algo="two_level"))
 
 
 def test_split_arithmetic_matches_fp32_matrix_cores():
@@ -199,13 +211,14 @@ def test_split_arithmetic_matches_fp32_matrix_cores():
     assert ea <= 4 * eb + 1e-7 and eb <= 4 * ea + 1e-7
 
 
+@pytest.mark.parametrize("algo", ["chain", "two_level"])
 @pytest.mark.parametrize("r", [64, 128])
 @pytest.mark.parametrize("dtype,arith", MODES, ids=MODE_IDS)
-def test_widths_hint_matches_unhinted(dtype, arith, r):
+def test_widths_hint_matches_unhinted(dtype, arith, r, algo):
     widths = synth.cyclic_widths(23, (16, 32, 64) if r == 64 else (32, 64, 128))
     x = synth.random_chain(6, 23, r, dtype=dtype, seed=2, widths=widths)
-    plain = run_gpu(x, math=arith)
-    hinted = run_gpu(x, widths=widths, math=arith)
+    plain = run_gpu(x, math=arith, algo=algo)
+    hinted = run_gpu(x, widths=widths, math=arith, algo=algo)
     assert torch.equal(plain, hinted)
     for j in range(23):
         if widths[j] < r:
@@ -241,3 +254,109 @@ def test_nan_propagates():
     lam = run_gpu(y).cpu()
     assert torch.isnan(lam[1]).all()
     assert torch.isfinite(lam[0]).all()
+
+
+# ----------------------------------------------------------------------------
+# the two-level scan (segments folded in parallel, carries, parallel apply)
+# ----------------------------------------------------------------------------
+
+TWO_LEVEL = [(1, 2, 64), (3, 17, 64), (2, 130, 16), (1, 513, 64), (2, 65, 32), (1, 40, 128)]
+
+
+@pytest.mark.parametrize("dtype,arith", MODES, ids=MODE_IDS)
+@pytest.mark.parametrize("B,K,r", TWO_LEVEL)
+def test_two_level_parity(B, K, r, dtype, arith):
+    _say(f"[two-level] B={B} K={K} r={r} {dtype} {arith}")
+    for affine in (True, False):
+        x = synth.random_chain(B, K, r, dtype=dtype, seed=K * 3 + r, affine=affine,
+                               spectrum="concentrated" if K > 200 else "uniform")
+        lam = run_gpu(x, math=arith, algo="two_level")
+        assert_close(lam.cpu().numpy(), ref(x), TOL[dtype] if dtype == "f32" else BF16_EXPECTED,
+                     f"two-level B{B} K{K} r{r} {dtype} {arith} affine={affine}")
+
+
+@pytest.mark.parametrize("arith", ["split", "mfma"])
+def test_two_level_orthogonal_long_chain(arith):
+    """Nothing decays: every segment's carry and every apply must be right."""
+    K, r = 512, 64
+    _say(f"[two-level] orthogonal K=512 r=64 {arith}")
+    x = synth.random_chain(2, K, r, dtype="f32", seed=19, spectrum="orthogonal", affine=False)
+    lam = run_gpu(x, math=arith, algo="two_level").cpu().numpy().astype(np.float64)
+    assert_close(lam, ref(x), 8 * math.sqrt(K * r) * U32, "two-level orthogonal K512")
+
+
+def test_auto_picks_two_level_for_few_long_chains():
+    x = synth.random_chain(2, 96, 64, dtype="f32", seed=23)
+    auto = run_gpu(x, algo="auto")
+    assert torch.equal(auto, run_gpu(x, algo="two_level"))
+    assert not torch.equal(auto, run_gpu(x, algo="chain"))  # a different bracketing
+    many = synth.random_chain(300, 20, 64, dtype="f32", seed=24)
+    assert torch.equal(run_gpu(many, algo="auto"), run_gpu(many, algo="chain"))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_two_level_widths_hint(dtype):
+    widths = synth.cyclic_widths(70)
+    x = synth.random_chain(2, 70, 128, dtype=dtype, seed=29, widths=widths)
+    plain = run_gpu(x, algo="two_level")
+    hinted = run_gpu(x, widths=widths, algo="two_level")
+    assert torch.equal(plain, hinted)
+    for j in range(70):
+        if widths[j] < 128:
+            assert float(hinted[:, j, widths[j]:].abs().max()) == 0.0
+    assert_close(hinted.cpu().numpy(), ref(x), BF16_EXPECTED if dtype == "bf16" else TOL["f32"],
+                 f"two-level hinted {dtype}")
+
+
+@pytest.mark.parametrize("name", ["tiny", "paper_width", "mixed_widths"])
+def test_two_level_workloads_full_size(name):
+    wl = synth.WORKLOADS[name]
+    _say(f"[two-level] workload {name}")
+    x = synth.generate(wl, device="cuda:0")
+    lam = run_gpu(x, widths=wl.widths, algo="two_level")
+    idx = sample_chains(wl.B)
+    assert_close(lam[idx.to(lam.device)].cpu().numpy(), ref(x.to("cpu"), idx), TOL[wl.dtype],
+                 f"{name} two-level")
+
+
+# ----------------------------------------------------------------------------
+# suffix-composite export
+# ----------------------------------------------------------------------------
+
+def _rel_per_slot(got, want):
+    got = np.asarray(got, dtype=np.float64)
+    d = np.linalg.norm((got - want).reshape(want.shape[0], want.shape[1], -1), axis=-1)
+    n = np.linalg.norm(want.reshape(want.shape[0], want.shape[1], -1), axis=-1)
+    return d / np.maximum(n, 1e-300)
+
+
+@pytest.mark.parametrize("dtype,arith", MODES, ids=MODE_IDS)
+@pytest.mark.parametrize("r", [16, 64, 128])
+def test_suffix_products_match_oracle(r, dtype, arith):
+    _say(f"[export] r={r} {dtype} {arith}")
+    x = synth.random_chain(3, 21, r, dtype=dtype, seed=31 + r)
+    A = x.A.to("cuda:0")
+    b = x.b.to("cuda:0")
+    P, c = binding.lbi_scan_suffix_products(A, b, math=MATH[arith] if arith else 0)
+    torch.cuda.synchronize()
+    Pr, cr = oracle.suffix_composites(x.A, x.b)
+    tol = TOL["f32"] if dtype == "f32" else BF16_EXPECTED
+    assert _rel_per_slot(P.cpu().numpy(), Pr).max() <= tol
+    assert _rel_per_slot(c.cpu().numpy()[..., None], cr[..., None]).max() <= tol
+    # the composites applied to lambda_K give the adjoints (Phase 2)
+    lam = np.einsum("bkij,bj->bki", P.cpu().double().numpy(), x.lamK.double().numpy()) \
+        + c.cpu().double().numpy()
+    assert_close(lam, ref(x), tol, f"export applied r={r} {dtype}")
+    # without b: c is written as zeros, P unchanged
+    P0, c0 = binding.lbi_scan_suffix_products(A, None, math=MATH[arith] if arith else 0)
+    torch.cuda.synchronize()
+    assert torch.equal(P0, P) and float(c0.abs().max()) == 0.0
+
+
+def test_suffix_products_exact_on_permutations():
+    x = synth.permutation_chain(2, 9, 64, dtype="f32", seed=37)
+    P, c = binding.lbi_scan_suffix_products(x.A.to("cuda:0"), x.b.to("cuda:0"))
+    torch.cuda.synchronize()
+    Pr, cr = oracle.suffix_composites(x.A, x.b)
+    assert np.array_equal(P.cpu().numpy().astype(np.float64), Pr)
+    assert np.array_equal(c.cpu().numpy().astype(np.float64), cr)
