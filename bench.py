@@ -34,7 +34,7 @@ import sys
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
-SRC = os.path.join(ROOT, "paper_2605_09204_amd", "csrc", "lbi_scan.hip")
+CSRC = os.path.join(ROOT, "paper_2605_09204_amd", "csrc")
 TRAFFIC_DIR = os.path.join(ROOT, "profiles")
 
 METRIC = "interface combines/sec and achieved MFMA TFLOP/s (r=64, bf16/fp32), % of peak"
@@ -129,8 +129,12 @@ def scan_payload_bytes(K: int, r: int, elem: int) -> int:
 
 
 def source_hash() -> str:
-    with open(SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of every library source (the PMC traffic figures hold for it only)."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
 
 
 def _counter_rows(path):

@@ -75,10 +75,12 @@ typedef enum {
 
 /* How the slots of a chain are scanned (lbi_scan_backward_ex). */
 typedef enum {
-    LBI_ALGO_AUTO = 0,      /* LBI_ALGO_TWO_LEVEL when the chains are too few to
-                             * fill the GPU (B * waves(r) <= 256, waves = 1, 2,
-                             * 4, 4 for r = 16, 32, 64, 128) and K >= 16, else
-                             * LBI_ALGO_CHAIN                                    */
+    LBI_ALGO_AUTO = 0,      /* for K >= 16, the one a cost model fitted to
+                             * MI355X timings predicts faster: the chain scan
+                             * costs K serial slot steps, the two-level scan
+                             * K/S slot steps over B*S workgroups, S carry
+                             * steps and 8 B K r^2 bytes of composite traffic;
+                             * few long chains go two-level.  K < 16: chain     */
     LBI_ALGO_CHAIN = 1,     /* one workgroup folds each whole chain right to
                              * left (K-1 combines, span K) and applies every
                              * composite to lambda_K as it forms; no workspace */

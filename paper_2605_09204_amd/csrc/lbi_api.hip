@@ -71,14 +71,31 @@ TwoLevelPlan two_level_plan(int64_t B, int64_t K, int32_t r)
 // The grid of the apply pass is B*K workgroups.
 bool two_level_possible(int64_t B, int64_t K) { return B * K < ((int64_t)1 << 31) - 1; }
 
-lbi_algo resolve_algo(lbi_algo algo, int64_t B, int64_t K, int32_t r)
+// Microseconds per slot of one chain-kernel workgroup at two or fewer waves
+// per SIMD (measured on MI355X, r = 16, 32, 64, 128).
+double slot_us(lbi_dtype dt, int32_t r)
+{
+    const int i = r == 16 ? 0 : (r == 32 ? 1 : (r == 64 ? 2 : 3));
+    static const double f32[4] = {0.40, 0.70, 1.40, 3.0}, bf16[4] = {0.35, 0.60, 0.88, 3.0};
+    return dt == LBI_BF16 ? bf16[i] : f32[i];
+}
+
+// LBI_ALGO_AUTO: the cheaper of the two by a cost model fitted to MI355X
+// timings.  Chain scan: K serial slot steps (more once the chains exceed two
+// waves per SIMD).  Two-level scan: K/S slot steps over B*S workgroups, S
+// carry steps, and the composites written and read once (8 B K r^2 bytes).
+lbi_algo resolve_algo(lbi_algo algo, int64_t B, int64_t K, int32_t r, lbi_dtype dt)
 {
     if (algo == LBI_ALGO_CHAIN || algo == LBI_ALGO_TWO_LEVEL)
         return algo;
-    // the chains leave most SIMDs idle and are long enough to split
-    if ((int64_t)waves_for_r(r) * B <= 256 && K >= 16 && two_level_possible(B, K))
-        return LBI_ALGO_TWO_LEVEL;
-    return LBI_ALGO_CHAIN;
+    if (K < 16 || !two_level_possible(B, K))
+        return LBI_ALGO_CHAIN;
+    const double ts = slot_us(dt, r), w = waves_for_r(r), simd2 = 2.0 * 1024;
+    const double chain = 8.0 + (double)K * ts * fmax(1.0, (double)B * w / simd2);
+    const TwoLevelPlan p = two_level_plan(B, K, r);
+    const double two = 12.0 + (double)p.L * ts * fmax(1.0, (double)B * p.S * w / simd2) +
+                       0.4 * p.S + 8.0 * (double)B * K * r * r / 4.0e6;
+    return two < chain ? LBI_ALGO_TWO_LEVEL : LBI_ALGO_CHAIN;
 }
 
 lbi_status check_common(lbi_dtype dt, lbi_math math, int32_t r, int64_t B, int64_t K)
@@ -150,7 +167,7 @@ lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam,
     const size_t nl = (size_t)B * r * esz, nout = (size_t)B * K * r * sizeof(float);
     if (overlaps(lam, nout, A, nA) || overlaps(lam, nout, b, nb) || overlaps(lam, nout, lamK, nl))
         return LBI_ERR_ALIAS;
-    const lbi_algo use = resolve_algo(algo, B, K, r);
+    const lbi_algo use = resolve_algo(algo, B, K, r, dt);
     const size_t need = lbi_scan_backward_workspace_bytes_ex(B, K, r, dt, use);
     if (need > 0 && (!ws || ws_bytes < need))
         return LBI_ERR_WORKSPACE;
@@ -211,7 +228,7 @@ size_t lbi_scan_backward_workspace_bytes_ex(int64_t B, int64_t K, int32_t r, lbi
         return 0;
     if (algo != LBI_ALGO_AUTO && algo != LBI_ALGO_CHAIN && algo != LBI_ALGO_TWO_LEVEL)
         return 0;
-    if (resolve_algo(algo, B, K, r) != LBI_ALGO_TWO_LEVEL || !two_level_possible(B, K))
+    if (resolve_algo(algo, B, K, r, dt) != LBI_ALGO_TWO_LEVEL || !two_level_possible(B, K))
         return 0;
     return two_level_plan(B, K, r).bytes;
 }
