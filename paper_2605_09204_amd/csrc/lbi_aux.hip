@@ -12,7 +12,9 @@
 //          segment's carry in place of mbar_K).
 // Both are matrix-vector work on fp32 composites: one 256-thread workgroup
 // per matrix, TPR lanes per row, each lane CPR consecutive columns (16-byte
-// loads), the row sum reduced by DPP within the lane group.
+// loads, coalesced across the row's lanes), the row sum reduced by DPP
+// within the lane group.  The carry walks its S aggregates serially, with
+// the loads of the next two issued ahead.
 
 #include "lbi_device.cuh"
 #include "lbi_internal.h"
@@ -85,8 +87,9 @@ __global__ __launch_bounds__(kThreads) void carry_kernel(const float *Pc, const 
         sl[0][tid] = v;
         carry[(beta * S + S - 1) * R + tid] = v;
     }
-    // aggregates of segments d = S-1 .. 1, prefetched one step ahead
-    auto fetch = [&](int32_t d, float (&p)[CPR], float &c) {
+    // aggregates of segments d = S-1 .. 1, prefetched two steps ahead (the
+    // loads are independent of lambda; only the products wait for it)
+    auto fetch = [&](int32_t d, float(&p)[CPR], float &c) {
         if (d >= 1) {
             const int64_t slot = beta * K + (int64_t)d * Lseg;  // first slot of segment d
             load_row<R>(p, Pc + (slot * R + row) * R + col0);
@@ -94,7 +97,7 @@ __global__ __launch_bounds__(kThreads) void carry_kernel(const float *Pc, const 
         }
     };
     int cur = 0;
-    auto step = [&](int32_t d, const float (&p)[CPR], float c) {
+    auto step = [&](int32_t d, const float(&p)[CPR], float c) {
         const float sum = row_dot<R>(p, sl[cur], col0);
         if (owner) {
             const float v = sum + c;
@@ -104,15 +107,20 @@ __global__ __launch_bounds__(kThreads) void carry_kernel(const float *Pc, const 
         __syncthreads();
         cur ^= 1;
     };
-    float p0[CPR], p1[CPR], c0 = 0.0f, c1 = 0.0f;
+    float p0[CPR], p1[CPR], p2[CPR], c0 = 0.0f, c1 = 0.0f, c2 = 0.0f;
     fetch(S - 1, p0, c0);
+    fetch(S - 2, p1, c1);
     __syncthreads();
-    for (int32_t d = S - 1; d >= 1; d -= 2) {
-        fetch(d - 1, p1, c1);
+    for (int32_t d = S - 1; d >= 1; d -= 3) {
+        fetch(d - 2, p2, c2);
         step(d, p0, c0);
         if (d - 1 >= 1) {
-            fetch(d - 2, p0, c0);
+            fetch(d - 3, p0, c0);
             step(d - 1, p1, c1);
+        }
+        if (d - 2 >= 1) {
+            fetch(d - 4, p1, c1);
+            step(d - 2, p2, c2);
         }
     }
 }

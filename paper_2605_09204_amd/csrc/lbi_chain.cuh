@@ -53,6 +53,8 @@
 #ifndef LBI_CHAIN_CUH
 #define LBI_CHAIN_CUH
 
+#include <type_traits>
+
 #include "lbi_device.cuh"
 #include "lbi_internal.h"
 
@@ -89,9 +91,6 @@ template <int R, int M, int NCA> struct Geo {
     static constexpr int T = 64 * NW;
     static constexpr int NRB = R / 16;    // 16-row blocks
     static constexpr int CB = NCA / NW;   // column blocks per wave
-    static constexpr int V = 4 * NRB;     // values per lane in the apply
-    static constexpr int VF = V >= 16 ? V / 16 : 1;
-    static constexpr int SHIFT = V >= 16 ? 0 : (V == 8 ? 1 : 2);
     using E = typename Mode<M>::E;
     using L = typename Mode<M>::L;
     static constexpr int PLANES = Mode<M>::PLANES;
@@ -185,16 +184,24 @@ __device__ __forceinline__ void combine(f4 (&Pn)[R / 16][NCA / waves_for(R)],
                     x[t][v + 4] = kPairs ? P[kPairs ? 2 * p + 1 : 0][t][v] : 0.0f;
                 }
             if constexpr (M == kBF16) {
-                // P = hi + lo (RNE hi, exact remainder, RNE lo)
+                // P = hi + lo (RNE hi, exact remainder, RNE lo), converted
+                // two values per instruction
                 bf16x8 bh[CB], bl[CB];
 #pragma unroll
-                for (int t = 0; t < CB; ++t)
+                for (int t = 0; t < CB; ++t) {
+                    u4 hh, ll;
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const __bf16 h = (__bf16)x[t][e];
-                        bh[t][e] = h;
-                        bl[t][e] = (__bf16)(x[t][e] - (float)h);
+                    for (int e = 0; e < 4; ++e) {
+                        const uint32_t hu = __builtin_bit_cast(
+                            uint32_t, __builtin_convertvector(f2{x[t][2 * e], x[t][2 * e + 1]}, bf16x2));
+                        const f2 rest = {x[t][2 * e] - bitsf(hu << 16),
+                                         x[t][2 * e + 1] - bitsf(hu & kHighHalf)};
+                        hh[e] = hu;
+                        ll[e] = __builtin_bit_cast(uint32_t, __builtin_convertvector(rest, bf16x2));
                     }
+                    bh[t] = __builtin_bit_cast(bf16x8, hh);
+                    bl[t] = __builtin_bit_cast(bf16x8, ll);
+                }
 #pragma unroll
                 for (int I = 0; I < NR; ++I) {
                     const bf16x8 a = a_operand<R, PITCH>(sAbuf, I, p, li, g);
@@ -319,8 +326,8 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
     using G = Geo<R, M, NCA>;
     using E = typename G::E;
     using L = typename G::L;
-    constexpr int NW = G::NW, T = G::T, NRB = G::NRB, CB = G::CB, V = G::V, VF = G::VF;
-    constexpr int SHIFT = G::SHIFT, PITCH = G::PITCH, EPC = G::EPC, CPT = G::CPT;
+    constexpr int NW = G::NW, T = G::T, NRB = G::NRB, CB = G::CB;
+    constexpr int PITCH = G::PITCH, EPC = G::EPC, CPT = G::CPT;
     constexpr int TILE_CHUNKS = G::TILE_CHUNKS, LPR = G::LPR, RPI = G::RPI;
     constexpr int SHIFT_S = G::SHIFT_S, PLANES = G::PLANES;
     constexpr bool PERM = G::PERM;
@@ -352,6 +359,13 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
     if (cout)
         cout += first * (int64_t)R;
     auto ring = [&](int64_t s) { return (int)((K - s) & 3); };
+    // rows of slot s that can be nonzero, rounded up to 16 x a power of two
+    auto live_rows = [&](int64_t s) {
+        if constexpr (HINT)
+            return s >= 0 && s < K ? 16 * pow2_at_least(width_blocks(args, s0 + s)) : 0;
+        else
+            return R;
+    };
 
     // staging lane roles: chunk i of this thread covers tile row
     // i * RPI + srow, columns scol .. scol + EPC - 1; after the row reduce,
@@ -427,10 +441,14 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
                 }
             }
             if constexpr (AFF) {
-                float s = x[0] * cv[0];
+                // with a widths hint, chunk rows at or past r_j are all zero
+                float s = 0.0f;
+                if (!HINT || i * RPI < live_rows(j)) {
+                    s = x[0] * cv[0];
 #pragma unroll
-                for (int e = 1; e < EPC; ++e)
-                    s += x[e] * cv[e];
+                    for (int e = 1; e < EPC; ++e)
+                        s += x[e] * cv[e];
+                }
                 part[i] = s;
             }
             if (TILE_CHUNKS % T == 0 || c < TILE_CHUNKS) {
@@ -469,10 +487,15 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
                                   : 0.0f;
 
     // ---- the apply: partial P lambda_K over this wave's columns ---------------
-    auto apply_partial = [&](const f4 (&P)[NRB][CB], int pbuf) {
-        float q[V];
+    // (NB row blocks; with a widths hint, only the blocks slot s can fill)
+    auto apply_rows = [&](const f4(&P)[NRB][CB], int pbuf, auto nb_tag) {
+        constexpr int NB = decltype(nb_tag)::value;
+        constexpr int VV = 4 * NB;
+        constexpr int VFF = VV >= 16 ? VV / 16 : 1;
+        constexpr int SH = VV >= 16 ? 0 : (VV == 8 ? 1 : 2);
+        float q[VV];
 #pragma unroll
-        for (int I = 0; I < NRB; ++I)
+        for (int I = 0; I < NB; ++I)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 float s = P[I][0][v] * lk[0];
@@ -481,14 +504,37 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
                     s += P[I][t][v] * lk[t];
                 q[4 * I + v] = s;
             }
-        group_reduce<16, V>(q, li);
-        if ((li & ((1 << SHIFT) - 1)) == 0) {
+        group_reduce<16, VV>(q, li);
+        if ((li & ((1 << SH) - 1)) == 0) {
 #pragma unroll
-            for (int e = 0; e < VF; ++e) {
-                const int idx = (li >> SHIFT) * VF + e;  // = 4*I + v
+            for (int e = 0; e < VFF; ++e) {
+                const int idx = (li >> SH) * VFF + e;  // = 4*I + v
                 const int row = 16 * (idx >> 2) + 4 * g + (idx & 3);
                 sPart[pbuf][w][row] = q[e];
             }
+        }
+    };
+    auto apply_partial = [&](const f4(&P)[NRB][CB], int pbuf, int64_t s) {
+        if constexpr (HINT) {
+            const int nb = live_rows(s) / 16;
+            if (nb <= 1 || NRB == 1) {
+                apply_rows(P, pbuf, std::integral_constant<int, 1>{});
+                return;
+            }
+            if constexpr (NRB >= 2)
+                if (nb <= 2) {
+                    apply_rows(P, pbuf, std::integral_constant<int, 2>{});
+                    return;
+                }
+            if constexpr (NRB >= 4)
+                if (nb <= 4) {
+                    apply_rows(P, pbuf, std::integral_constant<int, 4>{});
+                    return;
+                }
+            if constexpr (NRB >= 8)
+                apply_rows(P, pbuf, std::integral_constant<int, 8>{});
+        } else {
+            apply_rows(P, pbuf, std::integral_constant<int, NRB>{});
         }
     };
     // ---- lambda_s = sum of the wave partials + c_s, stored by one wave group ---
@@ -502,10 +548,14 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
         const int ft = tid - fw * 64 * WPF;
         const bool mine = valid && ft >= 0 && ft < R;
         const int fi = mine ? ft : 0;
-        float acc = sPart[pbuf][0][fi];
+        // rows the apply did not write are zero rows of P_s
+        float acc = 0.0f;
+        if (fi < live_rows(ss)) {
+            acc = sPart[pbuf][0][fi];
 #pragma unroll
-        for (int ww = 1; ww < NW; ++ww)
-            acc += sPart[pbuf][ww][fi];
+            for (int ww = 1; ww < NW; ++ww)
+                acc += sPart[pbuf][ww][fi];
+        }
         if constexpr (AFF)
             acc += sC[ring(ss)][fi];
         const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
@@ -613,7 +663,7 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
             pfb[nx] = load_b(j - 1 - NPF, j - 1 - NPF >= 0);
             load_tile(pf[nx], j - 1 - NPF, j - 1 - NPF >= 0);
             if constexpr (OUT == kOutLambda)
-                apply_partial(P, (int)((j + 1) & 1));
+                apply_partial(P, (int)((j + 1) & 1), j + 1);
             else
                 store_composite(P, j + 1);
 #pragma unroll
@@ -627,7 +677,7 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
         // slot 0's partials reuse the buffer finalize(2) read in the last
         // iteration
         __syncthreads();
-        apply_partial(P, 0);
+        apply_partial(P, 0, 0);
         __syncthreads();
         finalize(1, K >= 2, 1);
         finalize(0, true, 0);
