@@ -136,13 +136,28 @@ __device__ __forceinline__ bf16x8 a_operand(const __bf16 *plane, int I, int p, i
     }
 }
 
+struct NoFill {
+    __device__ void operator()(int) const {}
+};
+
 // Pn = A_j * P on the matrix cores, for the first NR row blocks and NK k blocks
-// (the rest of A_j is zero); rows past NR come out zero.
-template <int R, int M, int NCA, int NR, int NK>
+// (the rest of A_j is zero); rows past NR come out zero.  With FILL, fill(s)
+// runs after MFMA group s of the split arithmetic (the six partial-product
+// groups of each k pair), fenced so that the compiler keeps it there: other
+// work placed in the shadow of the matrix cores.
+template <int R, int M, int NCA, int NR, int NK, bool FILL = false, typename F = NoFill>
 __device__ __forceinline__ void combine(f4 (&Pn)[R / 16][NCA / waves_for(R)],
                                         const f4 (&P)[R / 16][NCA / waves_for(R)],
-                                        const typename Mode<M>::L *sAbuf, int li, int g)
+                                        const typename Mode<M>::L *sAbuf, int li, int g,
+                                        F &&fill = F())
 {
+    auto after_group = [&](int step) {
+        if constexpr (FILL) {
+            __builtin_amdgcn_sched_barrier(0);
+            fill(step);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
     using G = Geo<R, M, NCA>;
     constexpr int NRB = G::NRB, CB = G::CB, PITCH = G::PITCH;
     constexpr int PLANE = R * PITCH;
@@ -252,31 +267,37 @@ __device__ __forceinline__ void combine(f4 (&Pn)[R / 16][NCA / waves_for(R)],
 #pragma unroll
                         for (int I = 0; I < NR; ++I)
                             Pn[I][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[I], bh[t], Pn[I][t], 0, 0, 0);
+                    after_group(6 * p + 0);
 #pragma unroll
                     for (int t = 0; t < CB; ++t)
 #pragma unroll
                         for (int I = 0; I < NR; ++I)
                             Pn[I][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[I], bm[t], Pn[I][t], 0, 0, 0);
+                    after_group(6 * p + 1);
 #pragma unroll
                     for (int t = 0; t < CB; ++t)
 #pragma unroll
                         for (int I = 0; I < NR; ++I)
                             Pn[I][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am[I], bh[t], Pn[I][t], 0, 0, 0);
+                    after_group(6 * p + 2);
 #pragma unroll
                     for (int t = 0; t < CB; ++t)
 #pragma unroll
                         for (int I = 0; I < NR; ++I)
                             Pn[I][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[I], bl[t], Pn[I][t], 0, 0, 0);
+                    after_group(6 * p + 3);
 #pragma unroll
                     for (int t = 0; t < CB; ++t)
 #pragma unroll
                         for (int I = 0; I < NR; ++I)
                             Pn[I][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[I], bh[t], Pn[I][t], 0, 0, 0);
+                    after_group(6 * p + 4);
 #pragma unroll
                     for (int t = 0; t < CB; ++t)
 #pragma unroll
                         for (int I = 0; I < NR; ++I)
                             Pn[I][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am[I], bm[t], Pn[I][t], 0, 0, 0);
+                    after_group(6 * p + 5);
                 } else {
 #pragma unroll
                     for (int I = 0; I < NR; ++I) {
@@ -412,9 +433,11 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
         }
     };
     // Tile j from registers into LDS buffer buf, and (affine) c_j = A_j c_{j+1}
-    // + b_j from the same registers (c_{j+1} = 0 for the first slot).
-    auto stage = [&](const u4 (&src)[CPT], int buf, uint32_t braw, int64_t j, bool first) {
-        float cv[EPC];
+    // + b_j from the same registers (c_{j+1} = 0 for the first slot).  In
+    // three parts, so that the chunks can be spread between MFMAs.
+    float st_cv[EPC];
+    float st_part[CPT];
+    auto stage_begin = [&](int64_t j, bool first) {
         if constexpr (AFF) {
 #pragma unroll
             for (int e = 0; e < EPC; e += 4) {
@@ -422,61 +445,68 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
                                     : *(const f4 *)&sC[ring(j + 1)][scol + e];
 #pragma unroll
                 for (int u = 0; u < 4; ++u)
-                    cv[e + u] = c4[u];
+                    st_cv[e + u] = c4[u];
             }
         }
-        float part[CPT];
+    };
+    auto stage_chunk = [&](const u4 &src, int i, int buf, int64_t j) {
+        const int c = i * T + tid;
+        const int row = i * RPI + srow;
+        float x[EPC];
 #pragma unroll
-        for (int i = 0; i < CPT; ++i) {
-            const int c = i * T + tid;
-            const int row = i * RPI + srow;
-            float x[EPC];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                if constexpr (G::ESZ == 4) {
-                    x[e] = bitsf(src[i][e]);
-                } else {
-                    x[2 * e] = bitsf(src[i][e] << 16);
-                    x[2 * e + 1] = bitsf(src[i][e] & kHighHalf);
-                }
-            }
-            if constexpr (AFF) {
-                // with a widths hint, chunk rows at or past r_j are all zero
-                float s = 0.0f;
-                if (!HINT || i * RPI < live_rows(j)) {
-                    s = x[0] * cv[0];
-#pragma unroll
-                    for (int e = 1; e < EPC; ++e)
-                        s += x[e] * cv[e];
-                }
-                part[i] = s;
-            }
-            if (TILE_CHUNKS % T == 0 || c < TILE_CHUNKS) {
-                L *dst = &sA[buf][row * PITCH];
-                if constexpr (M == kF32) {
-                    *(u4 *)&dst[scol] = src[i];
-                } else if constexpr (M == kBF16) {
-                    if constexpr (PERM) {
-                        *(u2 *)&dst[lds_col<PERM>(scol)] = u2{src[i][0], src[i][1]};
-                        *(u2 *)&dst[lds_col<PERM>(scol + 4)] = u2{src[i][2], src[i][3]};
-                    } else {
-                        *(u4 *)&dst[scol] = src[i];
-                    }
-                } else {
-                    const Split2 s01 = split_pair(x[0], x[1]);
-                    const Split2 s23 = split_pair(x[2], x[3]);
-                    const int pos = lds_col<PERM>(scol);
-                    *(u2 *)&dst[pos] = u2{s01.h, s23.h};
-                    *(u2 *)&dst[PLANE + pos] = u2{s01.m, s23.m};
-                    *(u2 *)&dst[2 * PLANE + pos] = u2{s01.l, s23.l};
-                }
+        for (int e = 0; e < 4; ++e) {
+            if constexpr (G::ESZ == 4) {
+                x[e] = bitsf(src[e]);
+            } else {
+                x[2 * e] = bitsf(src[e] << 16);
+                x[2 * e + 1] = bitsf(src[e] & kHighHalf);
             }
         }
         if constexpr (AFF) {
-            group_reduce<LPR, CPT>(part, sgi);
-            if (oown)
-                sC[ring(j)][orow] = part[0] + bitsf(braw);
+            // with a widths hint, chunk rows at or past r_j are all zero
+            float s = 0.0f;
+            if (!HINT || i * RPI < live_rows(j)) {
+                s = x[0] * st_cv[0];
+#pragma unroll
+                for (int e = 1; e < EPC; ++e)
+                    s += x[e] * st_cv[e];
+            }
+            st_part[i] = s;
         }
+        if (TILE_CHUNKS % T == 0 || c < TILE_CHUNKS) {
+            L *dst = &sA[buf][row * PITCH];
+            if constexpr (M == kF32) {
+                *(u4 *)&dst[scol] = src;
+            } else if constexpr (M == kBF16) {
+                if constexpr (PERM) {
+                    *(u2 *)&dst[lds_col<PERM>(scol)] = u2{src[0], src[1]};
+                    *(u2 *)&dst[lds_col<PERM>(scol + 4)] = u2{src[2], src[3]};
+                } else {
+                    *(u4 *)&dst[scol] = src;
+                }
+            } else {
+                const Split2 s01 = split_pair(x[0], x[1]);
+                const Split2 s23 = split_pair(x[2], x[3]);
+                const int pos = lds_col<PERM>(scol);
+                *(u2 *)&dst[pos] = u2{s01.h, s23.h};
+                *(u2 *)&dst[PLANE + pos] = u2{s01.m, s23.m};
+                *(u2 *)&dst[2 * PLANE + pos] = u2{s01.l, s23.l};
+            }
+        }
+    };
+    auto stage_end = [&](uint32_t braw, int64_t j) {
+        if constexpr (AFF) {
+            group_reduce<LPR, CPT>(st_part, sgi);
+            if (oown)
+                sC[ring(j)][orow] = st_part[0] + bitsf(braw);
+        }
+    };
+    auto stage = [&](const u4 (&src)[CPT], int buf, uint32_t braw, int64_t j, bool first) {
+        stage_begin(j, first);
+#pragma unroll
+        for (int i = 0; i < CPT; ++i)
+            stage_chunk(src[i], i, buf, j);
+        stage_end(braw, j);
     };
 
     // ---- per-lane constants ---------------------------------------------------
@@ -648,24 +678,47 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
             if constexpr (OUT == kOutLambda)
                 finalize(j + 2, j + 2 <= K - 1, (int)((j + 2) & 1));
             f4 Pn[NRB][CB];
-            if constexpr (HINT) {
-                const int nr = pow2_at_least(width_blocks(args, s0 + j));
-                const int nk = pow2_at_least(width_blocks(args, s0 + j + 1));
-                combine_shape<R, M, NCA>(nr, nk, Pn, P, sA[buf], li, g);
+            // The staging of slot j-1 below is unconditional: at j = 0 it
+            // stages the all-zero registers of the nonexistent slot -1 into a
+            // buffer nothing reads again, and its c lands in ring entry
+            // (K + 1) mod 4, which no later reader uses.
+            auto reload = [&]() {
+                pfb[nx] = load_b(j - 1 - NPF, j - 1 - NPF >= 0);
+                load_tile(pf[nx], j - 1 - NPF, j - 1 - NPF >= 0);
+            };
+            auto emit = [&]() {
+                if constexpr (OUT == kOutLambda)
+                    apply_partial(P, (int)((j + 1) & 1), j + 1);
+                else
+                    store_composite(P, j + 1);
+            };
+            if constexpr (M == kF32X && !HINT) {
+                // split arithmetic: the staging chunks, the loads and the
+                // apply go between the 6 (r = 16, 32) or 12 (r = 64) MFMA
+                // groups of the combine
+                stage_begin(j - 1, false);
+                combine<R, M, NCA, NRB, NRB, true>(Pn, P, sA[buf], li, g, [&](int step) {
+                    if (step < CPT)
+                        stage_chunk(pf[nx][step], step, buf ^ 1, j - 1);
+                    else if (step == CPT)
+                        stage_end(pfb[nx], j - 1);
+                    else if (step == CPT + 1)
+                        reload();
+                    else if (step == CPT + 2)
+                        emit();
+                });
             } else {
-                combine<R, M, NCA, NRB, NRB>(Pn, P, sA[buf], li, g);
+                if constexpr (HINT) {
+                    const int nr = pow2_at_least(width_blocks(args, s0 + j));
+                    const int nk = pow2_at_least(width_blocks(args, s0 + j + 1));
+                    combine_shape<R, M, NCA>(nr, nk, Pn, P, sA[buf], li, g);
+                } else {
+                    combine<R, M, NCA, NRB, NRB>(Pn, P, sA[buf], li, g);
+                }
+                stage(pf[nx], buf ^ 1, pfb[nx], j - 1, false);
+                reload();
+                emit();
             }
-            // Unconditional, so that the scheduler can spread it between the
-            // MFMAs: at j = 0 it stages the all-zero registers of the
-            // nonexistent slot -1 into a buffer nothing reads again, and its
-            // c lands in ring entry (K + 1) mod 4, which no later reader uses.
-            stage(pf[nx], buf ^ 1, pfb[nx], j - 1, false);
-            pfb[nx] = load_b(j - 1 - NPF, j - 1 - NPF >= 0);
-            load_tile(pf[nx], j - 1 - NPF, j - 1 - NPF >= 0);
-            if constexpr (OUT == kOutLambda)
-                apply_partial(P, (int)((j + 1) & 1), j + 1);
-            else
-                store_composite(P, j + 1);
 #pragma unroll
             for (int I = 0; I < NRB; ++I)
 #pragma unroll
