@@ -71,6 +71,24 @@ def flops_alg(wl) -> int:
     return wl.B * per_chain
 
 
+def flops_combines(wl) -> int:
+    """The combines alone (the suffix-composite export applies nothing)."""
+    w = widths_of(wl)
+    rK = w[wl.K]
+    return wl.B * sum(2 * w[j] * w[j + 1] * rK + 2 * w[j] * w[j + 1] + w[j]
+                      for j in range(wl.K - 1))
+
+
+def bytes_export(wl) -> int:
+    """A, b read once; every P_j (r x r, fp32) and c_j (fp32) written once."""
+    e = ELEM[wl.dtype]
+    R = wl.r
+    w = widths_of(wl)
+    a = sum(w[j] * w[j + 1] for j in range(wl.K))
+    bb = sum(w[:wl.K]) if wl.affine else 0
+    return wl.B * ((a + bb) * e + wl.K * (R * R + R) * 4)
+
+
 def flops_seq(wl) -> int:
     """The sequential chain of K matvecs: lambda_j = A_j lambda_{j+1} + b_j."""
     w = widths_of(wl)
@@ -255,6 +273,12 @@ def main(argv=None) -> int:
                          "cores (the library default) or the fp32 matrix cores")
     ap.add_argument("--algo", choices=["auto", "chain", "two_level"], default="auto",
                     help="scan algorithm (auto: the library's choice)")
+    ap.add_argument("--op", choices=["adjoints", "suffix_products", "streaming"],
+                    default="adjoints",
+                    help="what one step computes: every lambda_j (lbi_scan_backward_ex), "
+                         "every composite (P_j, c_j) (lbi_scan_suffix_products), or every "
+                         "lambda_j with progress published (lbi_scan_backward_streaming)")
+    ap.add_argument("--chunk", type=int, default=16, help="streaming: slots per publication")
     ap.add_argument("--B", type=int, default=0, help="override the workload's chain count")
     ap.add_argument("--K", type=int, default=0, help="override the workload's slot count")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -323,9 +347,26 @@ def main(argv=None) -> int:
                                                          0 if wl.dtype == "f32" else 1, algo)
     ws = torch.empty((need,), dtype=torch.uint8, device=dev) if need else None
 
-    def step(i):
-        c = copies[i % ncopy]
-        binding.lbi_scan_backward_ex(c.A, c.b, c.lamK, hint, math, algo, lam=lam, workspace=ws)
+    if args.op == "streaming":
+        progress = torch.zeros(wl.B, dtype=torch.int32, device=dev)
+
+        def step(i):
+            c = copies[i % ncopy]
+            progress.zero_()
+            binding.lbi_scan_backward_streaming(c.A, c.b, c.lamK, progress, args.chunk, hint,
+                                                math, lam=lam)
+    elif args.op == "suffix_products":
+        Pout = torch.empty((wl.B, wl.K, wl.r, wl.r), dtype=torch.float32, device=dev)
+        cout = torch.empty((wl.B, wl.K, wl.r), dtype=torch.float32, device=dev)
+
+        def step(i):
+            c = copies[i % ncopy]
+            binding.lbi_scan_suffix_products(c.A, c.b, hint, math, P=Pout, c=cout)
+    else:
+        def step(i):
+            c = copies[i % ncopy]
+            binding.lbi_scan_backward_ex(c.A, c.b, c.lamK, hint, math, algo, lam=lam,
+                                         workspace=ws)
 
     if args.copy_calibration > 0:
         # A plain streaming kernel of known size (torch's elementwise negation:
@@ -360,8 +401,8 @@ def main(argv=None) -> int:
     ms_per_step = total_ms / args.steps
 
     value = combines(wl) * args.steps / (total_ms / 1e3)
-    f_alg = flops_alg(wl)
-    b_alg = bytes_alg(wl)
+    f_alg = flops_combines(wl) if args.op == "suffix_products" else flops_alg(wl)
+    b_alg = bytes_export(wl) if args.op == "suffix_products" else bytes_alg(wl)
     tflops = f_alg / avg_launch_s / 1e12
     gbs = b_alg / avg_launch_s / 1e9
     mode = mode_of(wl, args.math)
@@ -378,7 +419,8 @@ def main(argv=None) -> int:
     else:
         roof = {"bound": "hbm", "achieved": gbs, "peak": PEAK["hbm_gbs"], "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = load_traffic(wl.name) if args.math == "split" or wl.dtype == "bf16" else None
+    roof["traffic"] = (load_traffic(wl.name) if args.op == "adjoints" and
+                       (args.math == "split" or wl.dtype == "bf16") else None)
     out = {
         "metric": METRIC,
         "value": value,
@@ -395,7 +437,7 @@ def main(argv=None) -> int:
                 "Jacobians; no dataset or checkpoint)",
         "config": {"workload": wl.name, "B": wl.B, "K": wl.K, "r": wl.r,
                    "storage": wl.dtype, "affine": wl.affine, "arithmetic": mode,
-                   "algorithm": args.algo, "workspace_bytes": need,
+                   "algorithm": args.algo, "workspace_bytes": need, "op": args.op,
                    "widths": "cyclic 32/64/128" if wl.widths else "uniform",
                    "parallelism": "1 GPU, " + ("two-level scan (segments in parallel)" if need
                                                else "one workgroup per chain")},

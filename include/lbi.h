@@ -49,7 +49,7 @@ extern "C" {
 /* HIP stream handle (the same type as hipStream_t). */
 typedef struct ihipStream_t *lbi_stream_t;
 
-#define LBI_ABI_VERSION 3
+#define LBI_ABI_VERSION 4
 
 /* Largest K for which a widths hint is used (longer chains run unhinted,
  * which gives identical results). */
@@ -201,6 +201,35 @@ lbi_status lbi_scan_backward_ex(const void *A, const void *b, const void *lambda
 lbi_status lbi_scan_suffix_products(const void *A, const void *b, float *P, float *c, int64_t B,
                                     int64_t K, int32_t r, lbi_dtype dt, lbi_stream_t stream,
                                     const int32_t *widths_host, lbi_math math);
+
+/*
+ * lbi_scan_backward with LBI_ALGO_CHAIN, publishing progress while it runs
+ * (each chain's adjoints become final in the order lambda_{K-1}, ...,
+ * lambda_0), so that work on the latest regions (the region-local backward of
+ * Algorithm "Bounded-Interface Backpropagation", Phase 3) can start before the
+ * whole scan ends.
+ *
+ *   A, b, lambda_K, lambda, B, K, r, dt, stream, widths_host, math: as for
+ *                   lbi_scan_backward_ex.
+ *   progress [B]    uint32 in DEVICE memory, set to 0 by the caller before the
+ *                   call.  progress[beta] only grows; each value n it takes
+ *                   is a multiple of `chunk` or K, and by the time it is
+ *                   visible (device scope, e.g. to a kernel on another stream
+ *                   that reads it with acquire ordering), lambda_{K-n} ..
+ *                   lambda_{K-1} of chain beta are stored and visible.  It
+ *                   ends at K.
+ *   chunk >= 1      slots per publication; each costs the chain's storing
+ *                   wave a wait for its outstanding memory operations and an
+ *                   L2 write-back, so larger chunks cost less (measured in
+ *                   the design notes).
+ *
+ * Results equal lbi_scan_backward_ex(..., LBI_ALGO_CHAIN) bit for bit.
+ */
+lbi_status lbi_scan_backward_streaming(const void *A, const void *b, const void *lambda_K,
+                                       float *lambda, int64_t B, int64_t K, int32_t r,
+                                       lbi_dtype dt, lbi_stream_t stream,
+                                       const int32_t *widths_host, lbi_math math,
+                                       uint32_t *progress, int32_t chunk);
 
 /* A static, human-readable name for a status code. */
 const char *lbi_status_string(lbi_status s);

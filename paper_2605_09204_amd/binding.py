@@ -71,6 +71,10 @@ def load() -> ctypes.CDLL:
     lib.lbi_scan_suffix_products.argtypes = [vp, vp, vp, vp, i64, i64, i32, ctypes.c_int, vp,
                                              ctypes.POINTER(ctypes.c_int32), ctypes.c_int]
     lib.lbi_scan_suffix_products.restype = ctypes.c_int
+    lib.lbi_scan_backward_streaming.argtypes = [vp, vp, vp, vp, i64, i64, i32, ctypes.c_int, vp,
+                                                ctypes.POINTER(ctypes.c_int32), ctypes.c_int,
+                                                vp, i32]
+    lib.lbi_scan_backward_streaming.restype = ctypes.c_int
     lib.lbi_status_string.argtypes = [ctypes.c_int]
     lib.lbi_status_string.restype = ctypes.c_char_p
     lib.lbi_abi_version.argtypes = []
@@ -212,3 +216,24 @@ def lbi_scan_suffix_products(A: torch.Tensor, b: Optional[torch.Tensor],
         c.data_ptr() if c is not None else None, B, K, r, _DTYPES[A.dtype],
         _stream_ptr(stream, A.device), wptr, int(math)))
     return P, c
+
+
+def lbi_scan_backward_streaming(A: torch.Tensor, b: Optional[torch.Tensor],
+                                lambda_K: torch.Tensor, progress: torch.Tensor, chunk: int,
+                                widths: Optional[Sequence[int]] = None,
+                                math: int = LBI_MATH_DEFAULT, lam: Optional[torch.Tensor] = None,
+                                stream=None) -> torch.Tensor:
+    """The chain scan, raising progress[beta] (int32/uint32 [B] GPU tensor, zeroed by
+    the caller) to the count of final adjoints every ``chunk`` slots."""
+    lam, args = _marshal(A, b, lambda_K, lam, None, stream, LBI_ALGO_CHAIN)
+    B = int(A.shape[0])
+    if (progress.dim() != 1 or progress.shape[0] != B or progress.dtype not in
+            (torch.int32, torch.uint32) or not progress.is_contiguous()
+            or progress.device != A.device):
+        raise ValueError(f"progress must be a contiguous 32-bit [{B}] tensor on A's device")
+    warr, wptr = _widths_arg(widths, int(A.shape[1]))
+    Aptr, bptr, lkptr, lamptr, B_, K, r, dt, _ws, _wsb, sptr = args
+    _check(load().lbi_scan_backward_streaming(Aptr, bptr, lkptr, lamptr, B_, K, r, dt, sptr,
+                                              wptr, int(math), progress.data_ptr(),
+                                              int(chunk)))
+    return lam

@@ -304,6 +304,54 @@ lbi_status lbi_scan_suffix_products(const void *A, const void *b, float *P, floa
     return launch_chain_mode(cl, dt, math) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
 }
 
+lbi_status lbi_scan_backward_streaming(const void *A, const void *b, const void *lambda_K,
+                                       float *lambda, int64_t B, int64_t K, int32_t r,
+                                       lbi_dtype dt, lbi_stream_t stream,
+                                       const int32_t *widths_host, lbi_math math,
+                                       uint32_t *progress, int32_t chunk)
+{
+    lbi_status st = check_common(dt, math, r, B, K);
+    if (st != LBI_OK)
+        return st;
+    if (chunk < 1)
+        return LBI_ERR_SHAPE;
+    if (B == 0)
+        return LBI_OK;
+    if (!A || !lambda_K || !lambda || !progress)
+        return LBI_ERR_NULL;
+    if (misaligned(A) || misaligned(b) || misaligned(lambda_K) || misaligned(lambda) ||
+        ((uintptr_t)progress & 3u))
+        return LBI_ERR_ALIGN;
+    const size_t esz = dt == LBI_F32 ? 4 : 2;
+    const size_t nA = (size_t)B * K * r * r * esz, nb = b ? (size_t)B * K * r * esz : 0;
+    const size_t nl = (size_t)B * r * esz, nout = (size_t)B * K * r * sizeof(float);
+    const size_t np = (size_t)B * sizeof(uint32_t);
+    if (overlaps(lambda, nout, A, nA) || overlaps(lambda, nout, b, nb) ||
+        overlaps(lambda, nout, lambda_K, nl) || overlaps(progress, np, A, nA) ||
+        overlaps(progress, np, b, nb) || overlaps(progress, np, lambda_K, nl) ||
+        overlaps(progress, np, lambda, nout))
+        return LBI_ERR_ALIAS;
+    ChainLaunch c;
+    memset(&c, 0, sizeof c);
+    c.args.A = A;
+    c.args.b = b;
+    c.args.lamK = lambda_K;
+    c.args.lam = lambda;
+    c.args.K = K;
+    c.args.L = K;
+    c.args.S = 1;
+    c.args.progress = progress;
+    c.args.pchunk = chunk;
+    c.B = B;
+    c.r = r;
+    c.aff = b != nullptr;
+    c.out = kOutLambda;
+    c.stream = (hipStream_t)stream;
+    if (!encode_widths(widths_host, K, r, c))
+        return LBI_ERR_SHAPE;
+    return launch_chain_mode(c, dt, math) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
+}
+
 const char *lbi_status_string(lbi_status s)
 {
     switch (s) {

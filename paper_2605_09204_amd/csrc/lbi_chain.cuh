@@ -567,6 +567,18 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
             apply_rows(P, pbuf, std::integral_constant<int, NRB>{});
         }
     };
+    // ---- streaming: slots after which progress is published --------------------
+    // every pchunk final slots, and the last one
+    auto publish_point = [&](int64_t x) { return x == 0 || (K - x) % args.pchunk == 0; };
+    // Called after a barrier that follows finalize(x): the storing wave group
+    // fenced its stores of slots x .. K-1 before it, so the count K - x can be
+    // published.
+    auto publish_before = [&](int64_t x) {
+        if constexpr (OUT == kOutLambda) {
+            if (args.progress && x <= K - 1 && publish_point(x) && tid == 0)
+                atomicMax(&args.progress[beta], (uint32_t)(K - x));
+        }
+    };
     // ---- lambda_s = sum of the wave partials + c_s, stored by one wave group ---
     // Branch-free: lanes with nothing to store (and calls with valid = false)
     // get an out-of-range offset, which the buffer store drops; every wave
@@ -574,7 +586,9 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
     // count of outstanding loads exact.
     auto finalize = [&](int64_t s, bool valid, int pbuf) {
         const int64_t ss = valid ? s : 0;
-        const int fw = (int)((uint64_t)ss % NWF);
+        // (when streaming, one wave group stores every slot, so that only it
+        // has to fence before a publication)
+        const int fw = args.progress ? 0 : (int)((uint64_t)ss % NWF);
         const int ft = tid - fw * 64 * WPF;
         const bool mine = valid && ft >= 0 && ft < R;
         const int fi = mine ? ft : 0;
@@ -592,6 +606,14 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
             (void *)(lam + ss * R), 0, R * (int)sizeof(float), kBufferWord3);
         __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc), rs,
                                               mine ? fi * (int)sizeof(float) : kOutOfRange, 0, 0);
+        // Streaming: at a publish point the storing wave group makes its
+        // lambda stores visible device-wide (release: L2 written back); after
+        // the next barrier one lane raises progress[beta] to the count of
+        // final adjoints (see publish_before).
+        if constexpr (OUT == kOutLambda) {
+            if (args.progress && valid && publish_point(ss) && w / WPF == 0)
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        }
     };
     // ---- the composite (P_s, c_s) of local slot s, to global memory -----------
     // (branch-free buffer stores; each lane writes its rows of its columns)
@@ -675,6 +697,7 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
             const int buf = (int)((uint32_t)(K - 1 - j) & 1);
             const int nx = (s + 2) % NPF;  // register set of slot j-1 (constant once unrolled)
             __syncthreads();
+            publish_before(j + 3);
             if constexpr (OUT == kOutLambda)
                 finalize(j + 2, j + 2 <= K - 1, (int)((j + 2) & 1));
             f4 Pn[NRB][CB];
@@ -730,10 +753,19 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
         // slot 0's partials reuse the buffer finalize(2) read in the last
         // iteration
         __syncthreads();
+        publish_before(2);
         apply_partial(P, 0, 0);
         __syncthreads();
         finalize(1, K >= 2, 1);
+        if (args.progress) {
+            __syncthreads();
+            publish_before(1);
+        }
         finalize(0, true, 0);
+        if (args.progress) {
+            __syncthreads();
+            publish_before(0);
+        }
     } else {
         // c_0 was staged before the last barrier
         store_composite(P, 0);

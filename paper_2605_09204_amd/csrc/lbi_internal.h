@@ -31,6 +31,9 @@ struct ScanArgs {
                        // d*L .. min(K, (d+1)*L) - 1 into composites local to
                        // the segment (L = K: whole chains)
     int32_t S;         // segments per chain, ceil(K / L)
+    uint32_t *progress;  // [B] or NULL (kOutLambda, whole chains): raised to the
+                         // number of final adjoints after every pchunk slots
+    int32_t pchunk;
     // ceil(r_k / 16) for k = 0..K as 4-bit fields, 8 per word (hinted launches)
     uint32_t wcode[(LBI_MAX_HINT_K + 1 + 7) / 8];
 };

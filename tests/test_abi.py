@@ -31,8 +31,8 @@ def test_header_declares_entry_points():
     assert names == sorted(["lbi_scan_backward_workspace_bytes",
                             "lbi_scan_backward_workspace_bytes_ex", "lbi_scan_backward",
                             "lbi_scan_backward_widths", "lbi_scan_backward_ex",
-                            "lbi_scan_suffix_products", "lbi_status_string",
-                            "lbi_abi_version"])
+                            "lbi_scan_suffix_products", "lbi_scan_backward_streaming",
+                            "lbi_status_string", "lbi_abi_version"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -54,7 +54,7 @@ def test_header_compiles_as_c():
 
 
 def test_version_and_status_strings():
-    assert binding.lbi_abi_version() == 3
+    assert binding.lbi_abi_version() == 4
     assert binding.lbi_status_string(0) == "LBI_OK"
     for code in range(1, 9):
         assert binding.lbi_status_string(code).startswith("LBI_ERR_")
@@ -137,3 +137,14 @@ def test_suffix_products_argument_errors():
     assert f(PA, PB, POUT + 4, PL, 2, 3, 64, 0, None, None, 0) == 7
     assert f(PA, PB, PA + 64, PL, 2, 3, 64, 0, None, None, 0) == 8
     assert f(None, None, None, None, 0, 3, 64, 0, None, None, 0) == 0
+
+
+def test_streaming_argument_errors():
+    f = binding.load().lbi_scan_backward_streaming
+    PP = 0x60000000
+    assert f(PA, PB, PL, POUT, 2, 3, 64, 0, None, None, 0, PP, 0) == 2     # chunk < 1
+    assert f(PA, PB, PL, POUT, 2, 3, 64, 0, None, None, 0, None, 4) == 1   # no progress
+    assert f(PA, PB, PL, POUT, 2, 3, 64, 0, None, None, 0, PP + 2, 4) == 7
+    assert f(PA, PB, PL, POUT, 2, 3, 64, 0, None, None, 0, PA + 64, 4) == 8
+    assert f(PA, PB, PL, POUT, 2, 3, 64, 3, None, None, 0, PP, 4) == 3
+    assert f(None, None, None, None, 0, 3, 64, 0, None, None, 0, None, 4) == 0

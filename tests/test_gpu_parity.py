@@ -360,3 +360,60 @@ def test_suffix_products_exact_on_permutations():
     Pr, cr = oracle.suffix_composites(x.A, x.b)
     assert np.array_equal(P.cpu().numpy().astype(np.float64), Pr)
     assert np.array_equal(c.cpu().numpy().astype(np.float64), cr)
+
+
+# ----------------------------------------------------------------------------
+# streaming: adjoints published while the scan runs
+# ----------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype,arith", MODES, ids=MODE_IDS)
+@pytest.mark.parametrize("B,K,r,chunk", [(3, 40, 64, 8), (2, 33, 16, 1), (1, 130, 128, 16),
+                                         (4, 7, 32, 64)])
+def test_streaming_matches_chain_scan(B, K, r, chunk, dtype, arith):
+    _say(f"[streaming] B={B} K={K} r={r} chunk={chunk} {dtype} {arith}")
+    x = synth.random_chain(B, K, r, dtype=dtype, seed=43 + K)
+    dev = torch.device("cuda:0")
+    progress = torch.zeros(B, dtype=torch.int32, device=dev)
+    lam = binding.lbi_scan_backward_streaming(x.A.to(dev), x.b.to(dev), x.lamK.to(dev), progress,
+                                              chunk, math=MATH[arith] if arith else 0)
+    torch.cuda.synchronize()
+    assert torch.equal(lam, run_gpu(x, math=arith, algo="chain"))
+    assert progress.tolist() == [K] * B
+
+
+def test_streaming_exposes_adjoints_before_the_scan_ends():
+    """A second stream waits (hipStreamWaitValue32, >=) until 1024 adjoints of
+    every chain are published, then copies them while the scan still runs:
+    the copy must hold the final values and finish before the scan does."""
+    import ctypes
+    hip = ctypes.CDLL("libamdhip64.so")
+    hip.hipStreamWaitValue32.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint32,
+                                         ctypes.c_uint, ctypes.c_uint32]
+    hip.hipStreamWaitValue32.restype = ctypes.c_int
+    B, K, r, n, chunk = 2, 4096, 64, 1024, 64
+    dev = torch.device("cuda:0")
+    x = synth.random_chain(B, K, r, dtype="f32", seed=47, spectrum="orthogonal", device=dev)
+    progress = torch.zeros(B, dtype=torch.int32, device=dev)
+    lam = torch.empty((B, K, r), dtype=torch.float32, device=dev)
+    snap = torch.empty((B, n, r), dtype=torch.float32, device=dev)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    done_scan = torch.cuda.Event(enable_timing=True)
+    done_copy = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    binding.lbi_scan_backward_streaming(x.A, x.b, x.lamK, progress, chunk, lam=lam, stream=s1)
+    done_scan.record(s1)
+    for beta in range(B):
+        rc = hip.hipStreamWaitValue32(s2.cuda_stream, progress.data_ptr() + 4 * beta, n, 0,
+                                      0xFFFFFFFF)
+        if rc != 0:
+            torch.cuda.synchronize()
+            pytest.skip(f"hipStreamWaitValue32 unavailable (error {rc})")
+    with torch.cuda.stream(s2):
+        snap.copy_(lam[:, K - n:])
+        done_copy.record(s2)
+    torch.cuda.synchronize()
+    assert progress.tolist() == [K] * B
+    assert torch.equal(snap, lam[:, K - n:])
+    lead_ms = done_copy.elapsed_time(done_scan)
+    _say(f"  the copy of the first {n} adjoints finished {lead_ms:.3f} ms before the scan")
+    assert lead_ms > 0
