@@ -84,7 +84,7 @@ typedef enum {
     LBI_ALGO_CHAIN = 1,     /* one workgroup folds each whole chain right to
                              * left (K-1 combines, span K) and applies every
                              * composite to lambda_K as it forms; no workspace */
-    LBI_ALGO_TWO_LEVEL = 2  /* each chain is cut into S ~ sqrt(8K) segments; a
+    LBI_ALGO_TWO_LEVEL = 2  /* each chain is cut into S ~ sqrt(2K) segments; a
                              * workgroup per segment folds it into its local
                              * composites (kept in the workspace), a carry pass
                              * applies the segment aggregates right to left to

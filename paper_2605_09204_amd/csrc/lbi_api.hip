@@ -39,9 +39,10 @@ bool misaligned(const void *p) { return p && ((uintptr_t)p & 15u); }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Segments of the two-level scan: a segment costs about one chain-kernel slot
-// step per slot and a carry step costs about a tenth of that, so S ~ sqrt(8K)
-// balances the L = K/S fold steps against the S carry steps.
+// Segments of the two-level scan: S ~ sqrt(2K) balances the K/S fold steps
+// (each a chain-kernel slot step, plus a pipeline start per workgroup) against
+// the S carry steps; a sweep over S on MI355X (B = 1..128, K = 128..2048, r =
+// 64) puts the optimum there, within 5% or a flat region.
 struct TwoLevelPlan {
     int64_t L;
     int32_t S;
@@ -51,7 +52,7 @@ struct TwoLevelPlan {
 TwoLevelPlan two_level_plan(int64_t B, int64_t K, int32_t r)
 {
     TwoLevelPlan p;
-    int64_t S = (int64_t)ceil(sqrt(8.0 * (double)K));
+    int64_t S = (int64_t)ceil(sqrt(2.0 * (double)K));
     if (S > K)
         S = K;
     if (S < 1)
