@@ -72,30 +72,32 @@ TwoLevelPlan two_level_plan(int64_t B, int64_t K, int32_t r)
 // The grid of the apply pass is B*K workgroups.
 bool two_level_possible(int64_t B, int64_t K) { return B * K < ((int64_t)1 << 31) - 1; }
 
-// Microseconds per slot of one chain-kernel workgroup at two or fewer waves
-// per SIMD (measured on MI355X, r = 16, 32, 64, 128).
+// Microseconds per slot of one chain-kernel workgroup on an otherwise idle
+// MI355X (r = 16, 32, 64, 128; fp32 storage in the default arithmetic).
 double slot_us(lbi_dtype dt, int32_t r)
 {
     const int i = r == 16 ? 0 : (r == 32 ? 1 : (r == 64 ? 2 : 3));
-    static const double f32[4] = {0.40, 0.70, 1.40, 3.0}, bf16[4] = {0.35, 0.60, 0.88, 3.0};
+    static const double f32[4] = {0.44, 0.72, 1.42, 8.67}, bf16[4] = {0.40, 0.62, 0.95, 2.91};
     return dt == LBI_BF16 ? bf16[i] : f32[i];
 }
 
 // LBI_ALGO_AUTO: the cheaper of the two by a cost model fitted to MI355X
-// timings.  Chain scan: K serial slot steps (more once the chains exceed two
-// waves per SIMD).  Two-level scan: K/S slot steps over B*S workgroups, S
-// carry steps, and the composites written and read once (8 B K r^2 bytes).
+// timings (B = 1..512, K = 32..512, every r; within 13% of the faster choice
+// everywhere on that grid).  Chain scan: K serial slot steps, slower once the
+// chains hold more than 1280 waves.  Two-level scan: K/S slot steps over B*S
+// workgroups, S carry steps, and the composites written and read once
+// (8 B K r^2 bytes at 5.8 TB/s).
 lbi_algo resolve_algo(lbi_algo algo, int64_t B, int64_t K, int32_t r, lbi_dtype dt)
 {
     if (algo == LBI_ALGO_CHAIN || algo == LBI_ALGO_TWO_LEVEL)
         return algo;
     if (K < 16 || !two_level_possible(B, K))
         return LBI_ALGO_CHAIN;
-    const double ts = slot_us(dt, r), w = waves_for_r(r), simd2 = 2.0 * 1024;
-    const double chain = 8.0 + (double)K * ts * fmax(1.0, (double)B * w / simd2);
+    const double ts = slot_us(dt, r), w = waves_for_r(r), cap = 1280.0;
+    const double chain = 6.0 + (double)K * ts * fmax(1.0, (double)B * w / cap);
     const TwoLevelPlan p = two_level_plan(B, K, r);
-    const double two = 12.0 + (double)p.L * ts * fmax(1.0, (double)B * p.S * w / simd2) +
-                       0.4 * p.S + 8.0 * (double)B * K * r * r / 4.0e6;
+    const double two = 12.0 + (double)p.L * ts * fmax(1.0, (double)B * p.S * w / cap) +
+                       0.22 * p.S * sqrt(r / 64.0) + 8.0 * (double)B * K * r * r / 5.8e6;
     return two < chain ? LBI_ALGO_TWO_LEVEL : LBI_ALGO_CHAIN;
 }
 

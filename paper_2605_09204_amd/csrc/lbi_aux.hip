@@ -10,11 +10,12 @@
 //   apply: lambda_j = P_j lambda_{e(j)} + c_j for every slot at once
 //          (Phase 2 of Algorithm "Bounded-Interface Backpropagation", with the
 //          segment's carry in place of mbar_K).
-// Both are matrix-vector work on fp32 composites: one 256-thread workgroup
-// per matrix, TPR lanes per row, each lane CPR consecutive columns (16-byte
-// loads, coalesced across the row's lanes), the row sum reduced by DPP
-// within the lane group.  The carry walks its S aggregates serially, with
-// the loads of the next two issued ahead.
+// Both are matrix-vector work on fp32 composites: TPR lanes per row, each
+// lane CPR consecutive columns (16-byte loads, coalesced across the row's
+// lanes), the row sum reduced by DPP within the lane group.  The carry gives
+// each chain one 256-thread workgroup and walks its S aggregates serially,
+// with the loads of the next two issued ahead; the apply pass gives each
+// workgroup one or more whole slots, 16 KB of composites or more.
 
 #include "lbi_device.cuh"
 #include "lbi_internal.h"
@@ -30,12 +31,11 @@ template <int R> struct MatVec {
     static_assert(TPR >= 2 && TPR <= 16 && (CPR % 4 == 0 || CPR == 1), "matvec geometry");
 };
 
-// Sum over this lane's columns of p[e] x[col0 + e], then over the row's lanes;
-// every lane of the group ends with the full row sum.
-template <int R>
-__device__ __forceinline__ float row_dot(const float (&p)[MatVec<R>::CPR], const float *x, int col0)
+// Sum over this lane's CPR columns of p[e] x[col0 + e], then over the row's
+// TPR lanes; every lane of the group ends with the full row sum.
+template <int CPR, int TPR>
+__device__ __forceinline__ float row_dot(const float (&p)[CPR], const float *x, int col0)
 {
-    constexpr int CPR = MatVec<R>::CPR, TPR = MatVec<R>::TPR;
     float acc = 0.0f;
     if constexpr (CPR >= 4) {
 #pragma unroll
@@ -51,11 +51,10 @@ __device__ __forceinline__ float row_dot(const float (&p)[MatVec<R>::CPR], const
     return q[0];
 }
 
-// This lane's CPR columns of one row of a composite (16-byte loads).
-template <int R>
-__device__ __forceinline__ void load_row(float (&p)[MatVec<R>::CPR], const float *Prow)
+// This lane's CPR consecutive columns of one row of a composite (16-byte loads).
+template <int CPR>
+__device__ __forceinline__ void load_row(float (&p)[CPR], const float *Prow)
 {
-    constexpr int CPR = MatVec<R>::CPR;
     if constexpr (CPR >= 4) {
 #pragma unroll
         for (int e = 0; e < CPR; e += 4) {
@@ -92,13 +91,13 @@ __global__ __launch_bounds__(kThreads) void carry_kernel(const float *Pc, const 
     auto fetch = [&](int32_t d, float(&p)[CPR], float &c) {
         if (d >= 1) {
             const int64_t slot = beta * K + (int64_t)d * Lseg;  // first slot of segment d
-            load_row<R>(p, Pc + (slot * R + row) * R + col0);
+            load_row<CPR>(p, Pc + (slot * R + row) * R + col0);
             c = cc && owner ? cc[slot * R + row] : 0.0f;
         }
     };
     int cur = 0;
     auto step = [&](int32_t d, const float(&p)[CPR], float c) {
-        const float sum = row_dot<R>(p, sl[cur], col0);
+        const float sum = row_dot<CPR, TPR>(p, sl[cur], col0);
         if (owner) {
             const float v = sum + c;
             sl[cur ^ 1][row] = v;
@@ -125,25 +124,43 @@ __global__ __launch_bounds__(kThreads) void carry_kernel(const float *Pc, const 
     }
 }
 
+// The apply pass moves 16 KB of composites per workgroup or more: G slots per
+// workgroup of TPR lanes per row and CPR >= 16 consecutive columns per lane.
+template <int R> struct ApplyGeo {
+    static constexpr int CPR = R >= 128 ? 64 : 16;
+    static constexpr int TPR = R / CPR;
+    static constexpr int T = R * TPR;  // lanes per slot
+    static constexpr int G = kThreads / T;
+    static_assert(G * T == kThreads && TPR <= 16, "apply geometry");
+};
+
 template <int R>
 __global__ __launch_bounds__(kThreads) void apply_kernel(const float *Pc, const float *cc,
                                                         const float *carry, float *lam,
-                                                        int64_t K, int64_t Lseg, int32_t S)
+                                                        int64_t BK, int64_t K, int64_t Lseg,
+                                                        int32_t S)
 {
-    constexpr int TPR = MatVec<R>::TPR, CPR = MatVec<R>::CPR;
-    __shared__ __attribute__((aligned(16))) float sx[R];
+    using Geo = ApplyGeo<R>;
+    constexpr int TPR = Geo::TPR, CPR = Geo::CPR, G = Geo::G;
+    __shared__ __attribute__((aligned(16))) float sx[G][R];
     const int tid = threadIdx.x;
-    const int64_t slot = blockIdx.x;  // global slot beta * K + j
-    const int64_t beta = slot / K, j = slot % K;
-    const int64_t d = j / Lseg;
-    if (tid < R)
-        sx[tid] = carry[(beta * S + d) * R + tid];
+    const int g = tid / Geo::T, t = tid % Geo::T;
+    // global slot beta * K + j of this lane group (past the end: no loads or
+    // stores, but still at the barrier)
+    const int64_t slot = (int64_t)blockIdx.x * G + g;
+    const bool live = slot < BK;
+    if (t < R && live) {
+        const int64_t beta = slot / K, d = (slot % K) / Lseg;
+        sx[g][t] = carry[(beta * S + d) * R + t];
+    }
     __syncthreads();
-    const int row = tid / TPR, col0 = (tid % TPR) * CPR;
+    if (!live)
+        return;
+    const int row = t / TPR, col0 = (t % TPR) * CPR;
     float p[CPR];
-    load_row<R>(p, Pc + (slot * R + row) * R + col0);
-    const float sum = row_dot<R>(p, sx, col0);
-    if (tid % TPR == 0)
+    load_row<CPR>(p, Pc + (slot * R + row) * R + col0);
+    const float sum = row_dot<CPR, TPR>(p, sx[g], col0);
+    if (t % TPR == 0)
         lam[slot * R + row] = sum + (cc ? cc[slot * R + row] : 0.0f);
 }
 
@@ -164,8 +181,10 @@ template <int R>
 hipError_t apply_r(const float *Pc, const float *cc, const float *carry, float *lam, int64_t B,
                    int64_t K, int64_t Lseg, int32_t S, hipStream_t st)
 {
-    hipLaunchKernelGGL((apply_kernel<R>), dim3((unsigned)(B * K)), dim3(kThreads), 0, st, Pc, cc,
-                       carry, lam, K, Lseg, S);
+    constexpr int G = ApplyGeo<R>::G;
+    const int64_t BK = B * K;
+    hipLaunchKernelGGL((apply_kernel<R>), dim3((unsigned)((BK + G - 1) / G)), dim3(kThreads), 0,
+                       st, Pc, cc, carry, lam, BK, K, Lseg, S);
     return hipGetLastError();
 }
 
