@@ -222,6 +222,48 @@ def load_traffic(workload: str):
     return rec.get("hbm_bytes_per_launch")
 
 
+def norms_record(wl, args, total_ms, avg_launch_s, per_launch_ms, ncopy) -> dict:
+    """JSON line of the --op norms run: spectral + Frobenius norms of every
+    r x r tile of A.  Executed fp32 matrix-core work per matrix: the Gram
+    product and 24 normalised squarings, 25 r x r x r products (50 r^3 flop);
+    bytes: the A stack read twice (norms, then the Rayleigh quotient's
+    matrix-vector product) and two floats written per matrix."""
+    n = wl.B * wl.K
+    f_exec = 50.0 * wl.r ** 3 * n
+    b_alg = 2.0 * n * wl.r * wl.r * ELEM[wl.dtype] + 8.0 * n
+    t_mfma = f_exec / (PEAK["mfma_f32_tflops"] * 1e12)
+    t_hbm = b_alg / (PEAK["hbm_gbs"] * 1e9)
+    ach = f_exec / avg_launch_s / 1e12
+    return {
+        "metric": "interface-Jacobian norms/sec (spectral + Frobenius, appendix statistics)",
+        "value": n * args.steps / (total_ms / 1e3),
+        "unit": "matrices/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": total_ms / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded Haar-orthogonal x diag x Haar-orthogonal interface "
+                "Jacobians; no dataset or checkpoint)",
+        "config": {"workload": wl.name, "B": wl.B, "K": wl.K, "r": wl.r, "storage": wl.dtype,
+                   "op": "norms", "parallelism": "1 GPU, one wavefront per matrix"
+                   if wl.r <= 64 else "1 GPU, one workgroup per matrix"},
+        "roofline": {"bound": "mfma" if t_mfma >= t_hbm else "hbm",
+                     "achieved": ach if t_mfma >= t_hbm else b_alg / avg_launch_s / 1e9,
+                     "peak": PEAK["mfma_f32_tflops"] if t_mfma >= t_hbm else PEAK["hbm_gbs"],
+                     "unit": "TFLOP/s" if t_mfma >= t_hbm else "GB/s",
+                     "frac": (ach / PEAK["mfma_f32_tflops"]) if t_mfma >= t_hbm
+                     else (b_alg / avg_launch_s / 1e9) / PEAK["hbm_gbs"],
+                     "traffic": None},
+        "extra": {"avg_launch_ms": avg_launch_s * 1e3, "min_launch_ms": min(per_launch_ms),
+                  "executed_mfma_tflops": ach, "ideal_ms_mfma": t_mfma * 1e3,
+                  "ideal_ms_hbm": t_hbm * 1e3, "input_copies_rotated": ncopy},
+    }
+
+
 # ----------------------------------------------------------------------------
 # CPU baseline: the oracle on a bounded sample of the same workload
 # ----------------------------------------------------------------------------
@@ -273,11 +315,13 @@ def main(argv=None) -> int:
                          "cores (the library default) or the fp32 matrix cores")
     ap.add_argument("--algo", choices=["auto", "chain", "two_level"], default="auto",
                     help="scan algorithm (auto: the library's choice)")
-    ap.add_argument("--op", choices=["adjoints", "suffix_products", "streaming"],
+    ap.add_argument("--op", choices=["adjoints", "suffix_products", "streaming", "norms"],
                     default="adjoints",
                     help="what one step computes: every lambda_j (lbi_scan_backward_ex), "
-                         "every composite (P_j, c_j) (lbi_scan_suffix_products), or every "
-                         "lambda_j with progress published (lbi_scan_backward_streaming)")
+                         "every composite (P_j, c_j) (lbi_scan_suffix_products), every "
+                         "lambda_j with progress published (lbi_scan_backward_streaming), or "
+                         "the spectral and Frobenius norm of every A_j (lbi_matrix_norms; "
+                         "reported in matrices/s)")
     ap.add_argument("--chunk", type=int, default=16, help="streaming: slots per publication")
     ap.add_argument("--B", type=int, default=0, help="override the workload's chain count")
     ap.add_argument("--K", type=int, default=0, help="override the workload's slot count")
@@ -355,6 +399,13 @@ def main(argv=None) -> int:
             progress.zero_()
             binding.lbi_scan_backward_streaming(c.A, c.b, c.lamK, progress, args.chunk, hint,
                                                 math, lam=lam)
+    elif args.op == "norms":
+        spec = torch.empty((wl.B, wl.K), dtype=torch.float32, device=dev)
+        fro = torch.empty((wl.B, wl.K), dtype=torch.float32, device=dev)
+
+        def step(i):
+            c = copies[i % ncopy]
+            binding.lbi_matrix_norms(c.A, spec=spec, fro=fro)
     elif args.op == "suffix_products":
         Pout = torch.empty((wl.B, wl.K, wl.r, wl.r), dtype=torch.float32, device=dev)
         cout = torch.empty((wl.B, wl.K, wl.r), dtype=torch.float32, device=dev)
@@ -400,6 +451,10 @@ def main(argv=None) -> int:
     avg_launch_s = sum(per_launch_ms) / len(per_launch_ms) / 1e3
     ms_per_step = total_ms / args.steps
 
+    if args.op == "norms":
+        print(json.dumps(norms_record(wl, args, total_ms, avg_launch_s, per_launch_ms, ncopy)),
+              flush=True)
+        return 0
     value = combines(wl) * args.steps / (total_ms / 1e3)
     f_alg = flops_combines(wl) if args.op == "suffix_products" else flops_alg(wl)
     b_alg = bytes_export(wl) if args.op == "suffix_products" else bytes_alg(wl)

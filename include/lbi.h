@@ -49,7 +49,7 @@ extern "C" {
 /* HIP stream handle (the same type as hipStream_t). */
 typedef struct ihipStream_t *lbi_stream_t;
 
-#define LBI_ABI_VERSION 4
+#define LBI_ABI_VERSION 5
 
 /* Largest K for which a widths hint is used (longer chains run unhinted,
  * which gives identical results). */
@@ -230,6 +230,33 @@ lbi_status lbi_scan_backward_streaming(const void *A, const void *b, const void 
                                        lbi_dtype dt, lbi_stream_t stream,
                                        const int32_t *widths_host, lbi_math math,
                                        uint32_t *progress, int32_t chunk);
+
+/*
+ * The interface-Jacobian statistics of the appendix "Interface Jacobian
+ * Structure" (Table "jacobian-norm-final-checkpoint"): for each of n r x r
+ * matrices M_i, the spectral norm ||M_i||_2 and the rank-normalised Frobenius
+ * norm ||M_i||_F / sqrt(r) (the RMS singular value of a square matrix).  On
+ * the A stack (A_j = J_j^T has J_j's singular values) these are the local
+ * ||J_k||_2 and ||J_k||_F / sqrt(r); on the P output of
+ * lbi_scan_suffix_products, the suffix ||P_k||_2.
+ *
+ *   M     [n][r][r]  dt storage, row-major.
+ *   spec  [n]        OUTPUT float32, or NULL (not computed): ||M_i||_2, to
+ *                    within 2e-5 relative.  Method: repeated normalised
+ *                    squaring of M^T M on the fp32 matrix cores (24 steps),
+ *                    then a Rayleigh quotient; with no spectral-gap assumption
+ *                    the iteration's own error is at most r / (2 e 2^24)
+ *                    relative (1.4e-6 at r = 128); the rest is float32
+ *                    rounding.
+ *   fro   [n]        OUTPUT float32, or NULL: ||M_i||_F / sqrt(r).
+ *   n >= 0; r in {16, 32, 64, 128}.  At least one output; outputs must not
+ *   overlap M or each other.  A zero matrix gives 0 in both; a matrix with a
+ *   NaN or infinite entry gives NaN in both.  Zero padding of a widths-padded
+ *   tile changes neither norm, but the 1/sqrt(r) factor uses the tile width.
+ *   No workspace.
+ */
+lbi_status lbi_matrix_norms(const void *M, int64_t n, int32_t r, lbi_dtype dt, float *spec,
+                            float *fro, lbi_stream_t stream);
 
 /* A static, human-readable name for a status code. */
 const char *lbi_status_string(lbi_status s);

@@ -16,6 +16,9 @@ Bounded Interfaces"):
   the suffix products ``P_j = A_j ... A_{K-1}`` (empty product I) and offsets
   ``c_j``, obtained by folding the combine (A, b) o (A', b') = (AA', Ab' + b)
   from the right end of the chain.  fp64.
+* ``matrix_norms`` -- the statistics of the appendix "Interface Jacobian
+  Structure": spectral norm (largest singular value, from an fp64 SVD) and
+  Frobenius norm / sqrt(r) of each matrix of a stack.
 
 Every function here is pinned by the CPU tests against closed forms, exact
 rational brute force, invariants and torch autograd (see tests/test_oracle_*).
@@ -175,3 +178,28 @@ def per_chain_rel_frobenius(x: np.ndarray, ref: np.ndarray) -> np.ndarray:
     num = np.linalg.norm(x - ref, axis=1)
     den = np.linalg.norm(ref, axis=1)
     return np.where(den > 0, num / np.where(den > 0, den, 1.0), num)
+
+
+def matrix_norms(M) -> Tuple[np.ndarray, np.ndarray]:
+    """(||M_i||_2, ||M_i||_F / sqrt(r)) in float64 for M[..., r, r].
+
+    The spectral norm is the largest singular value (LAPACK SVD in fp64 on the
+    exactly widened input); the Frobenius norm is the square root of the sum
+    of squares.  r is the tile width (the last axis).
+    """
+    buf, dt = _host_array(M)
+    if dt == _BF16:
+        a = buf.to(dtype=__import__("torch").float64).numpy()
+    else:
+        a = np.asarray(buf if isinstance(buf, np.ndarray) else buf.numpy(), dtype=np.float64)
+    if a.ndim < 2 or a.shape[-1] != a.shape[-2]:
+        raise ValueError(f"M must be [..., r, r], got {a.shape}")
+    r = a.shape[-1]
+    lead = a.shape[:-2]
+    flat = a.reshape((-1, r, r))
+    spec = np.empty(flat.shape[0], dtype=np.float64)
+    fro = np.empty(flat.shape[0], dtype=np.float64)
+    for i in range(flat.shape[0]):
+        spec[i] = np.linalg.svd(flat[i], compute_uv=False)[0]
+        fro[i] = np.sqrt(np.sum(flat[i] * flat[i])) / np.sqrt(r)
+    return spec.reshape(lead), fro.reshape(lead)

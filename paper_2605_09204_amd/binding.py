@@ -75,6 +75,8 @@ def load() -> ctypes.CDLL:
                                                 ctypes.POINTER(ctypes.c_int32), ctypes.c_int,
                                                 vp, i32]
     lib.lbi_scan_backward_streaming.restype = ctypes.c_int
+    lib.lbi_matrix_norms.argtypes = [vp, i64, i32, ctypes.c_int, vp, vp, vp]
+    lib.lbi_matrix_norms.restype = ctypes.c_int
     lib.lbi_status_string.argtypes = [ctypes.c_int]
     lib.lbi_status_string.restype = ctypes.c_char_p
     lib.lbi_abi_version.argtypes = []
@@ -237,3 +239,31 @@ def lbi_scan_backward_streaming(A: torch.Tensor, b: Optional[torch.Tensor],
                                               wptr, int(math), progress.data_ptr(),
                                               int(chunk)))
     return lam
+
+
+def lbi_matrix_norms(M: torch.Tensor, want_spec: bool = True, want_fro: bool = True,
+                     spec: Optional[torch.Tensor] = None, fro: Optional[torch.Tensor] = None,
+                     stream=None):
+    """(||M_i||_2, ||M_i||_F / sqrt(r)) as float32 tensors of M's leading shape
+    (None where not wanted) for a [..., r, r] float32/bfloat16 GPU tensor M."""
+    if M.dim() < 2 or M.shape[-1] != M.shape[-2] or M.dtype not in _DTYPES or not M.is_cuda:
+        raise ValueError("M must be a [..., r, r] float32/bfloat16 GPU tensor")
+    if not M.is_contiguous():
+        raise ValueError("M must be contiguous")
+    lead = tuple(M.shape[:-2])
+    r = int(M.shape[-1])
+    n = 1
+    for d in lead:
+        n *= int(d)
+    if want_spec and spec is None:
+        spec = torch.empty(lead, dtype=torch.float32, device=M.device)
+    if want_fro and fro is None:
+        fro = torch.empty(lead, dtype=torch.float32, device=M.device)
+    for name, t in (("spec", spec), ("fro", fro)):
+        if t is not None and (tuple(t.shape) != lead or t.dtype != torch.float32
+                              or not t.is_contiguous() or t.device != M.device):
+            raise ValueError(f"{name} must be a contiguous float32 {lead} tensor on M's device")
+    _check(load().lbi_matrix_norms(
+        M.data_ptr(), n, r, _DTYPES[M.dtype], spec.data_ptr() if spec is not None else None,
+        fro.data_ptr() if fro is not None else None, _stream_ptr(stream, M.device)))
+    return spec, fro

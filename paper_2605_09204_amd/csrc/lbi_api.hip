@@ -307,6 +307,29 @@ lbi_status lbi_scan_suffix_products(const void *A, const void *b, float *P, floa
     return launch_chain_mode(cl, dt, math) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
 }
 
+lbi_status lbi_matrix_norms(const void *M, int64_t n, int32_t r, lbi_dtype dt, float *spec,
+                            float *fro, lbi_stream_t stream)
+{
+    // the shape checks of a scan over n chains of one slot
+    lbi_status st = check_common(dt, LBI_MATH_DEFAULT, r, n, 1);
+    if (st != LBI_OK)
+        return st;
+    if (n == 0)
+        return LBI_OK;
+    if (!M || (!spec && !fro))
+        return LBI_ERR_NULL;
+    if (misaligned(M) || misaligned(spec) || misaligned(fro))
+        return LBI_ERR_ALIGN;
+    const size_t esz = dt == LBI_F32 ? 4 : 2;
+    const size_t nM = (size_t)n * r * r * esz, nout = (size_t)n * sizeof(float);
+    if (overlaps(spec, nout, M, nM) || overlaps(fro, nout, M, nM) ||
+        overlaps(spec, nout, fro, nout))
+        return LBI_ERR_ALIAS;
+    return launch_norms(M, dt == LBI_BF16, n, r, spec, fro, (hipStream_t)stream) == hipSuccess
+               ? LBI_OK
+               : LBI_ERR_HIP;
+}
+
 lbi_status lbi_scan_backward_streaming(const void *A, const void *b, const void *lambda_K,
                                        float *lambda, int64_t B, int64_t K, int32_t r,
                                        lbi_dtype dt, lbi_stream_t stream,

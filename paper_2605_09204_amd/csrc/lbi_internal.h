@@ -66,6 +66,11 @@ hipError_t launch_apply(const float *Pc, const float *cc, const float *carry, fl
                         int64_t B, int64_t K, int64_t L, int32_t S, int32_t r,
                         hipStream_t stream);
 
+// Spectral norm and Frobenius norm / sqrt(r) of n r x r matrices (either
+// output may be NULL).
+hipError_t launch_norms(const void *M, bool bf16, int64_t n, int32_t r, float *spec, float *fro,
+                        hipStream_t stream);
+
 }  // namespace lbi
 
 #endif  // LBI_INTERNAL_H

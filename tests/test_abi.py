@@ -32,7 +32,7 @@ def test_header_declares_entry_points():
                             "lbi_scan_backward_workspace_bytes_ex", "lbi_scan_backward",
                             "lbi_scan_backward_widths", "lbi_scan_backward_ex",
                             "lbi_scan_suffix_products", "lbi_scan_backward_streaming",
-                            "lbi_status_string", "lbi_abi_version"])
+                            "lbi_matrix_norms", "lbi_status_string", "lbi_abi_version"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -54,7 +54,7 @@ def test_header_compiles_as_c():
 
 
 def test_version_and_status_strings():
-    assert binding.lbi_abi_version() == 4
+    assert binding.lbi_abi_version() == 5
     assert binding.lbi_status_string(0) == "LBI_OK"
     for code in range(1, 9):
         assert binding.lbi_status_string(code).startswith("LBI_ERR_")
@@ -148,3 +148,19 @@ def test_streaming_argument_errors():
     assert f(PA, PB, PL, POUT, 2, 3, 64, 0, None, None, 0, PA + 64, 4) == 8
     assert f(PA, PB, PL, POUT, 2, 3, 64, 3, None, None, 0, PP, 4) == 3
     assert f(None, None, None, None, 0, 3, 64, 0, None, None, 0, None, 4) == 0
+
+
+def test_matrix_norms_argument_errors():
+    f = binding.load().lbi_matrix_norms
+    PS, PF = 0x70000000, 0x78000000
+    assert f(PA, 5, 64, 7, PS, PF, None) == 3                  # dtype
+    assert f(PA, 5, 48, 0, PS, PF, None) == 4                  # r
+    assert f(PA, -1, 64, 0, PS, PF, None) == 2                 # n < 0
+    assert f(PA, 2**40, 128, 0, PS, PF, None) == 2             # size overflow
+    assert f(None, 5, 64, 0, PS, PF, None) == 1
+    assert f(PA, 5, 64, 0, None, None, None) == 1              # no output
+    assert f(PA + 4, 5, 64, 0, PS, PF, None) == 7
+    assert f(PA, 5, 64, 0, PS + 4, None, None) == 7
+    assert f(PA, 5, 64, 0, PA + 256, None, None) == 8          # output inside M
+    assert f(PA, 5, 64, 0, PS, PS + 16, None) == 8             # outputs overlap
+    assert f(None, 0, 64, 0, None, None, None) == 0            # n = 0: no-op
