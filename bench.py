@@ -95,7 +95,9 @@ def flops_seq(wl) -> int:
     return wl.B * sum(2 * w[j] * w[j + 1] + w[j] for j in range(wl.K))
 
 
-def bytes_alg(wl, padded: bool = False) -> int:
+def bytes_alg(wl, padded: bool = False, compact_out: bool = False) -> int:
+    """A, b, lambda_K read once at true widths (padded: whole tiles), lambda
+    written once in fp32 (padded rows included, unless compact_out)."""
     w = widths_of(wl)
     e = ELEM[wl.dtype]
     R = wl.r
@@ -105,7 +107,7 @@ def bytes_alg(wl, padded: bool = False) -> int:
         a = sum(w[j] * w[j + 1] for j in range(wl.K))
     bb = (wl.K * R if padded else sum(w[:wl.K])) if wl.affine else 0
     lk = R if padded else w[wl.K]
-    out = wl.K * R * 4
+    out = (sum(w[:wl.K]) if compact_out else wl.K * R) * 4
     return wl.B * ((a + bb + lk) * e + out)
 
 
@@ -323,6 +325,9 @@ def main(argv=None) -> int:
                          "the spectral and Frobenius norm of every A_j (lbi_matrix_norms; "
                          "reported in matrices/s)")
     ap.add_argument("--chunk", type=int, default=16, help="streaming: slots per publication")
+    ap.add_argument("--layout", choices=["padded", "compact"], default="padded",
+                    help="adjoints: R x R tiles with the widths hint (lbi_scan_backward_ex), or "
+                         "tiles at their true shapes back to back (lbi_scan_backward_ragged)")
     ap.add_argument("--B", type=int, default=0, help="override the workload's chain count")
     ap.add_argument("--K", type=int, default=0, help="override the workload's slot count")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -413,6 +418,19 @@ def main(argv=None) -> int:
         def step(i):
             c = copies[i % ncopy]
             binding.lbi_scan_suffix_products(c.A, c.b, hint, math, P=Pout, c=cout)
+    elif args.layout == "compact":
+        if args.op != "adjoints" or args.algo == "two_level" or any(
+                wk % 16 for wk in wl.interface_widths()):
+            print("--layout compact: adjoints, chain scan, widths multiples of 16",
+                  file=sys.stderr)
+            return 2
+        packed = [synth.pack_ragged(c) for c in copies]
+        lam_c = torch.empty((wl.B, sum(wl.interface_widths()[:wl.K])), dtype=torch.float32,
+                            device=dev)
+
+        def step(i):
+            c = packed[i % ncopy]
+            binding.lbi_scan_backward_ragged(c.A, c.b, c.lamK, c.widths, math, lam=lam_c)
     else:
         def step(i):
             c = copies[i % ncopy]
@@ -457,7 +475,8 @@ def main(argv=None) -> int:
         return 0
     value = combines(wl) * args.steps / (total_ms / 1e3)
     f_alg = flops_combines(wl) if args.op == "suffix_products" else flops_alg(wl)
-    b_alg = bytes_export(wl) if args.op == "suffix_products" else bytes_alg(wl)
+    b_alg = (bytes_export(wl) if args.op == "suffix_products"
+             else bytes_alg(wl, compact_out=args.layout == "compact"))
     tflops = f_alg / avg_launch_s / 1e12
     gbs = b_alg / avg_launch_s / 1e9
     mode = mode_of(wl, args.math)
@@ -493,6 +512,7 @@ def main(argv=None) -> int:
         "config": {"workload": wl.name, "B": wl.B, "K": wl.K, "r": wl.r,
                    "storage": wl.dtype, "affine": wl.affine, "arithmetic": mode,
                    "algorithm": args.algo, "workspace_bytes": need, "op": args.op,
+                   "layout": args.layout,
                    "widths": "cyclic 32/64/128" if wl.widths else "uniform",
                    "parallelism": "1 GPU, " + ("two-level scan (segments in parallel)" if need
                                                else "one workgroup per chain")},

@@ -232,6 +232,34 @@ lbi_status lbi_scan_backward_streaming(const void *A, const void *b, const void 
                                        uint32_t *progress, int32_t chunk);
 
 /*
+ * lbi_scan_backward for interfaces of different widths, stored compactly with
+ * no padding (Theorem "Bounded-Interface Backpropagation" for m_k of width r_k,
+ * so that J_k is r_{k+1} x r_k and A_j = J_j^T is r_j x r_{j+1}; the paper
+ * notes the variable-width case is analogous).
+ *
+ *   widths_host [K+1]  HOST array r_0 .. r_K, each a multiple of 16 in
+ *                      16..128; 1 <= K <= LBI_MAX_HINT_K.
+ *   A         per chain, A_0 .. A_{K-1} back to back, A_j as r_j rows x r_{j+1}
+ *             columns row-major (dt); chain stride SA = sum_{j<K} r_j r_{j+1}.
+ *   b         per chain, b_0 .. b_{K-1} back to back (r_j values each, dt);
+ *             chain stride SR = sum_{j<K} r_j; or NULL (= 0).
+ *   lambda_K  [B][r_K] dt.
+ *   lambda    OUTPUT float32, per chain lambda_0 .. lambda_{K-1} back to back
+ *             (r_j values each), chain stride SR.  Must not overlap the inputs.
+ *   math      as for lbi_scan_backward_ex.
+ * The chain scan (one workgroup per chain) on tiles of width R, the smallest
+ * of 16, 32, 64, 128 that holds every r_k.  Results equal, bit for bit, those
+ * of lbi_scan_backward_ex(..., widths, math, LBI_ALGO_CHAIN) on the same
+ * values zero-padded to R x R tiles (lambda's padding rows dropped).  No
+ * workspace.  Widths that break the rules give LBI_ERR_SHAPE, a NULL
+ * widths_host LBI_ERR_NULL.
+ */
+lbi_status lbi_scan_backward_ragged(const void *A, const void *b, const void *lambda_K,
+                                    float *lambda, int64_t B, int64_t K,
+                                    const int32_t *widths_host, lbi_dtype dt, lbi_stream_t stream,
+                                    lbi_math math);
+
+/*
  * The interface-Jacobian statistics of the appendix "Interface Jacobian
  * Structure" (Table "jacobian-norm-final-checkpoint"): for each of n r x r
  * matrices M_i, the spectral norm ||M_i||_2 and the rank-normalised Frobenius

@@ -75,6 +75,10 @@ def load() -> ctypes.CDLL:
                                                 ctypes.POINTER(ctypes.c_int32), ctypes.c_int,
                                                 vp, i32]
     lib.lbi_scan_backward_streaming.restype = ctypes.c_int
+    lib.lbi_scan_backward_ragged.argtypes = [vp, vp, vp, vp, i64, i64,
+                                             ctypes.POINTER(ctypes.c_int32), ctypes.c_int, vp,
+                                             ctypes.c_int]
+    lib.lbi_scan_backward_ragged.restype = ctypes.c_int
     lib.lbi_matrix_norms.argtypes = [vp, i64, i32, ctypes.c_int, vp, vp, vp]
     lib.lbi_matrix_norms.restype = ctypes.c_int
     lib.lbi_status_string.argtypes = [ctypes.c_int]
@@ -267,3 +271,35 @@ def lbi_matrix_norms(M: torch.Tensor, want_spec: bool = True, want_fro: bool = T
         M.data_ptr(), n, r, _DTYPES[M.dtype], spec.data_ptr() if spec is not None else None,
         fro.data_ptr() if fro is not None else None, _stream_ptr(stream, M.device)))
     return spec, fro
+
+
+def lbi_scan_backward_ragged(A: torch.Tensor, b: Optional[torch.Tensor], lambda_K: torch.Tensor,
+                             widths: Sequence[int], math: int = LBI_MATH_DEFAULT,
+                             lam: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """lambda [B, SR] (float32) from compact ragged storage: A [B, SA], b [B, SR] or None,
+    lambda_K [B, r_K], with SA = sum r_j r_{j+1} and SR = sum r_j over j < K."""
+    K = len(widths) - 1
+    if K < 1:
+        raise ValueError("widths must hold K+1 >= 2 entries")
+    SA = sum(int(widths[j]) * int(widths[j + 1]) for j in range(K))
+    SR = sum(int(widths[j]) for j in range(K))
+    if A.dim() != 2 or A.shape[1] != SA or A.dtype not in _DTYPES or not A.is_cuda:
+        raise ValueError(f"A must be a [B, {SA}] float32/bfloat16 GPU tensor")
+    B = int(A.shape[0])
+    for name, t, shape in (("b", b, (B, SR)), ("lambda_K", lambda_K, (B, int(widths[K])))):
+        if t is not None and (tuple(t.shape) != shape or t.dtype != A.dtype
+                              or t.device != A.device):
+            raise ValueError(f"{name} must be {shape} {A.dtype} on {A.device}")
+    if not all(t.is_contiguous() for t in (A, lambda_K) + ((b,) if b is not None else ())):
+        raise ValueError("tensors must be contiguous")
+    if lam is None:
+        lam = torch.empty((B, SR), dtype=torch.float32, device=A.device)
+    elif (tuple(lam.shape) != (B, SR) or lam.dtype != torch.float32 or not lam.is_contiguous()
+          or lam.device != A.device):
+        raise ValueError(f"lambda must be a contiguous float32 [B, {SR}] tensor on A's device")
+    warr, wptr = _widths_arg(widths, K)
+    _check(load().lbi_scan_backward_ragged(
+        A.data_ptr(), b.data_ptr() if b is not None else None, lambda_K.data_ptr(),
+        lam.data_ptr(), B, K, wptr, _DTYPES[A.dtype], _stream_ptr(stream, A.device),
+        int(math)))
+    return lam

@@ -307,6 +307,67 @@ lbi_status lbi_scan_suffix_products(const void *A, const void *b, float *P, floa
     return launch_chain_mode(cl, dt, math) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
 }
 
+lbi_status lbi_scan_backward_ragged(const void *A, const void *b, const void *lambda_K,
+                                    float *lambda, int64_t B, int64_t K,
+                                    const int32_t *widths_host, lbi_dtype dt, lbi_stream_t stream,
+                                    lbi_math math)
+{
+    if (dt != LBI_F32 && dt != LBI_BF16)
+        return LBI_ERR_DTYPE;
+    if (B < 0 || K < 1 || K > LBI_MAX_HINT_K)
+        return LBI_ERR_SHAPE;
+    if (!widths_host)
+        return LBI_ERR_NULL;
+    int32_t rmax = 0;
+    for (int64_t k = 0; k <= K; ++k) {
+        const int32_t wk = widths_host[k];
+        if (wk < 16 || wk > 128 || wk % 16 != 0)
+            return LBI_ERR_SHAPE;
+        rmax = wk > rmax ? wk : rmax;
+    }
+    const int32_t R = rmax <= 16 ? 16 : (rmax <= 32 ? 32 : (rmax <= 64 ? 64 : 128));
+    lbi_status st = check_common(dt, math, R, B, K);
+    if (st != LBI_OK)
+        return st;
+    int64_t totA = 0, totR = 0;
+    for (int64_t j = 0; j < K; ++j) {
+        totA += (int64_t)widths_host[j] * widths_host[j + 1];
+        totR += widths_host[j];
+    }
+    if (B == 0)
+        return LBI_OK;
+    if (!A || !lambda_K || !lambda)
+        return LBI_ERR_NULL;
+    if (misaligned(A) || misaligned(b) || misaligned(lambda_K) || misaligned(lambda))
+        return LBI_ERR_ALIGN;
+    const size_t esz = dt == LBI_F32 ? 4 : 2;
+    const size_t nA = (size_t)B * totA * esz, nb = b ? (size_t)B * totR * esz : 0;
+    const size_t nl = (size_t)B * widths_host[K] * esz, nout = (size_t)B * totR * sizeof(float);
+    if (overlaps(lambda, nout, A, nA) || overlaps(lambda, nout, b, nb) ||
+        overlaps(lambda, nout, lambda_K, nl))
+        return LBI_ERR_ALIAS;
+    ChainLaunch c;
+    memset(&c, 0, sizeof c);
+    c.args.A = A;
+    c.args.b = b;
+    c.args.lamK = lambda_K;
+    c.args.lam = lambda;
+    c.args.K = K;
+    c.args.L = K;
+    c.args.S = 1;
+    c.args.compact = 1;
+    c.args.totalA = (int32_t)totA;
+    c.args.totalR = (int32_t)totR;
+    c.B = B;
+    c.r = R;
+    c.aff = b != nullptr;
+    c.out = kOutLambda;
+    c.stream = (hipStream_t)stream;
+    if (!encode_widths(widths_host, K, R, c) || !c.hint)
+        return LBI_ERR_SHAPE;
+    return launch_chain_mode(c, dt, math) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
+}
+
 lbi_status lbi_matrix_norms(const void *M, int64_t n, int32_t r, lbi_dtype dt, float *spec,
                             float *fro, lbi_stream_t stream)
 {

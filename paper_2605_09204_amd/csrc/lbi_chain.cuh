@@ -340,7 +340,7 @@ __device__ __forceinline__ void combine_shape(int nr, int nk, f4 (&Pn)[R / 16][N
     if constexpr (NRB >= 8) combine_k<R, M, NCA, 8>(nk, Pn, P, sAbuf, li, g);
 }
 
-template <int R, int M, bool AFF, bool HINT, int NCA, int OUT>
+template <int R, int M, bool AFF, int HINT, int NCA, int OUT>
 __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const ScanArgs args)
 {
     static_assert(OUT == kOutLambda || NCA == R / 16, "composites are written whole");
@@ -372,9 +372,23 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
     const int64_t s0 = (int64_t)(blockIdx.x % args.S) * args.L;
     const int64_t K = args.K - s0 < args.L ? args.K - s0 : args.L;
     const int64_t first = beta * args.K + s0;  // global index of local slot 0
-    const E *A = (const E *)args.A + first * (int64_t)(R * R);
-    const E *bv = AFF ? (const E *)args.b + first * (int64_t)R : nullptr;
-    float *lam = OUT == kOutLambda ? args.lam + first * (int64_t)R : nullptr;
+    // compact storage (hinted whole chains): per-chain bases, and running
+    // element offsets of the A, b and lambda streams, each walked from the
+    // chain's end one slot at a time (every stream visits slots K-1, K-2, ...)
+    constexpr bool compact = HINT == kHintCompact && OUT == kOutLambda;
+    const E *A = (const E *)args.A +
+                 (compact ? beta * (int64_t)args.totalA : first * (int64_t)(R * R));
+    const E *bv = AFF ? (const E *)args.b + (compact ? beta * (int64_t)args.totalR
+                                                     : first * (int64_t)R)
+                      : nullptr;
+    float *lam = OUT == kOutLambda
+                     ? args.lam + (compact ? beta * (int64_t)args.totalR : first * (int64_t)R)
+                     : nullptr;
+    int32_t curA = args.totalA, curB = args.totalR, curL = args.totalR;
+    // (compact: one buffer resource per stream and chain; the running offset
+    // goes in the scalar offset of each access)
+    const __amdgpu_buffer_rsrc_t rsA_c = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)A, 0, compact ? args.totalA * G::ESZ : 0, kBufferWord3);
     float *Pout = OUT == kOutComposite ? args.Pout + first * (int64_t)(R * R) : nullptr;
     float *cout = OUT == kOutComposite ? args.cout : nullptr;  // NULL: not written
     if (cout)
@@ -403,31 +417,60 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
     // exactly and wait only for the slot being stored.
     auto load_tile = [&](u4 (&dst)[CPT], int64_t j, bool valid) {
         const int64_t jj = valid ? j : 0;
-        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-            (void *)(A + jj * (int64_t)(R * R)), 0, TILE_BYTES, kBufferWord3);
         int rows = valid ? R : 0, cols = R;
         if constexpr (HINT) {
             rows = valid ? 16 * width_blocks(args, s0 + jj) : 0;
             cols = 16 * width_blocks(args, s0 + jj + 1);
         }
+        if constexpr (compact) {
+            // the r_j x r_{j+1} tile sits just below the previous one
+            // (chunk i of this lane: row i * RPI + srow, columns scol ..; the
+            // lane part of the offset is the same for every chunk, the row
+            // step goes in the scalar offset)
+            if (valid)
+                curA -= rows * cols;
+            const int vbase = (srow * cols + scol) * G::ESZ;
+            const bool colok = scol < cols;
 #pragma unroll
-        for (int i = 0; i < CPT; ++i) {
-            const int c = i * T + tid;
-            const int e = c * EPC;
-            const bool ok = c < TILE_CHUNKS && (e / R) < rows && (e % R) < cols;
-            dst[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, ok ? c * 16 : kOutOfRange, 0, 0);
+            for (int i = 0; i < CPT; ++i) {
+                const int c = i * T + tid;
+                const bool ok = c < TILE_CHUNKS && colok && i * RPI + srow < rows;
+                dst[i] = __builtin_amdgcn_raw_buffer_load_b128(
+                    rsA_c, ok ? vbase : kOutOfRange, (curA + i * RPI * cols) * G::ESZ, 0);
+            }
+        } else {
+            const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                (void *)(A + jj * (int64_t)(R * R)), 0, TILE_BYTES, kBufferWord3);
+#pragma unroll
+            for (int i = 0; i < CPT; ++i) {
+                const int c = i * T + tid;
+                const int e = c * EPC;
+                const bool ok = c < TILE_CHUNKS && (e / R) < rows && (e % R) < cols;
+                dst[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, ok ? c * 16 : kOutOfRange, 0, 0);
+            }
         }
     };
     // b_j at the row this lane owns after the staging reduce (raw bits)
     auto load_b = [&](int64_t j, bool valid) -> uint32_t {
         if constexpr (AFF) {
-            const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-                (void *)(bv + (valid ? j : 0) * (int64_t)R), 0, R * G::ESZ, kBufferWord3);
-            const int off = (valid && oown) ? orow * G::ESZ : kOutOfRange;
+            int nrow = R, soff = 0;
+            const E *base = bv + (valid ? j : 0) * (int64_t)R;
+            int range = R * G::ESZ;
+            if constexpr (compact) {
+                // one resource over the chain's b; b_j just below b_{j+1}
+                nrow = valid ? 16 * width_blocks(args, s0 + j) : 0;
+                curB -= nrow;
+                base = bv;
+                range = args.totalR * G::ESZ;
+                soff = curB * G::ESZ;
+            }
+            const __amdgpu_buffer_rsrc_t rs =
+                __builtin_amdgcn_make_buffer_rsrc((void *)base, 0, range, kBufferWord3);
+            const int off = (valid && oown && orow < nrow) ? orow * G::ESZ : kOutOfRange;
             if constexpr (G::ESZ == 4)
-                return __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0);
+                return __builtin_amdgcn_raw_buffer_load_b32(rs, off, soff, 0);
             else
-                return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rs, off, 0, 0) << 16;
+                return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rs, off, soff, 0) << 16;
         } else {
             return 0u;
         }
@@ -511,10 +554,17 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
 
     // ---- per-lane constants ---------------------------------------------------
     float lk[CB];
+    {
+        // compact: lambda_K holds r_K values per chain
+        const int rK = compact ? 16 * width_blocks(args, args.K) : R;
 #pragma unroll
-    for (int t = 0; t < CB; ++t)
-        lk[t] = OUT == kOutLambda ? to_f32(((const E *)args.lamK)[beta * R + 16 * (w + NW * t) + li])
-                                  : 0.0f;
+        for (int t = 0; t < CB; ++t) {
+            const int idx = 16 * (w + NW * t) + li;
+            lk[t] = OUT == kOutLambda && idx < rK
+                        ? to_f32(((const E *)args.lamK)[beta * rK + idx])
+                        : 0.0f;
+        }
+    }
 
     // ---- the apply: partial P lambda_K over this wave's columns ---------------
     // (NB row blocks; with a widths hint, only the blocks slot s can fill)
@@ -602,10 +652,23 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
         }
         if constexpr (AFF)
             acc += sC[ring(ss)][fi];
-        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-            (void *)(lam + ss * R), 0, R * (int)sizeof(float), kBufferWord3);
-        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc), rs,
-                                              mine ? fi * (int)sizeof(float) : kOutOfRange, 0, 0);
+        // compact: lambda_s holds r_s values, just below lambda_{s+1}
+        int nrow = R, soff = 0;
+        float *base = lam + ss * R;
+        int range = R * (int)sizeof(float);
+        if constexpr (compact) {
+            // one resource over the chain's lambda; lambda_s just below lambda_{s+1}
+            nrow = valid ? 16 * width_blocks(args, s0 + ss) : 0;
+            curL -= nrow;
+            base = lam;
+            range = args.totalR * (int)sizeof(float);
+            soff = curL * (int)sizeof(float);
+        }
+        const __amdgpu_buffer_rsrc_t rs =
+            __builtin_amdgcn_make_buffer_rsrc((void *)base, 0, range, kBufferWord3);
+        __builtin_amdgcn_raw_buffer_store_b32(
+            __float_as_uint(acc), rs, mine && fi < nrow ? fi * (int)sizeof(float) : kOutOfRange,
+            soff, 0);
         // Streaming: at a publish point the storing wave group makes its
         // lambda stores visible device-wide (release: L2 written back); after
         // the next barrier one lane raises progress[beta] to the count of
@@ -775,7 +838,7 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
 
 // ---- launch -----------------------------------------------------------------
 
-template <int R, int M, bool AFF, bool HINT, int NCA, int OUT>
+template <int R, int M, bool AFF, int HINT, int NCA, int OUT>
 hipError_t launch_kernel(const ChainLaunch &c)
 {
     void *params[] = {(void *)&c.args};
@@ -784,7 +847,7 @@ hipError_t launch_kernel(const ChainLaunch &c)
                            dim3((unsigned)grid), dim3(64 * waves_for(R)), params, 0, c.stream);
 }
 
-template <int M, bool AFF, bool HINT, int OUT>
+template <int M, bool AFF, int HINT, int OUT>
 hipError_t launch_r(const ChainLaunch &c)
 {
     switch (c.r) {
@@ -813,16 +876,19 @@ hipError_t launch_chain(const ChainLaunch &c)
 {
     if (c.out == kOutComposite) {
         if (c.aff)
-            return c.hint ? launch_r<M, true, true, kOutComposite>(c)
-                          : launch_r<M, true, false, kOutComposite>(c);
-        return c.hint ? launch_r<M, false, true, kOutComposite>(c)
-                      : launch_r<M, false, false, kOutComposite>(c);
+            return c.hint ? launch_r<M, true, kHintWidths, kOutComposite>(c)
+                          : launch_r<M, true, kHintNone, kOutComposite>(c);
+        return c.hint ? launch_r<M, false, kHintWidths, kOutComposite>(c)
+                      : launch_r<M, false, kHintNone, kOutComposite>(c);
     }
+    if (c.hint && c.args.compact)
+        return c.aff ? launch_r<M, true, kHintCompact, kOutLambda>(c)
+                     : launch_r<M, false, kHintCompact, kOutLambda>(c);
     if (c.aff)
-        return c.hint ? launch_r<M, true, true, kOutLambda>(c)
-                      : launch_r<M, true, false, kOutLambda>(c);
-    return c.hint ? launch_r<M, false, true, kOutLambda>(c)
-                  : launch_r<M, false, false, kOutLambda>(c);
+        return c.hint ? launch_r<M, true, kHintWidths, kOutLambda>(c)
+                      : launch_r<M, true, kHintNone, kOutLambda>(c);
+    return c.hint ? launch_r<M, false, kHintWidths, kOutLambda>(c)
+                  : launch_r<M, false, kHintNone, kOutLambda>(c);
 }
 
 }  // namespace

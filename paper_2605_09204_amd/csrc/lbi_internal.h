@@ -19,6 +19,12 @@ enum : int { kF32 = 0, kBF16 = 1, kF32X = 2 };
 // composite (P_j, c_j) of its segment.
 enum : int { kOutLambda = 0, kOutComposite = 1 };
 
+// What the chain kernel knows of the interface widths: nothing (every tile
+// R x R), the widths hint (zero-padded R x R tiles, only the blocks a slot can
+// fill are read and multiplied), or the hint with compact storage (tiles at
+// their true shapes back to back; kOutLambda only).
+enum : int { kHintNone = 0, kHintWidths = 1, kHintCompact = 2 };
+
 struct ScanArgs {
     const void *A;     // [B][K][R][R] storage dtype
     const void *b;     // [B][K][R] storage dtype, or NULL
@@ -34,6 +40,13 @@ struct ScanArgs {
     uint32_t *progress;  // [B] or NULL (kOutLambda, whole chains): raised to the
                          // number of final adjoints after every pchunk slots
     int32_t pchunk;
+    // Compact (ragged) storage, hinted whole-chain kOutLambda launches only:
+    // slot j of a chain holds A_j as r_j x r_{j+1} row-major, b_j and lambda_j
+    // as r_j values, back to back; lambda_K as r_K values per chain.  totalA
+    // and totalR are the per-chain element counts of A and of b (= lambda).
+    int32_t compact;
+    int32_t totalA;
+    int32_t totalR;
     // ceil(r_k / 16) for k = 0..K as 4-bit fields, 8 per word (hinted launches)
     uint32_t wcode[(LBI_MAX_HINT_K + 1 + 7) / 8];
 };

@@ -258,3 +258,44 @@ def permutation_chain(B: int, K: int, r: int, dtype: str = "f32", seed: int = 0,
     lamK = torch.randint(-8, 9, (B, r), generator=gen).to(torch.float32).to(sd).to(device)
     wl = Workload(f"perm_B{B}_K{K}_r{r}", B, K, r, dtype, seed, "orthogonal", affine)
     return Inputs(A.to(sd).to(device), b, lamK, (r,) * (K + 1), wl)
+
+
+# ----------------------------------------------------------------------------
+# compact (ragged) storage: layout only, no arithmetic
+# ----------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class RaggedInputs:
+    """The operands of ``Inputs`` with every tile cut to its true shape and the
+    slots of a chain stored back to back: A [B, sum r_j r_{j+1}],
+    b [B, sum r_j] or None, lamK [B, r_K] (the layout of the library's ragged
+    entry point)."""
+
+    A: torch.Tensor
+    b: Optional[torch.Tensor]
+    lamK: torch.Tensor
+    widths: Tuple[int, ...]
+
+
+def pack_ragged(x: Inputs) -> RaggedInputs:
+    """Cut the zero-padded tiles of ``x`` to r_j x r_{j+1} and pack them."""
+    w = x.widths
+    K = len(w) - 1
+    B = x.A.shape[0]
+    A = torch.cat([x.A[:, j, :w[j], :w[j + 1]].reshape(B, -1) for j in range(K)], dim=1)
+    b = None
+    if x.b is not None:
+        b = torch.cat([x.b[:, j, :w[j]] for j in range(K)], dim=1).contiguous()
+    return RaggedInputs(A.contiguous(), b, x.lamK[:, :w[K]].contiguous(), tuple(w))
+
+
+def unpack_ragged(lam: torch.Tensor, widths: Sequence[int], R: int) -> torch.Tensor:
+    """lambda [B, sum r_j] in compact layout -> [B, K, R], zero-padded rows."""
+    K = len(widths) - 1
+    B = lam.shape[0]
+    out = torch.zeros((B, K, R), dtype=lam.dtype, device=lam.device)
+    o = 0
+    for j in range(K):
+        out[:, j, :widths[j]] = lam[:, o:o + widths[j]]
+        o += widths[j]
+    return out

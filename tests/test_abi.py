@@ -32,7 +32,8 @@ def test_header_declares_entry_points():
                             "lbi_scan_backward_workspace_bytes_ex", "lbi_scan_backward",
                             "lbi_scan_backward_widths", "lbi_scan_backward_ex",
                             "lbi_scan_suffix_products", "lbi_scan_backward_streaming",
-                            "lbi_matrix_norms", "lbi_status_string", "lbi_abi_version"])
+                            "lbi_matrix_norms", "lbi_scan_backward_ragged",
+                            "lbi_status_string", "lbi_abi_version"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -164,3 +165,26 @@ def test_matrix_norms_argument_errors():
     assert f(PA, 5, 64, 0, PA + 256, None, None) == 8          # output inside M
     assert f(PA, 5, 64, 0, PS, PS + 16, None) == 8             # outputs overlap
     assert f(None, 0, 64, 0, None, None, None) == 0            # n = 0: no-op
+
+
+def test_ragged_argument_errors():
+    f = binding.load().lbi_scan_backward_ragged
+
+    def w(vals):
+        arr = (ctypes.c_int32 * len(vals))(*vals)
+        return ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32)), arr
+
+    good, _g = w([32, 64, 128, 64])
+    assert f(PA, PB, PL, POUT, 2, 3, good, 7, None, 0) == 3           # dtype
+    assert f(PA, PB, PL, POUT, 2, 3, good, 0, None, 7) == 3           # math
+    assert f(PA, PB, PL, POUT, 2, 3, None, 0, None, 0) == 1           # no widths
+    for bad in ([32, 60, 128, 64], [32, 64, 144, 64], [0, 64, 128, 64], [8, 16, 16, 16]):
+        p, _a = w(bad)
+        assert f(PA, PB, PL, POUT, 2, 3, p, 0, None, 0) == 2, bad     # not 16..128 step 16
+    long_w, _l = w([64] * 2049)
+    assert f(PA, PB, PL, POUT, 2, 2048, long_w, 0, None, 0) == 2      # K above the hint limit
+    assert f(PA, PB, PL, POUT, 2, 0, good, 0, None, 0) == 2           # K = 0
+    assert f(None, PB, PL, POUT, 2, 3, good, 0, None, 0) == 1
+    assert f(PA, PB, PL, POUT + 4, 2, 3, good, 0, None, 0) == 7
+    assert f(PA, PB, PL, PA + 64, 2, 3, good, 0, None, 0) == 8        # output inside A
+    assert f(None, None, None, None, 0, 3, good, 0, None, 0) == 0     # B = 0: no-op

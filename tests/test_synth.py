@@ -105,3 +105,19 @@ def test_permutation_chain_is_exact():
     assert torch.equal(A.sum(-1), torch.ones(3, 5, 16))
     assert torch.equal(A.sum(-2), torch.ones(3, 5, 16))
     assert torch.equal(x.b.float(), x.b.float().round())
+
+
+def test_ragged_pack_round_trip():
+    widths = synth.cyclic_widths(7, (16, 48, 32))
+    x = synth.random_chain(3, 7, 64, dtype="bf16", seed=61, widths=widths)
+    p = synth.pack_ragged(x)
+    SA = sum(widths[j] * widths[j + 1] for j in range(7))
+    SR = sum(widths[:7])
+    assert tuple(p.A.shape) == (3, SA) and tuple(p.b.shape) == (3, SR)
+    assert tuple(p.lamK.shape) == (3, widths[7])
+    # slot 2's tile sits after slots 0 and 1, row-major at its true shape
+    o = widths[0] * widths[1] + widths[1] * widths[2]
+    tile = p.A[:, o:o + widths[2] * widths[3]].reshape(3, widths[2], widths[3])
+    assert torch.equal(tile, x.A[:, 2, :widths[2], :widths[3]])
+    # the padding that packing drops is zero, so unpacking restores b exactly
+    assert torch.equal(synth.unpack_ragged(p.b, widths, 64), x.b)
