@@ -266,6 +266,71 @@ def norms_record(wl, args, total_ms, avg_launch_s, per_launch_ms, ncopy) -> dict
     }
 
 
+def region_flops(wl) -> float:
+    """Matrix-core flops of one Phase 1 call (all B sequences, K regions): the
+    token product L x D x X per sequence and region, and the tangent products
+    with N = B r per region (Jdec: D x D, W1: X x D, W2: D x X, W_e1: D x D,
+    W_e2: r x D)."""
+    tok = 2.0 * wl.B * wl.K * wl.L * wl.D * wl.X
+    tan = 2.0 * wl.K * wl.B * wl.r * (2 * wl.D * wl.D + 2 * wl.X * wl.D + wl.r * wl.D)
+    return tok + tan
+
+
+def bench_phase1(args) -> int:
+    import torch
+    from paper_2605_09204_amd import binding, synth
+
+    if args.workload not in synth.REGION_WORKLOADS:
+        args.workload = "region_paper"
+    wl = synth.REGION_WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    print(f"[bench] generating {wl.name}", file=sys.stderr, flush=True)
+    x = synth.generate_region(wl, device=dev)
+    need = binding.lbi_region_jacobians_workspace_bytes(wl.B, wl.K, wl.L, wl.D, wl.X, wl.r)
+    ws = torch.empty((need,), dtype=torch.uint8, device=dev)
+    A = torch.empty((wl.B, wl.K, wl.r, wl.r), dtype=torch.float32, device=dev)
+    mn = torch.empty((wl.B, wl.K, wl.r), dtype=torch.float32, device=dev)
+
+    def step(i):
+        binding.lbi_region_jacobians(x.params, x.x_embed, x.m, A=A, m_next=mn, workspace=ws)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    for i in range(args.steps):
+        starts[i].record(stream)
+        step(i)
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    per = [a.elapsed_time(b) for a, b in zip(starts, ends)]
+    total_ms = starts[0].elapsed_time(ends[-1])
+    avg_s = sum(per) / len(per) / 1e3
+    f = region_flops(wl)
+    ach = f / avg_s / 1e12
+    out = {
+        "metric": "interface Jacobians/sec (Phase 1, synthetic region map)",
+        "value": wl.B * wl.K * args.steps / (total_ms / 1e3),
+        "unit": "jacobians/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": total_ms / args.steps, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded random region weights, x_embed and interface states; "
+                "no dataset or checkpoint)",
+        "config": {"workload": wl.name, "B": wl.B, "K": wl.K, "L": wl.L, "D": wl.D, "X": wl.X,
+                   "r": wl.r, "op": "phase1", "parallelism": "1 GPU"},
+        "roofline": {"bound": "mfma", "achieved": ach, "peak": PEAK["mfma_bf16_tflops"],
+                     "unit": "TFLOP/s", "frac": ach / PEAK["mfma_bf16_tflops"],
+                     "traffic": None},
+        "extra": {"avg_launch_ms": avg_s * 1e3, "min_launch_ms": min(per),
+                  "flops_per_call": f, "workspace_bytes": need},
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 # ----------------------------------------------------------------------------
 # CPU baseline: the oracle on a bounded sample of the same workload
 # ----------------------------------------------------------------------------
@@ -317,13 +382,16 @@ def main(argv=None) -> int:
                          "cores (the library default) or the fp32 matrix cores")
     ap.add_argument("--algo", choices=["auto", "chain", "two_level"], default="auto",
                     help="scan algorithm (auto: the library's choice)")
-    ap.add_argument("--op", choices=["adjoints", "suffix_products", "streaming", "norms"],
+    ap.add_argument("--op", choices=["adjoints", "suffix_products", "streaming", "norms",
+                                     "phase1"],
                     default="adjoints",
                     help="what one step computes: every lambda_j (lbi_scan_backward_ex), "
                          "every composite (P_j, c_j) (lbi_scan_suffix_products), every "
                          "lambda_j with progress published (lbi_scan_backward_streaming), or "
                          "the spectral and Frobenius norm of every A_j (lbi_matrix_norms; "
-                         "reported in matrices/s)")
+                         "reported in matrices/s), or Phase 1, the interface Jacobians of "
+                         "every region (lbi_region_jacobians; --workload region_paper or "
+                         "region_small)")
     ap.add_argument("--chunk", type=int, default=16, help="streaming: slots per publication")
     ap.add_argument("--layout", choices=["padded", "compact"], default="padded",
                     help="adjoints: R x R tiles with the widths hint (lbi_scan_backward_ex), or "
@@ -362,6 +430,8 @@ def main(argv=None) -> int:
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
     binding.load()  # fail loudly before any work if the library is missing
+    if args.op == "phase1":
+        return bench_phase1(args)
     if args.workload not in synth.WORKLOADS:
         print(f"unknown workload {args.workload}; one of {list(synth.WORKLOADS)}",
               file=sys.stderr)

@@ -49,7 +49,7 @@ extern "C" {
 /* HIP stream handle (the same type as hipStream_t). */
 typedef struct ihipStream_t *lbi_stream_t;
 
-#define LBI_ABI_VERSION 5
+#define LBI_ABI_VERSION 6
 
 /* Largest K for which a widths hint is used (longer chains run unhinted,
  * which gives identical results). */
@@ -285,6 +285,59 @@ lbi_status lbi_scan_backward_ragged(const void *A, const void *b, const void *la
  */
 lbi_status lbi_matrix_norms(const void *M, int64_t n, int32_t r, lbi_dtype dt, float *spec,
                             float *fro, lbi_stream_t stream);
+
+/*
+ * Phase 1 of Algorithm "Bounded-Interface Backpropagation" for a synthetic
+ * region map: the interface Jacobians J_k = d m_{k+1} / d m_k, from the
+ * differential applied to I_r (Eq. "jacobian-identity-construction"), of
+ *
+ *   m_{k+1} = LN(m_k + alpha_k Enc_k(pool(Phi_k(x_embed + Dec_k(m_k)))))
+ *
+ * (Eq. "concrete-region-arch") with Dec_k(m) = W_d2 silu(W_d1 m + b_d1) + b_d2,
+ * Phi_k(x) = x + W2 silu(W1 x) token by token, pool = the mean over a
+ * sequence's L tokens, Enc_k(p) = W_e2 silu(W_e1 p + b_e1) + b_e2, and LN a
+ * LayerNorm over the r interface features (gain gamma, shift beta, eps 1e-5).
+ * Every matrix of region k is the k-th of a stack; all pointers are DEVICE
+ * pointers; matrices bf16, row-major [rows][cols]; vectors float32.
+ */
+typedef struct {
+    const void *W_d1;    /* [K][D][r]  bf16 */
+    const float *b_d1;   /* [K][D] */
+    const void *W_d2;    /* [K][D][D]  bf16 */
+    const float *b_d2;   /* [K][D] */
+    const void *W1;      /* [K][X][D]  bf16 */
+    const void *W2;      /* [K][D][X]  bf16 */
+    const void *W_e1;    /* [K][D][D]  bf16 */
+    const float *b_e1;   /* [K][D] */
+    const void *W_e2;    /* [K][r][D]  bf16 */
+    const float *b_e2;   /* [K][r] */
+    const float *alpha;  /* [K] */
+    const float *gamma;  /* [K][r] */
+    const float *beta;   /* [K][r] */
+} lbi_region_params;
+
+/* Workspace bytes lbi_region_jacobians needs (0 for invalid sizes). */
+size_t lbi_region_jacobians_workspace_bytes(int64_t B, int64_t K, int64_t L, int32_t D,
+                                            int32_t X, int32_t r);
+
+/*
+ *   params   the K regions' parameters (HOST struct of device pointers).
+ *   x_embed  [B][L][D] bf16: each sequence's token embeddings (the canvas).
+ *   m        [B][K][r] float32: the interface state entering region k.
+ *   A        OUTPUT [B][K][r][r] float32: A[b][k] = J_k^T at m[b][k], the
+ *            operand layout of lbi_scan_backward.
+ *   m_next   OUTPUT [B][K][r] float32, or NULL: R_k(m[b][k]).
+ *   Sizes: B >= 0, K >= 1, L >= 1, D a multiple of 64 up to 2048, X a multiple
+ *   of 128 up to 8192, r in {16, 32, 64, 128}.  Workspace of
+ *   lbi_region_jacobians_workspace_bytes bytes, 256-byte aligned, owned by the
+ *   caller.  Outputs must not overlap the inputs or the workspace.
+ * Products run on the bf16 matrix cores with fp32 accumulation; x_embed + d
+ * and the tangent intermediates are rounded to bf16 where they feed one.
+ */
+lbi_status lbi_region_jacobians(const lbi_region_params *params, const void *x_embed,
+                                const float *m, float *A, float *m_next, int64_t B, int64_t K,
+                                int64_t L, int32_t D, int32_t X, int32_t r, void *workspace,
+                                size_t workspace_bytes, lbi_stream_t stream);
 
 /* A static, human-readable name for a status code. */
 const char *lbi_status_string(lbi_status s);

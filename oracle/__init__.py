@@ -19,6 +19,14 @@ Bounded Interfaces"):
 * ``matrix_norms`` -- the statistics of the appendix "Interface Jacobian
   Structure": spectral norm (largest singular value, from an fp64 SVD) and
   Frobenius norm / sqrt(r) of each matrix of a stack.
+* ``region_forward`` / ``region_jacobians`` -- Phase 1 of Algorithm
+  "Bounded-Interface Backpropagation" for the concrete region map of Eq.
+  "concrete-region-arch", m_{k+1} = LN(m_k + alpha_k Enc_k(pool(Phi_k(x_embed +
+  Dec_k(m_k))))), with the readings of the synthetic map (2-layer SiLU MLPs
+  for Dec and Enc, a token-wise residual SiLU MLP for Phi, mean pooling over
+  tokens, LayerNorm over the r interface features with eps 1e-5): the forward
+  written out in fp64 torch ops and J_k = dR_k(m_k) from torch autograd
+  (Eq. "jacobian-identity-construction": the differential applied to I_r).
 
 Every function here is pinned by the CPU tests against closed forms, exact
 rational brute force, invariants and torch autograd (see tests/test_oracle_*).
@@ -203,3 +211,50 @@ def matrix_norms(M) -> Tuple[np.ndarray, np.ndarray]:
         spec[i] = np.linalg.svd(flat[i], compute_uv=False)[0]
         fro[i] = np.sqrt(np.sum(flat[i] * flat[i])) / np.sqrt(r)
     return spec.reshape(lead), fro.reshape(lead)
+
+
+LN_EPS = 1e-5
+
+
+def _silu(t):
+    return t * (1.0 / (1.0 + (-t).exp()))
+
+
+def region_forward(params: dict, k: int, x_embed_b, m_bk):
+    """R_k(m) for one sequence in float64: x_embed_b [L, D], m_bk [r] (torch)."""
+    import torch
+    f = {n: v[k].to(torch.float64) for n, v in params.items()}
+    x_embed_b = x_embed_b.to(torch.float64)
+    m = m_bk.to(torch.float64)
+    # Dec_k: injects the interface state into the region (Eq. "concrete-region-injection")
+    d = f["W_d2"] @ _silu(f["W_d1"] @ m + f["b_d1"]) + f["b_d2"]
+    x_in = x_embed_b + d                               # [L, D]
+    # Phi_k: token-wise residual MLP
+    phi = x_in + _silu(x_in @ f["W1"].T) @ f["W2"].T   # [L, D]
+    # pool: mean over the L tokens
+    p = phi.mean(dim=0)
+    # Enc_k projects into the interface space
+    enc = f["W_e2"] @ _silu(f["W_e1"] @ p + f["b_e1"]) + f["b_e2"]
+    z = m + f["alpha"] * enc
+    mu = z.mean()
+    var = ((z - mu) ** 2).mean()
+    return f["gamma"] * (z - mu) / torch.sqrt(var + LN_EPS) + f["beta"]
+
+
+def region_jacobians(params: dict, x_embed, m, pairs=None) -> Tuple[np.ndarray, np.ndarray]:
+    """(J [B, K, r, r], m_next [B, K, r]) in float64: J[b, k] = d m_{k+1} / d m_k
+    of region k at m[b, k] (rows: outputs), and m_next[b, k] = R_k(m[b, k]).
+    With ``pairs`` (a list of (b, k)), only those entries are computed (the
+    rest are NaN)."""
+    import torch
+    B, K, r = m.shape
+    J = np.full((B, K, r, r), np.nan)
+    mn = np.full((B, K, r), np.nan)
+    todo = pairs if pairs is not None else [(b, k) for b in range(B) for k in range(K)]
+    for b, k in todo:
+        m0 = m[b, k].detach().to("cpu", torch.float64)
+        xb = x_embed[b].detach().to("cpu")
+        fn = lambda mm: region_forward(params, k, xb, mm)  # noqa: E731
+        J[b, k] = torch.autograd.functional.jacobian(fn, m0, vectorize=True).numpy()
+        mn[b, k] = fn(m0).detach().numpy()
+    return J, mn

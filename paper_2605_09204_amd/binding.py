@@ -28,6 +28,28 @@ LBI_ALGO_TWO_LEVEL = 2
 
 _DTYPES = {torch.float32: LBI_F32, torch.bfloat16: LBI_BF16}
 
+# lbi_region_params, in declaration order: (name, dtype, shape given K, D, X, r)
+REGION_PARAM_FIELDS = (
+    ("W_d1", torch.bfloat16, lambda K, D, X, r: (K, D, r)),
+    ("b_d1", torch.float32, lambda K, D, X, r: (K, D)),
+    ("W_d2", torch.bfloat16, lambda K, D, X, r: (K, D, D)),
+    ("b_d2", torch.float32, lambda K, D, X, r: (K, D)),
+    ("W1", torch.bfloat16, lambda K, D, X, r: (K, X, D)),
+    ("W2", torch.bfloat16, lambda K, D, X, r: (K, D, X)),
+    ("W_e1", torch.bfloat16, lambda K, D, X, r: (K, D, D)),
+    ("b_e1", torch.float32, lambda K, D, X, r: (K, D)),
+    ("W_e2", torch.bfloat16, lambda K, D, X, r: (K, r, D)),
+    ("b_e2", torch.float32, lambda K, D, X, r: (K, r)),
+    ("alpha", torch.float32, lambda K, D, X, r: (K,)),
+    ("gamma", torch.float32, lambda K, D, X, r: (K, r)),
+    ("beta", torch.float32, lambda K, D, X, r: (K, r)),
+)
+
+
+class RegionParams(ctypes.Structure):
+    """lbi_region_params: device pointers of the K regions' parameters."""
+    _fields_ = [(name, ctypes.c_void_p) for name, _, _ in REGION_PARAM_FIELDS]
+
 _lib = None
 
 
@@ -79,6 +101,11 @@ def load() -> ctypes.CDLL:
                                              ctypes.POINTER(ctypes.c_int32), ctypes.c_int, vp,
                                              ctypes.c_int]
     lib.lbi_scan_backward_ragged.restype = ctypes.c_int
+    lib.lbi_region_jacobians_workspace_bytes.argtypes = [i64, i64, i64, i32, i32, i32]
+    lib.lbi_region_jacobians_workspace_bytes.restype = sz
+    lib.lbi_region_jacobians.argtypes = [ctypes.POINTER(RegionParams), vp, vp, vp, vp, i64, i64,
+                                         i64, i32, i32, i32, vp, sz, vp]
+    lib.lbi_region_jacobians.restype = ctypes.c_int
     lib.lbi_matrix_norms.argtypes = [vp, i64, i32, ctypes.c_int, vp, vp, vp]
     lib.lbi_matrix_norms.restype = ctypes.c_int
     lib.lbi_status_string.argtypes = [ctypes.c_int]
@@ -303,3 +330,48 @@ def lbi_scan_backward_ragged(A: torch.Tensor, b: Optional[torch.Tensor], lambda_
         lam.data_ptr(), B, K, wptr, _DTYPES[A.dtype], _stream_ptr(stream, A.device),
         int(math)))
     return lam
+
+
+def lbi_region_jacobians_workspace_bytes(B: int, K: int, L: int, D: int, X: int, r: int) -> int:
+    return int(load().lbi_region_jacobians_workspace_bytes(int(B), int(K), int(L), int(D),
+                                                            int(X), int(r)))
+
+
+def lbi_region_jacobians(params: dict, x_embed: torch.Tensor, m: torch.Tensor,
+                         A: Optional[torch.Tensor] = None, m_next: Optional[torch.Tensor] = None,
+                         want_m_next: bool = True, workspace: Optional[torch.Tensor] = None,
+                         stream=None):
+    """(A [B, K, r, r] = J_k^T, m_next [B, K, r] or None), float32: Phase 1 for the
+    synthetic region map (include/lbi.h), from the parameter dict of
+    ``REGION_PARAM_FIELDS``, x_embed [B, L, D] bf16 and m [B, K, r] float32."""
+    if x_embed.dim() != 3 or x_embed.dtype != torch.bfloat16 or not x_embed.is_cuda:
+        raise ValueError("x_embed must be a [B, L, D] bfloat16 GPU tensor")
+    B, L, D = (int(v) for v in x_embed.shape)
+    if m.dim() != 3 or m.shape[0] != B or m.dtype != torch.float32 or m.device != x_embed.device:
+        raise ValueError("m must be a [B, K, r] float32 tensor on x_embed's device")
+    K, r = int(m.shape[1]), int(m.shape[2])
+    X = int(params["W1"].shape[1])
+    ptrs = []
+    for name, dt, shape in REGION_PARAM_FIELDS:
+        t = params[name]
+        if (tuple(t.shape) != shape(K, D, X, r) or t.dtype != dt or not t.is_contiguous()
+                or t.device != x_embed.device):
+            raise ValueError(f"{name} must be a contiguous {dt} {shape(K, D, X, r)} tensor "
+                             "on x_embed's device")
+        ptrs.append(t.data_ptr())
+    if not (x_embed.is_contiguous() and m.is_contiguous()):
+        raise ValueError("tensors must be contiguous")
+    if A is None:
+        A = torch.empty((B, K, r, r), dtype=torch.float32, device=x_embed.device)
+    if want_m_next and m_next is None:
+        m_next = torch.empty((B, K, r), dtype=torch.float32, device=x_embed.device)
+    need = lbi_region_jacobians_workspace_bytes(B, K, L, D, X, r)
+    if workspace is None and need > 0:
+        workspace = torch.empty((need,), dtype=torch.uint8, device=x_embed.device)
+    rp = RegionParams(*ptrs)
+    _check(load().lbi_region_jacobians(
+        ctypes.byref(rp), x_embed.data_ptr(), m.data_ptr(), A.data_ptr(),
+        m_next.data_ptr() if m_next is not None else None, B, K, L, D, X, r,
+        workspace.data_ptr() if workspace is not None else None,
+        workspace.numel() if workspace is not None else 0, _stream_ptr(stream, x_embed.device)))
+    return A, m_next

@@ -220,6 +220,49 @@ lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam,
     return LBI_OK;
 }
 
+// ---- Phase 1 (synthetic region map) ----------------------------------------
+
+constexpr int kRegionParts = 20;
+
+struct RegionPlan {
+    size_t off[kRegionParts];
+    size_t bytes;
+};
+
+// Workspace parts, each 256-byte aligned: su, sa, d, cvec, xpart, xbar, sbar,
+// gbar, p, sue, se, encv, zhat, isig, JencT (fp32) and P1, JdT, UT, dpT, TT (bf16).
+RegionPlan region_plan(int64_t B, int64_t K, int64_t L, int32_t D, int32_t X, int32_t r)
+{
+    const size_t BK = (size_t)B * K, Br = (size_t)B * r, nch = (size_t)((L + 63) / 64);
+    const size_t n[kRegionParts] = {
+        BK * D * 4, BK * D * 4, BK * D * 4, BK * X * 4, (size_t)B * nch * D * 4,
+        (size_t)B * D * 4, BK * X * 4, BK * X * 4, BK * D * 4, BK * D * 4, BK * D * 4,
+        BK * r * 4, BK * r * 4, BK * 4, (size_t)K * Br * r * 4,
+        (size_t)K * Br * D * 2, (size_t)K * Br * D * 2, (size_t)K * Br * X * 2,
+        (size_t)K * Br * D * 2, (size_t)K * Br * D * 2};
+    RegionPlan p;
+    size_t o = 0;
+    for (int i = 0; i < kRegionParts; ++i) {
+        p.off[i] = o;
+        o += align256(n[i]);
+    }
+    p.bytes = o;
+    return p;
+}
+
+bool region_sizes_ok(int64_t B, int64_t K, int64_t L, int32_t D, int32_t X, int32_t r)
+{
+    if (B < 0 || K < 1 || L < 1 || !supported_r(r))
+        return false;
+    if (D < 64 || D > 2048 || D % 64 != 0 || X < 128 || X > 8192 || X % 128 != 0)
+        return false;
+    // launch grids: the tangent products put B r / 128 row tiles in y and K in z
+    if (B > 65535 || K > 65535 || L > ((int64_t)1 << 24) ||
+        (B * r + 127) / 128 > 65535)
+        return false;
+    return B * K * (X / 128) < ((int64_t)1 << 31) - 1;
+}
+
 }  // namespace
 
 extern "C" {
@@ -366,6 +409,83 @@ lbi_status lbi_scan_backward_ragged(const void *A, const void *b, const void *la
     if (!encode_widths(widths_host, K, R, c) || !c.hint)
         return LBI_ERR_SHAPE;
     return launch_chain_mode(c, dt, math) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
+}
+
+size_t lbi_region_jacobians_workspace_bytes(int64_t B, int64_t K, int64_t L, int32_t D,
+                                            int32_t X, int32_t r)
+{
+    if (!region_sizes_ok(B, K, L, D, X, r))
+        return 0;
+    return region_plan(B, K, L, D, X, r).bytes;
+}
+
+lbi_status lbi_region_jacobians(const lbi_region_params *params, const void *x_embed,
+                                const float *m, float *A, float *m_next, int64_t B, int64_t K,
+                                int64_t L, int32_t D, int32_t X, int32_t r, void *workspace,
+                                size_t workspace_bytes, lbi_stream_t stream)
+{
+    if (!region_sizes_ok(B, K, L, D, X, r))
+        return r > 0 && !supported_r(r) ? LBI_ERR_UNSUPPORTED_R : LBI_ERR_SHAPE;
+    if (!params)
+        return LBI_ERR_NULL;
+    if (B == 0)
+        return LBI_OK;
+    const lbi_region_params &p = *params;
+    const void *ptrs[] = {p.W_d1, p.b_d1, p.W_d2, p.b_d2, p.W1, p.W2, p.W_e1, p.b_e1, p.W_e2,
+                          p.b_e2, p.alpha, p.gamma, p.beta, x_embed, m, A};
+    for (const void *q : ptrs)
+        if (!q)
+            return LBI_ERR_NULL;
+    for (const void *q : ptrs)
+        if (misaligned(q))
+            return LBI_ERR_ALIGN;
+    if (misaligned(m_next) || misaligned(workspace))
+        return LBI_ERR_ALIGN;
+    const RegionPlan plan = region_plan(B, K, L, D, X, r);
+    if (!workspace || workspace_bytes < plan.bytes)
+        return LBI_ERR_WORKSPACE;
+    const size_t nA = (size_t)B * K * r * r * 4, nm = (size_t)B * K * r * 4;
+    const size_t nx = (size_t)B * L * D * 2;
+    if (overlaps(A, nA, x_embed, nx) || overlaps(A, nA, m, nm) ||
+        overlaps(A, nA, workspace, plan.bytes) || overlaps(m_next, nm, x_embed, nx) ||
+        overlaps(m_next, nm, m, nm) || overlaps(m_next, nm, A, nA) ||
+        overlaps(m_next, nm, workspace, plan.bytes) || overlaps(workspace, plan.bytes, m, nm) ||
+        overlaps(workspace, plan.bytes, x_embed, nx))
+        return LBI_ERR_ALIAS;
+    RegionArgs q;
+    memset(&q, 0, sizeof q);
+    q.W_d1 = p.W_d1;
+    q.W_d2 = p.W_d2;
+    q.W1 = p.W1;
+    q.W2 = p.W2;
+    q.W_e1 = p.W_e1;
+    q.W_e2 = p.W_e2;
+    q.b_d1 = p.b_d1;
+    q.b_d2 = p.b_d2;
+    q.b_e1 = p.b_e1;
+    q.b_e2 = p.b_e2;
+    q.alpha = p.alpha;
+    q.gamma = p.gamma;
+    q.beta = p.beta;
+    q.x_embed = x_embed;
+    q.m = m;
+    q.A = A;
+    q.m_next = m_next;
+    q.B = B;
+    q.K = K;
+    q.L = L;
+    q.D = D;
+    q.X = X;
+    q.r = r;
+    char *w = (char *)workspace;
+    float **f32[15] = {&q.su,  &q.sa, &q.d,   &q.cvec, &q.xpart, &q.xbar, &q.sbar, &q.gbar,
+                       &q.p,   &q.sue, &q.se, &q.encv, &q.zhat,  &q.isig, &q.JencT};
+    for (int i = 0; i < 15; ++i)
+        *f32[i] = (float *)(w + plan.off[i]);
+    __bf16 **h16[5] = {&q.P1, &q.JdT, &q.UT, &q.dpT, &q.TT};
+    for (int i = 0; i < 5; ++i)
+        *h16[i] = (__bf16 *)(w + plan.off[15 + i]);
+    return launch_region_jacobians(q, (hipStream_t)stream) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
 }
 
 lbi_status lbi_matrix_norms(const void *M, int64_t n, int32_t r, lbi_dtype dt, float *spec,

@@ -1,0 +1,638 @@
+// Phase 1 of Algorithm "Bounded-Interface Backpropagation" (gfx950): the
+// interface Jacobians J_k = dR_k(m_k) I_r (Eq. "jacobian-identity-
+// construction") of the synthetic region map of Eq. "concrete-region-arch",
+//
+//   m_{k+1} = R_k(m_k) = LN(m_k + alpha_k Enc_k(pool(Phi_k(x_embed + Dec_k(m_k))))),
+//   Dec_k(m) = W_d2 silu(W_d1 m + b_d1) + b_d2          (r -> D -> D)
+//   Phi_k(x) = x + W2 silu(W1 x), token by token          (D -> X -> D)
+//   pool     = mean over the L tokens of a sequence
+//   Enc_k(p) = W_e2 silu(W_e1 p + b_e1) + b_e2          (D -> D -> r)
+//   LN       = LayerNorm over the r features, gain gamma, shift beta, eps 1e-5,
+//
+// for every sequence b and region k at once, written as A[b][k] = J_k^T, the
+// operand of the scan.
+//
+// The tangent of all r directions, taken exactly: Dec_k's differential
+// Jdec = W_d2 diag(silu'(a)) W_d1 (D x r) is the same for every token, so
+// through Phi_k and the mean pool
+//   dp = Jdec + W2 diag(gbar) W1 Jdec,   gbar = mean_l silu'(W1 x_l),
+// and p = mean_l x_embed + d + W2 sbar with sbar = mean_l silu(W1 x_l).  The
+// per-token work is therefore one product H = X_in W1^T per sequence and region
+// (L x D x X), whose epilogue reduces silu(H) and silu'(H) over the tokens; H
+// never reaches memory.  The r directions then go through skinny products with
+// N = B r (all sequences of a region at once) and the LayerNorm Jacobian
+//   J = diag(gamma) / sigma (I - 11^T / r - zhat zhat^T / r) (I + alpha Jenc).
+//
+// Arithmetic: bf16 operands on the bf16 matrix cores (v_mfma_f32_16x16x32_bf16)
+// with fp32 accumulation; x_embed + d and the tangent intermediates are rounded
+// to bf16 (round to nearest even) where they feed a product; every vector,
+// reduction and the LayerNorm part are fp32.
+//
+// The per-token product uses H = x_embed W1^T + 1 (W1 d)^T: x_embed is the
+// same bf16 operand for every region, and d enters in fp32 through the column
+// vector W1 d, added in the epilogue.
+//
+// Kernels, in launch order:
+//   bmv x2      per region, all sequences: a -> silu(a), silu'(a); d = Dec_k(m)
+//   p1          per (b, k): P1 = (diag(silu'(a)) W_d1)^T
+//   bmv         cvec = W1 d
+//   xpart/xfin  per b: mean_l x_embed (two-stage)
+//   region_gemm per (k, b, 128 columns of X): the token product and its reductions
+//   bmv x3      p = mean x_embed + d + W2 sbar; e -> silu(e), silu'(e); Enc_k
+//   ln_fwd      per (b, k): z = m + alpha Enc, LayerNorm -> m_{k+1}, zhat, 1/sigma
+//   gemm_nt x5  per k: Jdec^T, U'^T = (W1 Jdec)^T scaled by gbar, dp^T, T'^T, Jenc^T
+//   ln_jac      per (b, k): J, stored transposed as A[b][k]
+
+#include "lbi_device.cuh"
+#include "lbi_internal.h"
+
+namespace lbi {
+namespace {
+
+constexpr int kT = 256;
+constexpr int BM = 128, BN = 128, BK = 64;
+constexpr int LDK = BK + 8;  // LDS row stride in bf16 (16 rows of a b128 read hit distinct banks)
+constexpr float kLnEps = 1e-5f;
+
+__device__ __forceinline__ float sigm(float h) { return 1.0f / (1.0f + __expf(-h)); }
+__device__ __forceinline__ float silu(float h) { return h * sigm(h); }
+__device__ __forceinline__ float dsilu(float h)
+{
+    const float s = sigm(h);
+    return s * (1.0f + h * (1.0f - s));
+}
+
+__device__ __forceinline__ float bf(const __bf16 *p, int64_t i) { return (float)p[i]; }
+
+__device__ __forceinline__ float wave_sum(float x)
+{
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1)
+        x += __shfl_xor(x, o);
+    return x;
+}
+
+// ---- the tile pipeline shared by both products ---------------------------------
+// 128 rows x 64 k of a row-major bf16 matrix from (row0, k0); rows >= nrows
+// read as zero.  Thread t loads chunks c = t + 256 i: row c / 8, k 8 (c % 8).
+__device__ __forceinline__ void tile_load(u4 (&v)[4], const __bf16 *base, int64_t ld, int64_t row0,
+                                          int64_t nrows, int k0)
+{
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int c = threadIdx.x + kT * i;
+        const int64_t row = row0 + (c >> 3);
+        v[i] = row < nrows ? *(const u4 *)(base + row * ld + k0 + (c & 7) * 8)
+                           : u4{0u, 0u, 0u, 0u};
+    }
+}
+
+__device__ __forceinline__ void tile_store(const u4 (&v)[4], __bf16 *s)
+{
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int c = threadIdx.x + kT * i;
+        *(u4 *)(s + (c >> 3) * LDK + (c & 7) * 8) = v[i];
+    }
+}
+
+// acc += A_tile(128 x 64) B_tile(128 x 64)^T for this wave's 64 x 64 quarter
+// (waves 2 x 2; acc[i][j] is the 16 x 16 block (i, j); lane l holds rows
+// 4 (l / 16) + v, column l % 16 of it)
+__device__ __forceinline__ void mma_bk(f4 (&acc)[4][4], const __bf16 *sA, const __bf16 *sB, int wm,
+                                       int wn, int lane)
+{
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+        bf16x8 a[4], b[4];
+        const int kc = ks * 32 + (lane >> 4) * 8;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            a[i] = *(const bf16x8 *)(sA + (wm * 64 + i * 16 + (lane & 15)) * LDK + kc);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            b[j] = *(const bf16x8 *)(sB + (wn * 64 + j * 16 + (lane & 15)) * LDK + kc);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+}
+
+// ---- bmv: y[b][k] = W[k] v[b][k] (+ bias[k]) (+ add1[b][k]) (+ add2[b][k]) -----
+// for every sequence b of region k, fp32 sums of bf16 weights times fp32
+// vectors; outputs y, silu(y) and silu'(y) (each optional).  A wave takes 8
+// rows and 8 sequences: each weight row is read once per region and 8
+// sequences, each vector chunk serves 8 rows.
+struct BmvArgs {
+    const __bf16 *W;
+    int64_t sW;  // region stride (elements); rows N of C columns
+    const float *v;
+    int64_t v_sb, v_sk;
+    const float *bias;
+    int64_t s_bias;
+    const float *add1;
+    int64_t a1_sb, a1_sk;
+    const float *add2;
+    int64_t a2_sb, a2_sk;
+    float *y, *ys, *yd;
+    int64_t y_sb, y_sk;
+    int64_t B;
+    int N, C;
+};
+
+__global__ __launch_bounds__(kT) void bmv_kernel(BmvArgs a)
+{
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int64_t k = blockIdx.y, b0 = (int64_t)blockIdx.z * 8;
+    const int n0 = blockIdx.x * 32 + w * 8;
+    const __bf16 *W = a.W + k * a.sW;
+    float acc[64];  // [row rr][sequence bb]
+#pragma unroll
+    for (int i = 0; i < 64; ++i)
+        acc[i] = 0.0f;
+    for (int c = lane * 8; c < a.C; c += 64 * 8) {
+        float v[8][8];
+#pragma unroll
+        for (int bb = 0; bb < 8; ++bb) {
+            if (b0 + bb < a.B) {
+                const float *vp = a.v + (b0 + bb) * a.v_sb + k * a.v_sk + c;
+                const f4 x0 = *(const f4 *)vp, x1 = *(const f4 *)(vp + 4);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    v[bb][e] = x0[e];
+                    v[bb][4 + e] = x1[e];
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    v[bb][e] = 0.0f;
+            }
+        }
+#pragma unroll
+        for (int rr = 0; rr < 8; ++rr) {
+            if (n0 + rr < a.N) {
+                const bf16x8 wv = *(const bf16x8 *)(W + (int64_t)(n0 + rr) * a.C + c);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float wf = (float)wv[e];
+#pragma unroll
+                    for (int bb = 0; bb < 8; ++bb)
+                        acc[rr * 8 + bb] += wf * v[bb][e];
+                }
+            }
+        }
+    }
+    // the 64 partial sums over the 64 lanes: lane l ends with index l
+    {
+        const bool upper = (lane >> 5) & 1;
+#pragma unroll
+        for (int i = 0; i < 32; ++i) {
+            const float keep = upper ? acc[i + 32] : acc[i];
+            const float send = upper ? acc[i] : acc[i + 32];
+            acc[i] = keep + __shfl_xor(send, 32);
+        }
+        float q[32];
+#pragma unroll
+        for (int i = 0; i < 32; ++i)
+            q[i] = acc[i];
+        group_reduce<32, 32>(q, lane & 31);
+        acc[0] = q[0];
+    }
+    const int rr = lane >> 3, bb = lane & 7;
+    const int n = n0 + rr;
+    const int64_t b = b0 + bb;
+    if (n < a.N && b < a.B) {
+        float y = acc[0];
+        if (a.bias)
+            y += a.bias[k * a.s_bias + n];
+        if (a.add1)
+            y += a.add1[b * a.a1_sb + k * a.a1_sk + n];
+        if (a.add2)
+            y += a.add2[b * a.a2_sb + k * a.a2_sk + n];
+        const int64_t o = b * a.y_sb + k * a.y_sk + n;
+        if (a.y)
+            a.y[o] = y;
+        if (a.ys)
+            a.ys[o] = silu(y);
+        if (a.yd)
+            a.yd[o] = dsilu(y);
+    }
+}
+
+// ---- p1: P1[k][b r + j][h] = W_d1[k][h][j] silu'(a)[b][k][h], the A operand of Jdec^T
+__global__ __launch_bounds__(kT) void p1_kernel(RegionArgs q)
+{
+    const int64_t bk = blockIdx.x, b = bk / q.K, k = bk % q.K;
+    const int D = q.D, r = q.r;
+    const __bf16 *Wd1 = (const __bf16 *)q.W_d1 + k * (int64_t)D * r;
+    __bf16 *P1 = q.P1 + (k * q.B + b) * (int64_t)r * D;
+    const float *sa = q.sa + bk * D;
+    for (int idx = threadIdx.x; idx < r * D; idx += kT) {
+        const int j = idx / D, h = idx % D;
+        P1[idx] = (__bf16)(bf(Wd1, (int64_t)h * r + j) * sa[h]);
+    }
+}
+
+// ---- xpart / xfin: mean over the tokens of x_embed, 64-token partial sums first
+__global__ __launch_bounds__(kT) void xpart_kernel(RegionArgs q)
+{
+    const int64_t b = blockIdx.y, ch = blockIdx.x;
+    const int64_t l0 = ch * 64, l1 = l0 + 64 < q.L ? l0 + 64 : q.L;
+    const __bf16 *x = (const __bf16 *)q.x_embed + b * q.L * q.D;
+    const int64_t nch = (q.L + 63) / 64;
+    for (int c = threadIdx.x; c < q.D; c += kT) {
+        float s = 0.0f;
+        for (int64_t l = l0; l < l1; ++l)
+            s += bf(x, l * q.D + c);
+        q.xpart[(b * nch + ch) * q.D + c] = s;
+    }
+}
+
+__global__ __launch_bounds__(kT) void xfin_kernel(RegionArgs q)
+{
+    const int64_t b = blockIdx.y;
+    const int c = blockIdx.x * kT + threadIdx.x;
+    if (c >= q.D)
+        return;
+    const int64_t nch = (q.L + 63) / 64;
+    float s = 0.0f;
+    for (int64_t ch = 0; ch < nch; ++ch)
+        s += q.xpart[(b * nch + ch) * q.D + c];
+    q.xbar[b * q.D + c] = s / (float)q.L;
+}
+
+// ---- region_gemm: sbar, gbar for 128 columns of X, one sequence and region ----
+// H = x_embed[b] W1[k]^T + 1 cvec[b, k]^T (cvec = W1 d) over all L tokens in
+// 128-row tiles; the epilogue of each tile adds silu(H) and silu'(H) of its
+// valid rows into per-lane column sums.
+__global__ __launch_bounds__(kT) void region_gemm_kernel(RegionArgs q)
+{
+    __shared__ __attribute__((aligned(16))) __bf16 sA[2][BM * LDK];
+    __shared__ __attribute__((aligned(16))) __bf16 sB[2][BN * LDK];
+    __shared__ float sred[2][2][BN];
+    const int nxt = q.X / BN;
+    // workgroups that share W1[k]'s column tile (all b) run on one XCD: the
+    // scheduler deals workgroup i to XCD i % 8, so consecutive logical indices
+    // are gathered from every eighth workgroup
+    const int64_t G = (int64_t)gridDim.x;
+    int64_t lg = blockIdx.x;
+    if (G % 8 == 0)
+        lg = (lg % 8) * (G / 8) + lg / 8;
+    const int64_t b = lg % q.B;
+    const int64_t xt = (lg / q.B) % nxt;
+    const int64_t k = lg / (q.B * nxt);
+    const int D = q.D;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wm = w >> 1, wn = w & 1;
+    const int64_t bk = b * q.K + k;
+    const __bf16 *Xe = (const __bf16 *)q.x_embed + b * q.L * D;
+    const __bf16 *W = (const __bf16 *)q.W1 + (k * q.X + xt * BN) * (int64_t)D;
+    // this lane's four columns of W1 d
+    float cv[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        cv[j] = q.cvec[bk * q.X + xt * BN + wn * 64 + j * 16 + (lane & 15)];
+
+    const int nk = D / BK;
+    const int64_t ntile = (q.L + BM - 1) / BM;
+    const int64_t nit = ntile * nk;
+    float cs[4] = {0.0f, 0.0f, 0.0f, 0.0f}, cg[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    f4 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    u4 ra[4], rb[4];
+    tile_load(ra, Xe, D, 0, q.L, 0);
+    tile_load(rb, W, D, 0, BN, 0);
+    tile_store(ra, sA[0]);
+    tile_store(rb, sB[0]);
+    __syncthreads();
+    for (int64_t it = 0; it < nit; ++it) {
+        const int cur = (int)(it & 1);
+        const int64_t t = it / nk;
+        const int kb = (int)(it % nk);
+        const bool more = it + 1 < nit;
+        const int64_t tn = (it + 1) / nk;
+        const int kn = (int)((it + 1) % nk);
+        if (more) {
+            tile_load(ra, Xe, D, tn * BM, q.L, kn * BK);
+            tile_load(rb, W, D, 0, BN, kn * BK);
+        }
+        mma_bk(acc, sA[cur], sB[cur], wm, wn, lane);
+        if (kb == nk - 1) {
+            // epilogue of row tile t: column sums of silu and silu' over its
+            // valid rows, then a fresh accumulator
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int64_t row = t * BM + wm * 64 + i * 16 + 4 * (lane >> 4) + v;
+                    const bool ok = row < q.L;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const float h = acc[i][j][v] + cv[j];
+                        const float s = sigm(h);
+                        cs[j] += ok ? h * s : 0.0f;
+                        cg[j] += ok ? s * (1.0f + h * (1.0f - s)) : 0.0f;
+                    }
+                }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+        }
+        if (more) {
+            tile_store(ra, sA[cur ^ 1]);
+            tile_store(rb, sB[cur ^ 1]);
+        }
+        __syncthreads();
+    }
+    // lanes l, l ^ 16, l ^ 32, l ^ 48 hold the same columns; then the two
+    // waves of a column half through LDS
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        cs[j] += __shfl_xor(cs[j], 16);
+        cs[j] += __shfl_xor(cs[j], 32);
+        cg[j] += __shfl_xor(cg[j], 16);
+        cg[j] += __shfl_xor(cg[j], 32);
+    }
+    if (lane < 16) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            sred[0][wm][wn * 64 + j * 16 + lane] = cs[j];
+            sred[1][wm][wn * 64 + j * 16 + lane] = cg[j];
+        }
+    }
+    __syncthreads();
+    if (tid < BN) {
+        const float inv = 1.0f / (float)q.L;
+        const int64_t o = bk * q.X + xt * BN + tid;
+        q.sbar[o] = (sred[0][0][tid] + sred[0][1][tid]) * inv;
+        q.gbar[o] = (sred[1][0][tid] + sred[1][1][tid]) * inv;
+    }
+}
+
+// ---- ln_fwd: z = m + alpha Enc, LayerNorm -> m_{k+1}, zhat, 1/sigma ------------
+__global__ __launch_bounds__(64) void ln_fwd_kernel(RegionArgs q)
+{
+    const int r = q.r, lane = threadIdx.x;
+    const int64_t bk = blockIdx.x, k = bk % q.K;
+    const float alpha = q.alpha[k];
+    float z[2];
+    float s = 0.0f;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const int i = lane + 64 * u;
+        z[u] = i < r ? q.m[bk * r + i] + alpha * q.encv[bk * r + i] : 0.0f;
+        s += z[u];
+    }
+    const float mu = wave_sum(s) / (float)r;
+    float v = 0.0f;
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+        if (lane + 64 * u < r)
+            v += (z[u] - mu) * (z[u] - mu);
+    const float is = 1.0f / sqrtf(wave_sum(v) / (float)r + kLnEps);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const int i = lane + 64 * u;
+        if (i < r) {
+            const float zh = (z[u] - mu) * is;
+            q.zhat[bk * r + i] = zh;
+            if (q.m_next)
+                q.m_next[bk * r + i] = q.gamma[k * r + i] * zh + q.beta[k * r + i];
+        }
+    }
+    if (lane == 0)
+        q.isig[bk] = is;
+}
+
+// ---- gemm_nt: C[M][N] = A[M][K] B[N][K]^T per batch, with the epilogue
+//      v = acc * scale[batch][row / grp][col] + add[batch][row][col] ------------
+struct GemmOp {
+    const __bf16 *A;
+    int64_t lda, sA;
+    const __bf16 *B;
+    int64_t ldb, sB;
+    void *C;
+    int64_t ldc, sC;
+    int64_t M, N;
+    int K;
+    const float *scale;  // NULL: 1
+    int64_t s_scale_b, s_scale_g;
+    int grp;
+    const __bf16 *add;  // NULL: 0 (ld ldc, batch stride sC)
+    bool out_bf16;
+};
+
+__global__ __launch_bounds__(kT) void gemm_nt_kernel(GemmOp g)
+{
+    __shared__ __attribute__((aligned(16))) __bf16 sA[2][BM * LDK];
+    __shared__ __attribute__((aligned(16))) __bf16 sB[2][BN * LDK];
+    const int64_t z = blockIdx.z;
+    const int64_t m0 = (int64_t)blockIdx.y * BM, n0 = (int64_t)blockIdx.x * BN;
+    const __bf16 *A = g.A + z * g.sA;
+    const __bf16 *B = g.B + z * g.sB;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wm = w >> 1, wn = w & 1;
+    f4 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    u4 ra[4], rb[4];
+    tile_load(ra, A, g.lda, m0, g.M, 0);
+    tile_load(rb, B, g.ldb, n0, g.N, 0);
+    tile_store(ra, sA[0]);
+    tile_store(rb, sB[0]);
+    __syncthreads();
+    const int nk = g.K / BK;
+    for (int kb = 0; kb < nk; ++kb) {
+        const int cur = kb & 1;
+        const bool more = kb + 1 < nk;
+        if (more) {
+            tile_load(ra, A, g.lda, m0, g.M, (kb + 1) * BK);
+            tile_load(rb, B, g.ldb, n0, g.N, (kb + 1) * BK);
+        }
+        mma_bk(acc, sA[cur], sB[cur], wm, wn, lane);
+        if (more) {
+            tile_store(ra, sA[cur ^ 1]);
+            tile_store(rb, sB[cur ^ 1]);
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int64_t row = m0 + wm * 64 + i * 16 + 4 * (lane >> 4) + v;
+            if (row >= g.M)
+                continue;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int64_t col = n0 + wn * 64 + j * 16 + (lane & 15);
+                if (col >= g.N)
+                    continue;
+                float val = acc[i][j][v];
+                if (g.scale)
+                    val *= g.scale[z * g.s_scale_b + (row / g.grp) * g.s_scale_g + col];
+                const int64_t o = z * g.sC + row * g.ldc + col;
+                if (g.add)
+                    val += (float)g.add[o];
+                if (g.out_bf16)
+                    ((__bf16 *)g.C)[o] = (__bf16)val;
+                else
+                    ((float *)g.C)[o] = val;
+            }
+        }
+}
+
+// ---- ln_jac: J = diag(gamma) / sigma (I - 11^T/r - zhat zhat^T/r)(I + alpha Jenc),
+//      stored as A[b][k] = J^T ------------------------------------------------------
+__global__ __launch_bounds__(kT) void ln_jac_kernel(RegionArgs q)
+{
+    extern __shared__ float lsh[];
+    const int r = q.r;
+    float *cm = lsh;    // [r] column means of dz
+    float *cd = cm + r; // [r] column dots of dz with zhat, over r
+    float *zh = cd + r; // [r]
+    const int64_t bk = blockIdx.x, b = bk / q.K, k = bk % q.K;
+    const float alpha = q.alpha[k];
+    // Jenc^T[k][b r + j][i] = Jenc[i][j]; dz = I + alpha Jenc
+    const float *JT = q.JencT + (k * q.B + b) * (int64_t)r * r;
+    for (int i = threadIdx.x; i < r; i += kT)
+        zh[i] = q.zhat[bk * r + i];
+    __syncthreads();
+    for (int j = threadIdx.x; j < r; j += kT) {
+        float s = 0.0f, t = 0.0f;
+        for (int i = 0; i < r; ++i) {
+            const float v = (i == j ? 1.0f : 0.0f) + alpha * JT[(int64_t)j * r + i];
+            s += v;
+            t += zh[i] * v;
+        }
+        cm[j] = s / (float)r;
+        cd[j] = t / (float)r;
+    }
+    __syncthreads();
+    const float is = q.isig[bk];
+    float *A = q.A + bk * (int64_t)r * r;
+    for (int idx = threadIdx.x; idx < r * r; idx += kT) {
+        const int j = idx / r, i = idx % r;
+        const float v = (i == j ? 1.0f : 0.0f) + alpha * JT[idx];
+        A[idx] = q.gamma[k * r + i] * is * (v - cm[j] - zh[i] * cd[j]);
+    }
+}
+
+hipError_t gemm(const GemmOp &g, int64_t batch, hipStream_t st)
+{
+    const dim3 grid((unsigned)((g.N + BN - 1) / BN), (unsigned)((g.M + BM - 1) / BM),
+                    (unsigned)batch);
+    hipLaunchKernelGGL(gemm_nt_kernel, grid, dim3(kT), 0, st, g);
+    return hipGetLastError();
+}
+
+hipError_t bmv(const BmvArgs &a, int64_t K, hipStream_t st)
+{
+    const dim3 grid((unsigned)((a.N + 31) / 32), (unsigned)K, (unsigned)((a.B + 7) / 8));
+    hipLaunchKernelGGL(bmv_kernel, grid, dim3(kT), 0, st, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_region_jacobians(const RegionArgs &q, hipStream_t st)
+{
+    const int64_t BKn = q.B * q.K;
+    const int64_t Br = q.B * (int64_t)q.r;
+    const int D = q.D, X = q.X, r = q.r;
+    const int64_t K = q.K;
+    hipError_t e;
+    // a = W_d1 m + b_d1 -> silu(a) (su), silu'(a) (sa)
+    BmvArgs v{};
+    v = BmvArgs{(const __bf16 *)q.W_d1, (int64_t)D * r, q.m, K * r, r, q.b_d1, D, nullptr, 0, 0,
+                nullptr, 0, 0, nullptr, q.su, q.sa, K * D, D, q.B, D, r};
+    if ((e = bmv(v, K, st)) != hipSuccess)
+        return e;
+    // d = W_d2 silu(a) + b_d2
+    v = BmvArgs{(const __bf16 *)q.W_d2, (int64_t)D * D, q.su, K * D, D, q.b_d2, D, nullptr, 0, 0,
+                nullptr, 0, 0, q.d, nullptr, nullptr, K * D, D, q.B, D, D};
+    if ((e = bmv(v, K, st)) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(p1_kernel, dim3((unsigned)BKn), dim3(kT), 0, st, q);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    // cvec = W1 d
+    v = BmvArgs{(const __bf16 *)q.W1, (int64_t)X * D, q.d, K * D, D, nullptr, 0, nullptr, 0, 0,
+                nullptr, 0, 0, q.cvec, nullptr, nullptr, K * X, X, q.B, X, D};
+    if ((e = bmv(v, K, st)) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(xpart_kernel, dim3((unsigned)((q.L + 63) / 64), (unsigned)q.B), dim3(kT), 0,
+                       st, q);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(xfin_kernel, dim3((unsigned)((D + kT - 1) / kT), (unsigned)q.B), dim3(kT),
+                       0, st, q);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(region_gemm_kernel, dim3((unsigned)(K * q.B * (X / BN))), dim3(kT), 0, st,
+                       q);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    // p = W2 sbar + d + mean_l x_embed
+    v = BmvArgs{(const __bf16 *)q.W2, (int64_t)D * X, q.sbar, K * X, X, nullptr, 0, q.d, K * D, D,
+                q.xbar, D, 0, q.p, nullptr, nullptr, K * D, D, q.B, D, X};
+    if ((e = bmv(v, K, st)) != hipSuccess)
+        return e;
+    // e = W_e1 p + b_e1 -> silu(e) (sue), silu'(e) (se)
+    v = BmvArgs{(const __bf16 *)q.W_e1, (int64_t)D * D, q.p, K * D, D, q.b_e1, D, nullptr, 0, 0,
+                nullptr, 0, 0, nullptr, q.sue, q.se, K * D, D, q.B, D, D};
+    if ((e = bmv(v, K, st)) != hipSuccess)
+        return e;
+    // Enc = W_e2 silu(e) + b_e2
+    v = BmvArgs{(const __bf16 *)q.W_e2, (int64_t)r * D, q.sue, K * D, D, q.b_e2, r, nullptr, 0, 0,
+                nullptr, 0, 0, q.encv, nullptr, nullptr, K * r, r, q.B, r, D};
+    if ((e = bmv(v, K, st)) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(ln_fwd_kernel, dim3((unsigned)BKn), dim3(64), 0, st, q);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+
+    const __bf16 *Wd2 = (const __bf16 *)q.W_d2, *W1 = (const __bf16 *)q.W1;
+    const __bf16 *W2 = (const __bf16 *)q.W2, *We1 = (const __bf16 *)q.W_e1;
+    const __bf16 *We2 = (const __bf16 *)q.W_e2;
+    GemmOp g;
+    // Jdec^T[k] = P1[k] W_d2[k]^T                      (B r x D, K = D)
+    g = GemmOp{q.P1, D, Br * D, Wd2, D, (int64_t)D * D, q.JdT, D, Br * D, Br, D, D,
+               nullptr, 0, 0, 1, nullptr, true};
+    if ((e = gemm(g, q.K, st)) != hipSuccess)
+        return e;
+    // U'^T[k] = (Jdec^T W1[k]^T) * gbar[b][k][x]        (B r x X, K = D)
+    g = GemmOp{q.JdT, D, Br * D, W1, D, (int64_t)X * D, q.UT, X, Br * X, Br, X, D,
+               q.gbar, X, q.K * (int64_t)X, r, nullptr, true};
+    if ((e = gemm(g, q.K, st)) != hipSuccess)
+        return e;
+    // dp^T[k] = U'^T W2[k]^T + Jdec^T                   (B r x D, K = X)
+    g = GemmOp{q.UT, X, Br * X, W2, X, (int64_t)D * X, q.dpT, D, Br * D, Br, D, X,
+               nullptr, 0, 0, 1, q.JdT, true};
+    if ((e = gemm(g, q.K, st)) != hipSuccess)
+        return e;
+    // T'^T[k] = (dp^T W_e1[k]^T) * silu'(e)[b][k][h]    (B r x D, K = D)
+    g = GemmOp{q.dpT, D, Br * D, We1, D, (int64_t)D * D, q.TT, D, Br * D, Br, D, D,
+               q.se, D, q.K * (int64_t)D, r, nullptr, true};
+    if ((e = gemm(g, q.K, st)) != hipSuccess)
+        return e;
+    // Jenc^T[k] = T'^T W_e2[k]^T                        (B r x r, K = D), fp32
+    g = GemmOp{q.TT, D, Br * D, We2, D, (int64_t)r * D, q.JencT, r, Br * r, Br, r, D,
+               nullptr, 0, 0, 1, nullptr, false};
+    if ((e = gemm(g, q.K, st)) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(ln_jac_kernel, dim3((unsigned)BKn), dim3(kT), (size_t)3 * r * sizeof(float),
+                       st, q);
+    return hipGetLastError();
+}
+
+}  // namespace lbi

@@ -1,10 +1,11 @@
-"""Seeded synthetic inputs for the interface-adjoint scan.
+"""Seeded synthetic inputs for the interface-adjoint scan and its Phase 1.
 
-This module draws the operands of the scan and nothing else: the stack of
-interface-Jacobian transposes ``A[B, K, R, R]``, the affine terms ``b[B, K, R]``
-and the terminal adjoints ``lambda_K[B, R]``.  It contains none of the scan's
-arithmetic, so the HIP path and the CPU oracle can both consume what it makes
-without sharing any of the method.
+This module draws operands and nothing else: the stack of interface-Jacobian
+transposes ``A[B, K, R, R]``, the affine terms ``b[B, K, R]`` and the terminal
+adjoints ``lambda_K[B, R]`` of the scan; the weights, token embeddings and
+interface states of a synthetic region map (Phase 1); and the compact packing
+of ragged tiles.  It contains none of the method's arithmetic, so the HIP path
+and the CPU oracle can both consume what it makes without sharing any of it.
 
 Layout (row-major, C-contiguous):
   * ``A[beta, j]`` is the transpose of the interface Jacobian
@@ -299,3 +300,83 @@ def unpack_ragged(lam: torch.Tensor, widths: Sequence[int], R: int) -> torch.Ten
         out[:, j, :widths[j]] = lam[:, o:o + widths[j]]
         o += widths[j]
     return out
+
+
+# ----------------------------------------------------------------------------
+# Phase 1 inputs: a synthetic bounded-interface region map with random weights
+# ----------------------------------------------------------------------------
+#
+# Region k maps the interface state m_k (r values per sequence) to
+#   m_{k+1} = LN(m_k + alpha_k Enc_k(pool(Phi_k(x_embed + Dec_k(m_k)))))
+# (Eq. "concrete-region-arch").  The parameters drawn here, per region k:
+#   Dec_k = 2-layer MLP r -> D -> D:  W_d1 [D, r], b_d1 [D], W_d2 [D, D], b_d2 [D]
+#   Phi_k = token-wise residual MLP D -> X -> D:  W1 [X, D], W2 [D, X]
+#   Enc_k = 2-layer MLP D -> D -> r:  W_e1 [D, D], b_e1 [D], W_e2 [r, D], b_e2 [r]
+#   alpha_k (scalar), LN gain gamma [r] and shift beta [r].
+# Matrices ~ N(0, 1/fan_in), rounded to bf16; biases ~ N(0, 0.01) and the
+# rest in fp32.  x_embed [B, L, D] ~ N(0, 1) in bf16; m [B, K, r] ~ N(0, 1) in
+# fp32 (each region's Jacobian depends only on its own m_k and x_embed).
+
+@dataclasses.dataclass(frozen=True)
+class RegionWorkload:
+    name: str
+    B: int  # sequences
+    K: int  # regions
+    L: int  # tokens per sequence
+    D: int  # model width
+    X: int  # width of the region MLP
+    r: int  # interface width
+    seed: int
+
+
+REGION_WORKLOADS = {
+    # The illustrative configuration of the paper's cost analysis (about 1B
+    # parameters): B=8, L=2048, D=768, X=3072 (Transformer MLP width), r=64,
+    # K=16 (32 layers at 2 layers per region).
+    "region_paper": RegionWorkload("region_paper", B=8, K=16, L=2048, D=768, X=3072, r=64,
+                                   seed=5),
+    # small enough for the fp64 autograd oracle in seconds
+    "region_small": RegionWorkload("region_small", B=2, K=3, L=256, D=128, X=256, r=32, seed=6),
+}
+
+REGION_MATRICES = ("W_d1", "W_d2", "W1", "W2", "W_e1", "W_e2")
+REGION_VECTORS = ("b_d1", "b_d2", "b_e1", "b_e2", "alpha", "gamma", "beta")
+
+
+@dataclasses.dataclass
+class RegionInputs:
+    params: dict  # name -> tensor, stacked over the K regions
+    x_embed: torch.Tensor  # [B, L, D] bf16
+    m: torch.Tensor  # [B, K, r] fp32
+    workload: RegionWorkload
+
+    def to(self, device) -> "RegionInputs":
+        return RegionInputs({k: v.to(device) for k, v in self.params.items()},
+                            self.x_embed.to(device), self.m.to(device), self.workload)
+
+
+def generate_region(wl: RegionWorkload, device="cpu") -> RegionInputs:
+    """Draw the region parameters, x_embed and m of ``wl`` (seeded)."""
+    device = torch.device(device)
+    gen = torch.Generator(device=device)
+    gen.manual_seed(_chunk_seed(wl.seed, 777))
+    K, D, X, r = wl.K, wl.D, wl.X, wl.r
+
+    def mat(rows, cols):
+        w = torch.randn((K, rows, cols), generator=gen, device=device, dtype=torch.float64)
+        return (w / math.sqrt(cols)).to(torch.float32).to(torch.bfloat16)
+
+    def vec(n, scale=0.1):
+        v = torch.randn((K, n), generator=gen, device=device, dtype=torch.float64) * scale
+        return v.to(torch.float32)
+
+    p = {"W_d1": mat(D, r), "b_d1": vec(D), "W_d2": mat(D, D), "b_d2": vec(D),
+         "W1": mat(X, D), "W2": mat(D, X),
+         "W_e1": mat(D, D), "b_e1": vec(D), "W_e2": mat(r, D), "b_e2": vec(r)}
+    p["alpha"] = (0.5 + 0.5 * torch.rand((K,), generator=gen, device=device,
+                                         dtype=torch.float64)).to(torch.float32)
+    p["gamma"] = (1.0 + vec(r)).contiguous()
+    p["beta"] = vec(r)
+    x = torch.randn((wl.B, wl.L, D), generator=gen, device=device, dtype=torch.float64)
+    m = torch.randn((wl.B, K, r), generator=gen, device=device, dtype=torch.float64)
+    return RegionInputs(p, x.to(torch.float32).to(torch.bfloat16), m.to(torch.float32), wl)

@@ -33,6 +33,7 @@ def test_header_declares_entry_points():
                             "lbi_scan_backward_widths", "lbi_scan_backward_ex",
                             "lbi_scan_suffix_products", "lbi_scan_backward_streaming",
                             "lbi_matrix_norms", "lbi_scan_backward_ragged",
+                            "lbi_region_jacobians_workspace_bytes", "lbi_region_jacobians",
                             "lbi_status_string", "lbi_abi_version"])
 
 
@@ -55,7 +56,7 @@ def test_header_compiles_as_c():
 
 
 def test_version_and_status_strings():
-    assert binding.lbi_abi_version() == 5
+    assert binding.lbi_abi_version() == 6
     assert binding.lbi_status_string(0) == "LBI_OK"
     for code in range(1, 9):
         assert binding.lbi_status_string(code).startswith("LBI_ERR_")
@@ -188,3 +189,36 @@ def test_ragged_argument_errors():
     assert f(PA, PB, PL, POUT + 4, 2, 3, good, 0, None, 0) == 7
     assert f(PA, PB, PL, PA + 64, 2, 3, good, 0, None, 0) == 8        # output inside A
     assert f(None, None, None, None, 0, 3, good, 0, None, 0) == 0     # B = 0: no-op
+
+
+def test_region_argument_errors():
+    f = binding.load().lbi_region_jacobians
+    wsb = binding.lbi_region_jacobians_workspace_bytes
+    assert wsb(8, 16, 2048, 768, 3072, 64) > 0
+    assert wsb(8, 16, 2048, 760, 3072, 64) == 0      # D not a multiple of 64
+    assert wsb(8, 16, 2048, 768, 3000, 64) == 0      # X not a multiple of 128
+    assert wsb(8, 16, 2048, 768, 3072, 48) == 0      # r
+    assert wsb(8, 0, 2048, 768, 3072, 64) == 0       # K = 0
+    base = 0x10000000
+    good = binding.RegionParams(*[base + 0x01000000 * i for i in range(13)])
+    XE, M, A, MN, WS = 0x30000000, 0x31000000, 0x32000000, 0x33000000, 0x40000000
+    need = wsb(2, 3, 256, 128, 256, 32)
+
+    def call(params=good, xe=XE, m=M, a=A, mn=MN, B=2, K=3, L=256, D=128, X=256, r=32, ws=WS,
+             nws=None):
+        return f(ctypes.byref(params) if params is not None else None, xe, m, a, mn, B, K, L, D,
+                 X, r, ws, need if nws is None else nws, None)
+
+    assert call(r=48) == 4                           # unsupported r
+    assert call(D=100) == 2 and call(X=200) == 2 and call(L=0) == 2 and call(K=0) == 2
+    assert call(params=None) == 1
+    assert call(xe=None) == 1 and call(m=None) == 1 and call(a=None) == 1
+    bad = binding.RegionParams(*[base + 0x01000000 * i for i in range(13)])
+    bad.W1 = None
+    assert call(params=bad) == 1
+    bad.W1 = base + 8                                # misaligned weight
+    assert call(params=bad) == 7
+    assert call(ws=None) == 5 and call(nws=need - 1) == 5
+    assert call(a=XE + 256) == 8                     # A inside x_embed
+    assert call(mn=WS + 1024) == 8                   # m_next inside the workspace
+    assert call(B=0, xe=None, m=None, a=None) == 0   # B = 0: no-op
