@@ -51,7 +51,7 @@ namespace {
 
 constexpr int kT = 256;
 constexpr int BM = 128, BN = 128, BK = 64;
-constexpr int LDK = BK + 8;  // LDS row stride in bf16 (16 rows of a b128 read hit distinct banks)
+constexpr int TILE = 128 * BK;  // bf16 elements of one LDS tile (no padding)
 constexpr float kLnEps = 1e-5f;
 
 __device__ __forceinline__ float sigm(float h) { return 1.0f / (1.0f + __expf(-h)); }
@@ -73,18 +73,43 @@ __device__ __forceinline__ float wave_sum(float x)
 }
 
 // ---- the tile pipeline shared by both products ---------------------------------
-// 128 rows x 64 k of a row-major bf16 matrix from (row0, k0); rows >= nrows
-// read as zero.  Thread t loads chunks c = t + 256 i: row c / 8, k 8 (c % 8).
-__device__ __forceinline__ void tile_load(u4 (&v)[4], const __bf16 *base, int64_t ld, int64_t row0,
-                                          int64_t nrows, int k0)
+// LDS tile layout: 128 rows of 64 bf16 (eight 16-byte chunks), two rows per
+// 256-byte line, chunk q of row R at line R / 2, slot ((R & 1) 8 + q) ^ (R / 2 & 7).
+// The 16 lanes that a b128 access serves together then touch 16 distinct
+// slots (all 64 banks) both when they read one chunk of 16 consecutive rows
+// (an MFMA operand) and when they write the 8 chunks of 2 consecutive rows.
+__device__ __forceinline__ int lds_off(int row, int q)
+{
+    return (row >> 1) * 128 + ((((row & 1) << 3) + q) ^ ((row >> 1) & 7)) * 8;
+}
+
+// 128 rows x 64 k of a row-major bf16 matrix (row stride ld) from row0, k0;
+// rows >= nrows read as zero.  Thread t loads chunks c = t + 256 i: row c / 8,
+// chunk c % 8, at the per-lane byte offsets voff (tile_offsets).  One buffer
+// resource per call starts at (row0, k0) and ends with the last valid row, so
+// the lanes of missing rows fall outside it and read zero (no lane masks).
+__device__ __forceinline__ void tile_offsets(uint32_t (&voff)[4], int ld)
 {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int c = threadIdx.x + kT * i;
-        const int64_t row = row0 + (c >> 3);
-        v[i] = row < nrows ? *(const u4 *)(base + row * ld + k0 + (c & 7) * 8)
-                           : u4{0u, 0u, 0u, 0u};
+        voff[i] = (uint32_t)(((c >> 3) * ld + (c & 7) * 8) * 2);
     }
+}
+
+__device__ __forceinline__ void tile_load(u4 (&v)[4], const uint32_t (&voff)[4],
+                                          const __bf16 *base, int64_t ld, int64_t row0,
+                                          int64_t nrows, int k0)
+{
+    const int64_t left = nrows - row0;
+    const int valid = left < 128 ? (int)left : 128;
+    // the last valid row's chunks end at most 2 (ld - k0 - 64) bytes before
+    // valid * ld * 2 - k0 * 2; the first missing row starts at or past it
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(base + row0 * ld + k0), 0, (int)(valid * (int)ld * 2 - k0 * 2), kBufferWord3);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        v[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, voff[i], 0, 0);
 }
 
 __device__ __forceinline__ void tile_store(const u4 (&v)[4], __bf16 *s)
@@ -92,7 +117,7 @@ __device__ __forceinline__ void tile_store(const u4 (&v)[4], __bf16 *s)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int c = threadIdx.x + kT * i;
-        *(u4 *)(s + (c >> 3) * LDK + (c & 7) * 8) = v[i];
+        *(u4 *)(s + lds_off(c >> 3, c & 7)) = v[i];
     }
 }
 
@@ -105,13 +130,13 @@ __device__ __forceinline__ void mma_bk(f4 (&acc)[4][4], const __bf16 *sA, const 
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
         bf16x8 a[4], b[4];
-        const int kc = ks * 32 + (lane >> 4) * 8;
+        const int q = ks * 4 + (lane >> 4);
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-            a[i] = *(const bf16x8 *)(sA + (wm * 64 + i * 16 + (lane & 15)) * LDK + kc);
+            a[i] = *(const bf16x8 *)(sA + lds_off(wm * 64 + i * 16 + (lane & 15), q));
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-            b[j] = *(const bf16x8 *)(sB + (wn * 64 + j * 16 + (lane & 15)) * LDK + kc);
+            b[j] = *(const bf16x8 *)(sB + lds_off(wn * 64 + j * 16 + (lane & 15), q));
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -221,33 +246,51 @@ __global__ __launch_bounds__(kT) void bmv_kernel(BmvArgs a)
     }
 }
 
-// ---- p1: P1[k][b r + j][h] = W_d1[k][h][j] silu'(a)[b][k][h], the A operand of Jdec^T
+// ---- p1: P1[k][b r + j][h] = W_d1[k][h][j] silu'(a)[b][k][h], the A operand of
+//      Jdec^T; 64 values of h per workgroup, transposed through LDS so that
+//      both the reads of W_d1 rows and the writes of P1 rows are contiguous
 __global__ __launch_bounds__(kT) void p1_kernel(RegionArgs q)
 {
+    __shared__ float tile[64][129];  // [h - h0][j], r <= 128
     const int64_t bk = blockIdx.x, b = bk / q.K, k = bk % q.K;
     const int D = q.D, r = q.r;
+    const int h0 = blockIdx.y * 64;
     const __bf16 *Wd1 = (const __bf16 *)q.W_d1 + k * (int64_t)D * r;
-    __bf16 *P1 = q.P1 + (k * q.B + b) * (int64_t)r * D;
     const float *sa = q.sa + bk * D;
-    for (int idx = threadIdx.x; idx < r * D; idx += kT) {
-        const int j = idx / D, h = idx % D;
-        P1[idx] = (__bf16)(bf(Wd1, (int64_t)h * r + j) * sa[h]);
+    for (int idx = threadIdx.x; idx < 64 * r; idx += kT) {
+        const int hh = idx / r, j = idx % r;
+        tile[hh][j] = bf(Wd1, (int64_t)(h0 + hh) * r + j) * sa[h0 + hh];
+    }
+    __syncthreads();
+    __bf16 *P1 = q.P1 + (k * q.B + b) * (int64_t)r * D;
+    for (int idx = threadIdx.x; idx < 64 * r; idx += kT) {
+        const int j = idx / 64, hh = idx % 64;
+        P1[(int64_t)j * D + h0 + hh] = (__bf16)tile[hh][j];
     }
 }
 
 // ---- xpart / xfin: mean over the tokens of x_embed, 64-token partial sums first
 __global__ __launch_bounds__(kT) void xpart_kernel(RegionArgs q)
 {
+    // thread t sums the 8 columns 8t .. 8t + 7 over the workgroup's 64 tokens
     const int64_t b = blockIdx.y, ch = blockIdx.x;
     const int64_t l0 = ch * 64, l1 = l0 + 64 < q.L ? l0 + 64 : q.L;
-    const __bf16 *x = (const __bf16 *)q.x_embed + b * q.L * q.D;
-    const int64_t nch = (q.L + 63) / 64;
-    for (int c = threadIdx.x; c < q.D; c += kT) {
-        float s = 0.0f;
-        for (int64_t l = l0; l < l1; ++l)
-            s += bf(x, l * q.D + c);
-        q.xpart[(b * nch + ch) * q.D + c] = s;
+    const int c = threadIdx.x * 8;
+    if (c >= q.D)
+        return;
+    const __bf16 *x = (const __bf16 *)q.x_embed + b * q.L * q.D + c;
+    float s[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+    for (int64_t l = l0; l < l1; ++l) {
+        const bf16x8 v = *(const bf16x8 *)(x + l * q.D);
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            s[e] += (float)v[e];
     }
+    const int64_t nch = (q.L + 63) / 64;
+    float *o = q.xpart + (b * nch + ch) * q.D + c;
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        o[e] = s[e];
 }
 
 __global__ __launch_bounds__(kT) void xfin_kernel(RegionArgs q)
@@ -269,8 +312,8 @@ __global__ __launch_bounds__(kT) void xfin_kernel(RegionArgs q)
 // valid rows into per-lane column sums.
 __global__ __launch_bounds__(kT) void region_gemm_kernel(RegionArgs q)
 {
-    __shared__ __attribute__((aligned(16))) __bf16 sA[2][BM * LDK];
-    __shared__ __attribute__((aligned(16))) __bf16 sB[2][BN * LDK];
+    __shared__ __attribute__((aligned(16))) __bf16 sA[2][TILE];
+    __shared__ __attribute__((aligned(16))) __bf16 sB[2][TILE];
     __shared__ float sred[2][2][BN];
     const int nxt = q.X / BN;
     // workgroups that share W1[k]'s column tile (all b) run on one XCD: the
@@ -295,48 +338,65 @@ __global__ __launch_bounds__(kT) void region_gemm_kernel(RegionArgs q)
         cv[j] = q.cvec[bk * q.X + xt * BN + wn * 64 + j * 16 + (lane & 15)];
 
     const int nk = D / BK;
-    const int64_t ntile = (q.L + BM - 1) / BM;
-    const int64_t nit = ntile * nk;
-    float cs[4] = {0.0f, 0.0f, 0.0f, 0.0f}, cg[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    const int ntile = (int)((q.L + BM - 1) / BM);
+    // column sums of s = sigmoid(h), silu(h) = h s and silu(h) s
+    float s1[4] = {0.0f, 0.0f, 0.0f, 0.0f}, s2[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    float s3[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     f4 acc[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
             acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-    u4 ra[4], rb[4];
-    tile_load(ra, Xe, D, 0, q.L, 0);
-    tile_load(rb, W, D, 0, BN, 0);
-    tile_store(ra, sA[0]);
-    tile_store(rb, sB[0]);
-    __syncthreads();
-    for (int64_t it = 0; it < nit; ++it) {
-        const int cur = (int)(it & 1);
-        const int64_t t = it / nk;
-        const int kb = (int)(it % nk);
-        const bool more = it + 1 < nit;
-        const int64_t tn = (it + 1) / nk;
-        const int kn = (int)((it + 1) % nk);
-        if (more) {
-            tile_load(ra, Xe, D, tn * BM, q.L, kn * BK);
-            tile_load(rb, W, D, 0, BN, kn * BK);
+    // Loads run three stages ahead of the products (stage = one 64-wide k
+    // block of one row tile), rotating through three register sets: a fifth
+    // of the loads miss L2 and come from the last-level cache or HBM.
+    int lt = 0, lkb = 0;  // next stage to load
+    uint32_t voff[4];
+    tile_offsets(voff, D);
+    auto load = [&](u4 (&va)[4], u4 (&vb)[4]) {
+        if (lt < ntile) {
+            tile_load(va, voff, Xe, D, (int64_t)lt * BM, q.L, lkb * BK);
+            tile_load(vb, voff, W, D, 0, BN, lkb * BK);
         }
+        if (++lkb == nk) {
+            lkb = 0;
+            ++lt;
+        }
+    };
+    u4 ra0[4], rb0[4], ra1[4], rb1[4], ra2[4], rb2[4];
+    load(ra0, rb0);
+    tile_store(ra0, sA[0]);
+    tile_store(rb0, sB[0]);
+    load(ra0, rb0);
+    load(ra1, rb1);
+    load(ra2, rb2);
+    __syncthreads();
+    int t = 0, kb = 0, cur = 0;  // the stage being multiplied
+    // one stage: products from LDS[cur]; the row tile's epilogue after its
+    // last k block; then the next stage (held in va, vb) into LDS[cur ^ 1] and
+    // the stage three ahead into va, vb
+    auto body = [&](u4 (&va)[4], u4 (&vb)[4]) -> bool {
         mma_bk(acc, sA[cur], sB[cur], wm, wn, lane);
         if (kb == nk - 1) {
-            // epilogue of row tile t: column sums of silu and silu' over its
-            // valid rows, then a fresh accumulator
+            // epilogue of row tile t over its valid rows: with s = sigmoid(h),
+            // silu = h s and silu' = s + silu - silu s, so the sums of s, silu
+            // and silu s carry both reductions
+            const int64_t rbase = (int64_t)t * BM + wm * 64 + 4 * (lane >> 4);
+            const bool full = (int64_t)(t + 1) * BM <= q.L;
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
-                    const int64_t row = t * BM + wm * 64 + i * 16 + 4 * (lane >> 4) + v;
-                    const bool ok = row < q.L;
+                    const float w8 = full || rbase + i * 16 + v < q.L ? 1.0f : 0.0f;
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
                         const float h = acc[i][j][v] + cv[j];
-                        const float s = sigm(h);
-                        cs[j] += ok ? h * s : 0.0f;
-                        cg[j] += ok ? s * (1.0f + h * (1.0f - s)) : 0.0f;
+                        const float sg = w8 * sigm(h);
+                        const float sl = h * sg;
+                        s1[j] += sg;
+                        s2[j] += sl;
+                        s3[j] = fmaf(sl, sg, s3[j]);
                     }
                 }
 #pragma unroll
@@ -345,16 +405,34 @@ __global__ __launch_bounds__(kT) void region_gemm_kernel(RegionArgs q)
                 for (int j = 0; j < 4; ++j)
                     acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
         }
-        if (more) {
-            tile_store(ra, sA[cur ^ 1]);
-            tile_store(rb, sB[cur ^ 1]);
+        if (++kb == nk) {
+            kb = 0;
+            ++t;
         }
+        if (t >= ntile)
+            return false;
+        tile_store(va, sA[cur ^ 1]);
+        tile_store(vb, sB[cur ^ 1]);
         __syncthreads();
+        cur ^= 1;
+        load(va, vb);
+        return true;
+    };
+    for (;;) {
+        if (!body(ra0, rb0))
+            break;
+        if (!body(ra1, rb1))
+            break;
+        if (!body(ra2, rb2))
+            break;
     }
     // lanes l, l ^ 16, l ^ 32, l ^ 48 hold the same columns; then the two
     // waves of a column half through LDS
+    float cs[4], cg[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
+        cs[j] = s2[j];
+        cg[j] = s1[j] + s2[j] - s3[j];
         cs[j] += __shfl_xor(cs[j], 16);
         cs[j] += __shfl_xor(cs[j], 32);
         cg[j] += __shfl_xor(cg[j], 16);
@@ -431,8 +509,8 @@ struct GemmOp {
 
 __global__ __launch_bounds__(kT) void gemm_nt_kernel(GemmOp g)
 {
-    __shared__ __attribute__((aligned(16))) __bf16 sA[2][BM * LDK];
-    __shared__ __attribute__((aligned(16))) __bf16 sB[2][BN * LDK];
+    __shared__ __attribute__((aligned(16))) __bf16 sA[2][TILE];
+    __shared__ __attribute__((aligned(16))) __bf16 sB[2][TILE];
     const int64_t z = blockIdx.z;
     const int64_t m0 = (int64_t)blockIdx.y * BM, n0 = (int64_t)blockIdx.x * BN;
     const __bf16 *A = g.A + z * g.sA;
@@ -444,26 +522,42 @@ __global__ __launch_bounds__(kT) void gemm_nt_kernel(GemmOp g)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
             acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-    u4 ra[4], rb[4];
-    tile_load(ra, A, g.lda, m0, g.M, 0);
-    tile_load(rb, B, g.ldb, n0, g.N, 0);
-    tile_store(ra, sA[0]);
-    tile_store(rb, sB[0]);
-    __syncthreads();
     const int nk = g.K / BK;
-    for (int kb = 0; kb < nk; ++kb) {
-        const int cur = kb & 1;
-        const bool more = kb + 1 < nk;
-        if (more) {
-            tile_load(ra, A, g.lda, m0, g.M, (kb + 1) * BK);
-            tile_load(rb, B, g.ldb, n0, g.N, (kb + 1) * BK);
+    int lkb = 0;  // next k block to load (two ahead of the products)
+    uint32_t voa[4], vob[4];
+    tile_offsets(voa, (int)g.lda);
+    tile_offsets(vob, (int)g.ldb);
+    auto load = [&](u4 (&va)[4], u4 (&vb)[4]) {
+        if (lkb < nk) {
+            tile_load(va, voa, A, g.lda, m0, g.M, lkb * BK);
+            tile_load(vb, vob, B, g.ldb, n0, g.N, lkb * BK);
         }
+        ++lkb;
+    };
+    u4 ra0[4], rb0[4], ra1[4], rb1[4];
+    load(ra0, rb0);
+    tile_store(ra0, sA[0]);
+    tile_store(rb0, sB[0]);
+    load(ra0, rb0);
+    load(ra1, rb1);
+    __syncthreads();
+    int kb = 0, cur = 0;
+    auto body = [&](u4 (&va)[4], u4 (&vb)[4]) -> bool {
         mma_bk(acc, sA[cur], sB[cur], wm, wn, lane);
-        if (more) {
-            tile_store(ra, sA[cur ^ 1]);
-            tile_store(rb, sB[cur ^ 1]);
-        }
+        if (++kb == nk)
+            return false;
+        tile_store(va, sA[cur ^ 1]);
+        tile_store(vb, sB[cur ^ 1]);
         __syncthreads();
+        cur ^= 1;
+        load(va, vb);
+        return true;
+    };
+    for (;;) {
+        if (!body(ra0, rb0))
+            break;
+        if (!body(ra1, rb1))
+            break;
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -562,7 +656,7 @@ hipError_t launch_region_jacobians(const RegionArgs &q, hipStream_t st)
                 nullptr, 0, 0, q.d, nullptr, nullptr, K * D, D, q.B, D, D};
     if ((e = bmv(v, K, st)) != hipSuccess)
         return e;
-    hipLaunchKernelGGL(p1_kernel, dim3((unsigned)BKn), dim3(kT), 0, st, q);
+    hipLaunchKernelGGL(p1_kernel, dim3((unsigned)BKn, (unsigned)(D / 64)), dim3(kT), 0, st, q);
     if ((e = hipGetLastError()) != hipSuccess)
         return e;
     // cvec = W1 d
