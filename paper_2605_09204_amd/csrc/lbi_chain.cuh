@@ -97,6 +97,8 @@ template <int R, int M, int NCA> struct Geo {
     static constexpr int ESZ = sizeof(E);
     static constexpr int PITCH = R + Mode<M>::PAD;               // LDS row pitch in L
     static constexpr bool PERM = sizeof(L) == 2 && R >= 32;      // k blocks in operand order
+    static constexpr bool SWZ = PERM;                            // swizzled bf16 planes
+    static constexpr int PLANE = SWZ ? R * R : R * PITCH;        // elements per LDS plane
     static constexpr int EPC = 16 / ESZ;                         // elements per 16-byte chunk
     static constexpr int TILE_CHUNKS = R * R / EPC;
     static constexpr int CPT = (TILE_CHUNKS + T - 1) / T;        // chunks per thread
@@ -123,12 +125,25 @@ template <bool PERM> __device__ __forceinline__ int lds_col(int col)
     }
 }
 
+// Element offset of (row, physical column pc) in a swizzled bf16 plane (R >=
+// 32): rows hold C = R / 8 chunks of 16 bytes, 16 / C rows share a 256-byte
+// line, and chunk q of row r sits in slot (r % (16 / C)) C + (q ^ (r / (16 / C)) % C).
+// The 16 lanes that an access serves together then hit 16 distinct slots
+// (all 64 banks), both for an operand read (one chunk of 16 consecutive rows)
+// and for the staging writes (whole rows, 256 bytes at a time).
+template <int R> __device__ __forceinline__ int swz_pos(int row, int pc)
+{
+    constexpr int C = R / 8, RHO = 16 / C;
+    const int line = row / RHO, q = pc >> 3;
+    return line * 128 + ((row % RHO) * C + (q ^ (line % C))) * 8 + (pc & 7);
+}
+
 // A operand (8 bf16 values) of row block I, k pair p, from one LDS plane.
 template <int R, int PITCH>
 __device__ __forceinline__ bf16x8 a_operand(const __bf16 *plane, int I, int p, int li, int g)
 {
     if constexpr (R >= 32) {
-        return *(const bf16x8 *)&plane[(16 * I + li) * PITCH + 32 * p + 8 * g];
+        return *(const bf16x8 *)&plane[swz_pos<R>(16 * I + li, 32 * p + 8 * g)];
     } else {
         const bf16x4 a0 = *(const bf16x4 *)&plane[li * PITCH + 4 * g];
         const bf16x4 z = {};
@@ -160,7 +175,7 @@ __device__ __forceinline__ void combine(f4 (&Pn)[R / 16][NCA / waves_for(R)],
     };
     using G = Geo<R, M, NCA>;
     constexpr int NRB = G::NRB, CB = G::CB, PITCH = G::PITCH;
-    constexpr int PLANE = R * PITCH;
+    constexpr int PLANE = G::PLANE;
 #pragma unroll
     for (int I = 0; I < NRB; ++I)
 #pragma unroll
@@ -354,7 +369,14 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
     constexpr bool PERM = G::PERM;
     constexpr int NPF = G::NPF, WPF = G::WPF, NWF = G::NWF;
     constexpr int TILE_BYTES = R * R * G::ESZ;
-    constexpr int PLANE = R * PITCH;
+    constexpr int PLANE = G::PLANE;
+    // element offset of (row, physical column) in an LDS plane
+    auto tpos = [](int row, int pc) {
+        if constexpr (G::SWZ)
+            return swz_pos<R>(row, pc);
+        else
+            return row * PITCH + pc;
+    };
 
     __shared__ __attribute__((aligned(16))) L sA[2][PLANES * PLANE];
     // c_s in a ring of four, indexed (K - s) mod 4
@@ -517,20 +539,20 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
             st_part[i] = s;
         }
         if (TILE_CHUNKS % T == 0 || c < TILE_CHUNKS) {
-            L *dst = &sA[buf][row * PITCH];
+            L *dst = sA[buf];
             if constexpr (M == kF32) {
-                *(u4 *)&dst[scol] = src;
+                *(u4 *)&dst[tpos(row, scol)] = src;
             } else if constexpr (M == kBF16) {
                 if constexpr (PERM) {
-                    *(u2 *)&dst[lds_col<PERM>(scol)] = u2{src[0], src[1]};
-                    *(u2 *)&dst[lds_col<PERM>(scol + 4)] = u2{src[2], src[3]};
+                    *(u2 *)&dst[tpos(row, lds_col<PERM>(scol))] = u2{src[0], src[1]};
+                    *(u2 *)&dst[tpos(row, lds_col<PERM>(scol + 4))] = u2{src[2], src[3]};
                 } else {
-                    *(u4 *)&dst[scol] = src;
+                    *(u4 *)&dst[tpos(row, scol)] = src;
                 }
             } else {
                 const Split2 s01 = split_pair(x[0], x[1]);
                 const Split2 s23 = split_pair(x[2], x[3]);
-                const int pos = lds_col<PERM>(scol);
+                const int pos = tpos(row, lds_col<PERM>(scol));
                 *(u2 *)&dst[pos] = u2{s01.h, s23.h};
                 *(u2 *)&dst[PLANE + pos] = u2{s01.m, s23.m};
                 *(u2 *)&dst[2 * PLANE + pos] = u2{s01.l, s23.l};
@@ -618,15 +640,19 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
         }
     };
     // ---- streaming: slots after which progress is published --------------------
-    // every pchunk final slots, and the last one
-    auto publish_point = [&](int64_t x) { return x == 0 || (K - x) % args.pchunk == 0; };
+    // every pchunk final slots, and the last one.  Slots are finalized in the
+    // order K-1, K-2, ..., so a countdown over the finalized slots decides it
+    // (finalize(x) sets pub_now; the publish_before(x) that follows it uses it).
+    int32_t pub_left = args.pchunk;
+    bool pub_now = false;
     // Called after a barrier that follows finalize(x): the storing wave group
     // fenced its stores of slots x .. K-1 before it, so the count K - x can be
     // published.
     auto publish_before = [&](int64_t x) {
         if constexpr (OUT == kOutLambda) {
-            if (args.progress && x <= K - 1 && publish_point(x) && tid == 0)
+            if (args.progress && pub_now && tid == 0)
                 atomicMax(&args.progress[beta], (uint32_t)(K - x));
+            pub_now = false;
         }
     };
     // ---- lambda_s = sum of the wave partials + c_s, stored by one wave group ---
@@ -674,8 +700,13 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
         // the next barrier one lane raises progress[beta] to the count of
         // final adjoints (see publish_before).
         if constexpr (OUT == kOutLambda) {
-            if (args.progress && valid && publish_point(ss) && w / WPF == 0)
-                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            if (args.progress && valid) {
+                pub_now = --pub_left == 0 || ss == 0;
+                if (pub_left == 0)
+                    pub_left = args.pchunk;
+                if (pub_now && w / WPF == 0)
+                    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            }
         }
     };
     // ---- the composite (P_s, c_s) of local slot s, to global memory -----------
@@ -731,7 +762,7 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 const int row = 16 * I + 4 * g + v, col = 16 * (w + NW * t) + li;
-                const int pos = row * PITCH + lds_col<PERM>(col & ~3) + (col & 3);
+                const int pos = tpos(row, lds_col<PERM>(col & ~3) + (col & 3));
                 if constexpr (M == kF32X)
                     P[I][t][v] = (to_f32(sA[0][pos]) + to_f32(sA[0][PLANE + pos])) +
                                  to_f32(sA[0][2 * PLANE + pos]);
