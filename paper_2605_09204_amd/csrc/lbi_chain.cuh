@@ -105,7 +105,9 @@ template <int R, int M, int NCA> struct Geo {
     static constexpr int LPR = R / EPC;                          // staging lanes per tile row
     static constexpr int RPI = T / LPR;                          // tile rows per chunk index
     static constexpr int SHIFT_S = ilog2(LPR) - ilog2(CPT);      // staging reduce layout
-    static constexpr int NPF = (M == kBF16 && R <= 64) ? 3 : 2;  // slots prefetched
+    // slots prefetched (bf16 at r <= 32 takes a third; at r = 64 the third
+    // costs the fifth wave per SIMD, which is worth more)
+    static constexpr int NPF = (M == kBF16 && R <= 32) ? 3 : 2;
     static constexpr int WPF = R > 64 ? R / 64 : 1;              // waves per finalize
     static constexpr int NWF = NW / WPF;                         // finalizing wave groups
     static_assert(NCA % NW == 0 && CB >= 1, "tile geometry");
