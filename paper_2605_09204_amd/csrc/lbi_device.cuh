@@ -93,25 +93,36 @@ template <typename T> __device__ __forceinline__ float to_f32(T x) { return (flo
 __device__ __forceinline__ uint32_t fbits(float x) { return __float_as_uint(x); }
 __device__ __forceinline__ float bitsf(uint32_t u) { return __uint_as_float(u); }
 
-// Upper halves of two words, packed: the bf16 pair (lo, hi).
-__device__ __forceinline__ uint32_t pack_hi(uint32_t lo, uint32_t hi)
-{
-    return __builtin_amdgcn_perm(hi, lo, 0x07060302u);
-}
-
 // Three bf16 parts of two fp32 values with h + m + l == x exactly (for
-// normal x): h keeps the top 8 significant bits, m the next 8 of the
-// remainder, l the rest, which has at most 8 significant bits.
+// normal x), each packed as the bf16 pair (part of x0, part of x1):
+//   h = x rounded to the nearest bf16; the remainder r = x - h is exact and
+//       has at most 16 significant bits (|r| <= half an ulp of h);
+//   m = r rounded to the nearest bf16; l = r - m is exact and has at most 8
+//       significant bits, so it is a bf16 value.
+// Rounding to nearest, rather than truncating, keeps every part centred: the
+// partial products that the six-product scheme leaves out then have no sign
+// bias, and their rounding does not build up along a long chain of products.
+// Each remainder is one bf16 dot product, x - 1 * part, which is exact.  The
+// selectors (-1, 0) and (0, -1) are passed in registers: an inline constant
+// in a packed bf16 operand is not read as a bf16 pair.
 struct Split2 {
     uint32_t h, m, l;
 };
 __device__ __forceinline__ Split2 split_pair(float x0, float x1)
 {
-    const uint32_t h0 = fbits(x0) & kHighHalf, h1 = fbits(x1) & kHighHalf;
-    const float r0 = x0 - bitsf(h0), r1 = x1 - bitsf(h1);
-    const uint32_t m0 = fbits(r0) & kHighHalf, m1 = fbits(r1) & kHighHalf;
-    const float l0 = r0 - bitsf(m0), l1 = r1 - bitsf(m1);
-    return {pack_hi(h0, h1), pack_hi(m0, m1), pack_hi(fbits(l0), fbits(l1))};
+    uint32_t sel0 = 0x0000BF80u, sel1 = 0xBF800000u;  // bf16 pairs (-1, 0), (0, -1)
+    asm("" : "+v"(sel0), "+v"(sel1));
+    const bf16x2 neg0 = __builtin_bit_cast(bf16x2, sel0);
+    const bf16x2 neg1 = __builtin_bit_cast(bf16x2, sel1);
+    const bf16x2 h = __builtin_convertvector(f2{x0, x1}, bf16x2);
+    const float r0 = __builtin_amdgcn_fdot2_f32_bf16(h, neg0, x0, false);
+    const float r1 = __builtin_amdgcn_fdot2_f32_bf16(h, neg1, x1, false);
+    const bf16x2 m = __builtin_convertvector(f2{r0, r1}, bf16x2);
+    const float l0 = __builtin_amdgcn_fdot2_f32_bf16(m, neg0, r0, false);
+    const float l1 = __builtin_amdgcn_fdot2_f32_bf16(m, neg1, r1, false);
+    const bf16x2 l = __builtin_convertvector(f2{l0, l1}, bf16x2);
+    return {__builtin_bit_cast(uint32_t, h), __builtin_bit_cast(uint32_t, m),
+            __builtin_bit_cast(uint32_t, l)};
 }
 
 }  // namespace
