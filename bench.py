@@ -386,7 +386,7 @@ def main(argv=None) -> int:
     ap.add_argument("--math", choices=["split", "mfma"], default="split",
                     help="float32 arithmetic: three-part bf16 splits on the bf16 matrix "
                          "cores (the library default) or the fp32 matrix cores")
-    ap.add_argument("--algo", choices=["auto", "chain", "two_level"], default="auto",
+    ap.add_argument("--algo", choices=["auto", "chain", "two_level", "chain_wave"], default="auto",
                     help="scan algorithm (auto: the library's choice)")
     ap.add_argument("--op", choices=["adjoints", "suffix_products", "streaming", "norms",
                                      "phase1"],
@@ -405,6 +405,8 @@ def main(argv=None) -> int:
     ap.add_argument("--B", type=int, default=0, help="override the workload's chain count")
     ap.add_argument("--K", type=int, default=0, help="override the workload's slot count")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--per-launch", action="store_true",
+                    help="print every timed launch's duration (µs) to stderr")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="also run a plain device copy of this many MiB (for PMC scaling)")
     ap.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -467,7 +469,8 @@ def main(argv=None) -> int:
 
     math = binding.LBI_MATH_F32_SPLIT if args.math == "split" else binding.LBI_MATH_F32_MFMA
     algo = {"auto": binding.LBI_ALGO_AUTO, "chain": binding.LBI_ALGO_CHAIN,
-            "two_level": binding.LBI_ALGO_TWO_LEVEL}[args.algo]
+            "two_level": binding.LBI_ALGO_TWO_LEVEL,
+            "chain_wave": binding.LBI_ALGO_CHAIN_WAVE}[args.algo]
     need = binding.lbi_scan_backward_workspace_bytes_ex(wl.B, wl.K, wl.r,
                                                          0 if wl.dtype == "f32" else 1, algo)
     ws = torch.empty((need,), dtype=torch.uint8, device=dev) if need else None
@@ -541,6 +544,9 @@ def main(argv=None) -> int:
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
     per_launch_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    if args.per_launch:
+        print("[bench] per-launch µs: " + " ".join(f"{t * 1e3:.1f}" for t in per_launch_ms),
+              file=sys.stderr, flush=True)
     total_ms = starts[0].elapsed_time(ends[-1])
     avg_launch_s = sum(per_launch_ms) / len(per_launch_ms) / 1e3
     ms_per_step = total_ms / args.steps

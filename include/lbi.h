@@ -49,7 +49,7 @@ extern "C" {
 /* HIP stream handle (the same type as hipStream_t). */
 typedef struct ihipStream_t *lbi_stream_t;
 
-#define LBI_ABI_VERSION 6
+#define LBI_ABI_VERSION 7
 
 /* Largest K for which a widths hint is used (longer chains run unhinted,
  * which gives identical results). */
@@ -80,11 +80,13 @@ typedef enum {
                              * costs K serial slot steps, the two-level scan
                              * K/S slot steps over B*S workgroups, S carry
                              * steps and 8 B K r^2 bytes of composite traffic;
-                             * few long chains go two-level.  K < 16: chain     */
+                             * few long chains go two-level.  K < 16: chain.
+                             * Otherwise bf16 with r <= 32 and B <= 8192 goes
+                             * to LBI_ALGO_CHAIN_WAVE                           */
     LBI_ALGO_CHAIN = 1,     /* one workgroup folds each whole chain right to
                              * left (K-1 combines, span K) and applies every
                              * composite to lambda_K as it forms; no workspace */
-    LBI_ALGO_TWO_LEVEL = 2  /* each chain is cut into S ~ sqrt(2K) segments; a
+    LBI_ALGO_TWO_LEVEL = 2, /* each chain is cut into S ~ sqrt(2K) segments; a
                              * workgroup per segment folds it into its local
                              * composites (kept in the workspace), a carry pass
                              * applies the segment aggregates right to left to
@@ -92,6 +94,19 @@ typedef enum {
                              * lambda_j = P_j carry + c_j at once (span K/S
                              * combines + S matrix-vector products); needs
                              * workspace, B * K < 2^31                           */
+    LBI_ALGO_CHAIN_WAVE = 3 /* the chain scan with one 64-lane wavefront per
+                             * chain instead of a workgroup: the same combines
+                             * and apply, with A_j loaded straight into
+                             * matrix-core operand registers and no barriers;
+                             * for many chains (a batch of token positions).
+                             * bf16 storage and r <= 64 only (else
+                             * LBI_ERR_DTYPE / LBI_ERR_UNSUPPORTED_R); a widths
+                             * hint is accepted and not needed; no workspace.
+                             * At r <= 32 it is 1.3-1.9x faster than the
+                             * workgroup kernel for B <= 4096; at r = 64 it
+                             * holds two waves per SIMD and is about 10%
+                             * slower.  AUTO picks it for bf16, r <= 32,
+                             * B <= 8192                                       */
 } lbi_algo;
 
 typedef enum {
@@ -118,7 +133,8 @@ size_t lbi_scan_backward_workspace_bytes(int64_t B, int64_t K, int32_t r, lbi_dt
 
 /*
  * As lbi_scan_backward_workspace_bytes, for a given algorithm: 0 for
- * LBI_ALGO_CHAIN; for LBI_ALGO_TWO_LEVEL about 4 B K r (r + 1) bytes (the
+ * LBI_ALGO_CHAIN and LBI_ALGO_CHAIN_WAVE; for LBI_ALGO_TWO_LEVEL about
+ * 4 B K r (r + 1) bytes (the
  * segment composites in float32, plus the carries).
  */
 size_t lbi_scan_backward_workspace_bytes_ex(int64_t B, int64_t K, int32_t r, lbi_dtype dt,

@@ -25,6 +25,7 @@ LBI_MATH_F32_SPLIT = 2
 LBI_ALGO_AUTO = 0
 LBI_ALGO_CHAIN = 1
 LBI_ALGO_TWO_LEVEL = 2
+LBI_ALGO_CHAIN_WAVE = 3
 
 _DTYPES = {torch.float32: LBI_F32, torch.bfloat16: LBI_BF16}
 

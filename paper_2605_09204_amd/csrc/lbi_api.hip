@@ -87,18 +87,25 @@ double slot_us(lbi_dtype dt, int32_t r)
 // chains hold more than 1280 waves.  Two-level scan: K/S slot steps over B*S
 // workgroups, S carry steps, and the composites written and read once
 // (8 B K r^2 bytes at 5.8 TB/s).
+// Chains that the two-level scan does not take: bf16 chains of width <= 32
+// go to the wavefront-per-chain kernel (no barrier, no LDS staging), which
+// measured 1.3-1.9x faster than the workgroup kernel up to B = 4096 and no
+// slower up to 8192; at r = 64 its registers allow two waves per SIMD and the
+// workgroup kernel is faster.
 lbi_algo resolve_algo(lbi_algo algo, int64_t B, int64_t K, int32_t r, lbi_dtype dt)
 {
-    if (algo == LBI_ALGO_CHAIN || algo == LBI_ALGO_TWO_LEVEL)
+    if (algo != LBI_ALGO_AUTO)
         return algo;
+    const lbi_algo chain =
+        dt == LBI_BF16 && r <= 32 && B <= 8192 ? LBI_ALGO_CHAIN_WAVE : LBI_ALGO_CHAIN;
     if (K < 16 || !two_level_possible(B, K))
-        return LBI_ALGO_CHAIN;
+        return chain;
     const double ts = slot_us(dt, r), w = waves_for_r(r), cap = 1280.0;
-    const double chain = 6.0 + (double)K * ts * fmax(1.0, (double)B * w / cap);
+    const double t_chain = 6.0 + (double)K * ts * fmax(1.0, (double)B * w / cap);
     const TwoLevelPlan p = two_level_plan(B, K, r);
     const double two = 12.0 + (double)p.L * ts * fmax(1.0, (double)B * p.S * w / cap) +
                        0.22 * p.S * sqrt(r / 64.0) + 8.0 * (double)B * K * r * r / 5.8e6;
-    return two < chain ? LBI_ALGO_TWO_LEVEL : LBI_ALGO_CHAIN;
+    return two < t_chain ? LBI_ALGO_TWO_LEVEL : chain;
 }
 
 lbi_status check_common(lbi_dtype dt, lbi_math math, int32_t r, int64_t B, int64_t K)
@@ -155,10 +162,15 @@ lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam,
     lbi_status st = check_common(dt, math, r, B, K);
     if (st != LBI_OK)
         return st;
-    if (algo != LBI_ALGO_AUTO && algo != LBI_ALGO_CHAIN && algo != LBI_ALGO_TWO_LEVEL)
+    if (algo != LBI_ALGO_AUTO && algo != LBI_ALGO_CHAIN && algo != LBI_ALGO_TWO_LEVEL &&
+        algo != LBI_ALGO_CHAIN_WAVE)
         return LBI_ERR_DTYPE;
     if (algo == LBI_ALGO_TWO_LEVEL && !two_level_possible(B, K))
         return LBI_ERR_SHAPE;
+    if (algo == LBI_ALGO_CHAIN_WAVE && dt != LBI_BF16)
+        return LBI_ERR_DTYPE;
+    if (algo == LBI_ALGO_CHAIN_WAVE && r > 64)
+        return LBI_ERR_UNSUPPORTED_R;
     if (B == 0)
         return LBI_OK;
     if (!A || !lamK || !lam)
@@ -191,11 +203,13 @@ lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam,
     if (!encode_widths(widths, K, r, c))
         return LBI_ERR_SHAPE;
 
-    if (use == LBI_ALGO_CHAIN) {
+    if (use == LBI_ALGO_CHAIN || use == LBI_ALGO_CHAIN_WAVE) {
         c.args.lam = lam;
         c.args.L = K;
         c.args.S = 1;
         c.out = kOutLambda;
+        if (use == LBI_ALGO_CHAIN_WAVE)
+            return launch_chain_wave_bf16(c) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
         return launch_chain_mode(c, dt, math) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
     }
 
@@ -272,7 +286,8 @@ size_t lbi_scan_backward_workspace_bytes_ex(int64_t B, int64_t K, int32_t r, lbi
 {
     if (check_common(dt, LBI_MATH_DEFAULT, r, B, K) != LBI_OK || B == 0)
         return 0;
-    if (algo != LBI_ALGO_AUTO && algo != LBI_ALGO_CHAIN && algo != LBI_ALGO_TWO_LEVEL)
+    if (algo != LBI_ALGO_AUTO && algo != LBI_ALGO_CHAIN && algo != LBI_ALGO_TWO_LEVEL &&
+        algo != LBI_ALGO_CHAIN_WAVE)
         return 0;
     if (resolve_algo(algo, B, K, r, dt) != LBI_ALGO_TWO_LEVEL || !two_level_possible(B, K))
         return 0;

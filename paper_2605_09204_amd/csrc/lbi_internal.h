@@ -67,6 +67,11 @@ hipError_t launch_chain_f32(const ChainLaunch &c);
 hipError_t launch_chain_f32x(const ChainLaunch &c);
 hipError_t launch_chain_bf16(const ChainLaunch &c);
 
+// The chain scan with one wavefront per chain (bf16 storage, r <= 64, whole
+// chains, kOutLambda without progress counters; a widths hint is ignored).
+bool chain_wave_supported(const ChainLaunch &c);
+hipError_t launch_chain_wave_bf16(const ChainLaunch &c);
+
 // Segment carries of the two-level scan: carry[beta][d] is lambda at the end
 // of segment d (lambda_K for the last), obtained by applying the segment
 // aggregates (the composites at each segment's first slot) right to left.

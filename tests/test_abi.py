@@ -56,7 +56,7 @@ def test_header_compiles_as_c():
 
 
 def test_version_and_status_strings():
-    assert binding.lbi_abi_version() == 6
+    assert binding.lbi_abi_version() == 7
     assert binding.lbi_status_string(0) == "LBI_OK"
     for code in range(1, 9):
         assert binding.lbi_status_string(code).startswith("LBI_ERR_")
@@ -126,6 +126,17 @@ def test_two_level_needs_workspace():
     # workspace overlapping an input
     assert call(B=2, K=512, algo=2, ws=PA + 64, wsb=need) == 8
     assert call(B=2, K=512, algo=9) == 3
+
+
+def test_chain_wave_argument_errors():
+    # one wavefront per chain: bf16 storage and r <= 64 only, no workspace;
+    # rejected before any pointer is touched
+    assert call(algo=3) == 3                    # fp32 storage: LBI_ERR_DTYPE
+    assert call(dt=1, r=128, algo=3) == 4       # LBI_ERR_UNSUPPORTED_R
+    assert call(dt=1, r=64, algo=3, A=None) == 1
+    for r in (16, 32, 64):
+        assert binding.lbi_scan_backward_workspace_bytes_ex(4096, 32, r, 1, 3) == 0
+        assert binding.lbi_scan_backward_workspace_bytes_ex(2, 512, r, 1, 3) == 0
 
 
 def test_suffix_products_argument_errors():

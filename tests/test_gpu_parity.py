@@ -45,7 +45,7 @@ MODE_IDS = ["f32-split", "f32-mfma", "bf16"]
 
 
 ALGO = {"auto": binding.LBI_ALGO_AUTO, "chain": binding.LBI_ALGO_CHAIN,
-        "two_level": binding.LBI_ALGO_TWO_LEVEL}
+        "two_level": binding.LBI_ALGO_TWO_LEVEL, "chain_wave": binding.LBI_ALGO_CHAIN_WAVE}
 
 
 def run_gpu(x: synth.Inputs, widths=None, stream=None, math=None, algo=None):
@@ -142,6 +142,53 @@ def test_stress_shapes(B, K, r, dtype, arith, algo):
         lam = run_gpu(x, math=arith, algo=algo)
         assert_close(lam.cpu().numpy(), ref(x), TOL[dtype] if dtype == "f32" else BF16_EXPECTED,
                      f"B{B} K{K} r{r} {dtype} {arith} {algo} affine={affine}")
+
+
+@pytest.mark.parametrize("r", [16, 32, 64])
+@pytest.mark.parametrize("B,K", [(1, 1), (3, 2), (2, 3), (5, 31), (4, 33), (1, 130), (70, 9)])
+def test_chain_wave_shapes(B, K, r):
+    """One wavefront per chain (bf16 storage, r <= 64), ragged K and B, with
+    and without b, against the oracle; with a widths hint it is unchanged."""
+    _say(f"[wave] B={B} K={K} r={r}")
+    for affine in (True, False):
+        x = synth.random_chain(B, K, r, dtype="bf16", seed=K * 11 + r, affine=affine)
+        lam = run_gpu(x, algo="chain_wave")
+        assert_close(lam.cpu().numpy(), ref(x), BF16_EXPECTED,
+                     f"wave B{B} K{K} r{r} affine={affine}")
+        hinted = run_gpu(x, widths=[r] * (K + 1), algo="chain_wave")
+        assert torch.equal(lam, hinted)
+
+
+@pytest.mark.parametrize("r", [16, 32, 64])
+def test_chain_wave_permutation_exact(r):
+    for K in (1, 7, 40):
+        x = synth.permutation_chain(3, K, r, dtype="bf16", seed=K + r)
+        got = run_gpu(x, algo="chain_wave").cpu().numpy().astype(np.float64)
+        assert np.array_equal(got, ref(x)), f"K={K}"
+
+
+def test_chain_wave_token_batches_and_auto():
+    """Token batches (K = 32, b = NULL, bf16): at r = 32 AUTO runs the
+    wavefront-per-chain scan, which equals the explicit call bit for bit and
+    meets the oracle on sampled chains; at r = 64 (the bf16_tokens workload)
+    AUTO keeps the workgroup kernel, and the wave kernel agrees with it to the
+    bf16 tolerance."""
+    x = synth.random_chain(3000, 32, 32, dtype="bf16", seed=21, affine=False, device="cuda:0")
+    auto = run_gpu(x)
+    wave = run_gpu(x, algo="chain_wave")
+    assert torch.equal(auto, wave)
+    idx = sample_chains(3000, seed=5)
+    assert_close(wave[idx.to(wave.device)].cpu().numpy(), ref(x.to("cpu"), idx), BF16_EXPECTED,
+                 "r32 token batch wave")
+    wl = synth.WORKLOADS["bf16_tokens"]
+    y = synth.generate(wl, device="cuda:0")
+    auto = run_gpu(y)
+    assert torch.equal(auto, run_gpu(y, algo="chain"))
+    wave = run_gpu(y, algo="chain_wave")
+    idx = sample_chains(wl.B, seed=6)
+    assert_close(wave[idx.to(wave.device)].cpu().numpy(), ref(y.to("cpu"), idx), BF16_EXPECTED,
+                 "bf16_tokens wave")
+    assert oracle.rel_frobenius(wave.cpu().double().numpy(), auto.cpu().double().numpy()) < 1e-4
 
 
 @pytest.mark.parametrize("algo", ["chain", "two_level"])
