@@ -38,6 +38,11 @@ CSRC = os.path.join(ROOT, "paper_2605_09204_amd", "csrc")
 TRAFFIC_DIR = os.path.join(ROOT, "profiles")
 
 METRIC = "interface combines/sec and achieved MFMA TFLOP/s (r=64, bf16/fp32), % of peak"
+# Default warm-up: at least 5 launches and at least this much time.  Under a
+# sustained load the GPU's clocks move for some tens of milliseconds (a
+# memory-bound launch first gets faster, then up to a third slower, then
+# settles), so a short warm-up times a transient rather than the steady state.
+WARMUP_MIN_S = 0.25
 PEAK = {  # MI355X published peaks
     "hbm_gbs": 8000.0,
     "mfma_f32_tflops": 157.3,
@@ -49,6 +54,24 @@ ELEM = {"f32": 4, "bf16": 2}
 # ----------------------------------------------------------------------------
 # accounting
 # ----------------------------------------------------------------------------
+
+
+def warm_up(step, args, torch) -> int:
+    """Runs the untimed launches; returns how many (recorded in args.warmup)."""
+    if args.warmup is not None:
+        for i in range(args.warmup):
+            step(i)
+        torch.cuda.synchronize()
+        return args.warmup
+    n, t0 = 0, time.perf_counter()
+    while n < 5 or (time.perf_counter() - t0 < WARMUP_MIN_S and n < 20000):
+        step(n)
+        n += 1
+        if n % 8 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    args.warmup = n
+    return n
 
 def widths_of(wl):
     return wl.interface_widths()
@@ -300,9 +323,7 @@ def bench_phase1(args) -> int:
     def step(i):
         binding.lbi_region_jacobians(x.params, x.x_embed, x.m, A=A, m_next=mn, workspace=ws)
 
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
+    warm_up(step, args, torch)
     stream = torch.cuda.current_stream(dev)
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
@@ -381,7 +402,8 @@ def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=30)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed launches (default: >= 5 and >= %.2f s of launches)" % WARMUP_MIN_S)
     ap.add_argument("--workload", default="long_chain")
     ap.add_argument("--math", choices=["split", "mfma"], default="split",
                     help="float32 arithmetic: three-part bf16 splits on the bf16 matrix "
@@ -528,9 +550,7 @@ def main(argv=None) -> int:
         torch.cuda.synchronize()
         del src, dst
 
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
+    warm_up(step, args, torch)
 
     stream = torch.cuda.current_stream(dev)
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
