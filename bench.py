@@ -426,6 +426,7 @@ def main(argv=None) -> int:
                          "tiles at their true shapes back to back (lbi_scan_backward_ragged)")
     ap.add_argument("--B", type=int, default=0, help="override the workload's chain count")
     ap.add_argument("--K", type=int, default=0, help="override the workload's slot count")
+    ap.add_argument("--r", type=int, default=0, help="override the workload's interface width")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--per-launch", action="store_true",
                     help="print every timed launch's duration (µs) to stderr")
@@ -467,12 +468,12 @@ def main(argv=None) -> int:
               file=sys.stderr)
         return 2
     wl = synth.WORKLOADS[args.workload]
-    if args.B or args.K:
+    if args.B or args.K or args.r:
         if wl.widths is not None:
-            print("--B/--K apply to uniform-width workloads only", file=sys.stderr)
+            print("--B/--K/--r apply to uniform-width workloads only", file=sys.stderr)
             return 2
-        wl = wl.with_(B=args.B or wl.B, K=args.K or wl.K, name=f"{wl.name}_B{args.B or wl.B}"
-                      f"_K{args.K or wl.K}")
+        wl = wl.with_(B=args.B or wl.B, K=args.K or wl.K, r=args.r or wl.r,
+                      name=f"{wl.name}_B{args.B or wl.B}_K{args.K or wl.K}_r{args.r or wl.r}")
     dev = torch.device("cuda:0")
     print(f"[bench] generating {wl.name}: B={wl.B} K={wl.K} r={wl.r} {wl.dtype}",
           file=sys.stderr, flush=True)
@@ -577,6 +578,11 @@ def main(argv=None) -> int:
         return 0
     value = combines(wl) * args.steps / (total_ms / 1e3)
     f_alg = flops_combines(wl) if args.op == "suffix_products" else flops_alg(wl)
+    # the chain-scan mapping the library uses for adjoints (its AUTO rule: bf16,
+    # r <= 32, B <= 8192, unless the two-level scan is taken)
+    wave = args.op == "adjoints" and args.layout == "padded" and (
+        args.algo == "chain_wave" or (args.algo == "auto" and wl.dtype == "bf16"
+                                      and wl.r <= 32 and wl.B <= 8192))
     b_alg = (bytes_export(wl) if args.op == "suffix_products"
              else bytes_alg(wl, compact_out=args.layout == "compact"))
     tflops = f_alg / avg_launch_s / 1e12
@@ -617,6 +623,10 @@ def main(argv=None) -> int:
                    "layout": args.layout,
                    "widths": "cyclic 32/64/128" if wl.widths else "uniform",
                    "parallelism": "1 GPU, " + ("two-level scan (segments in parallel)" if need
+                                               else "one wavefront per chain"
+                                               if args.algo == "chain_wave"
+                                               else "chain scan (one workgroup or wavefront "
+                                                    "per chain)" if args.algo == "auto"
                                                else "one workgroup per chain")},
         "roofline": roof,
         "extra": {
