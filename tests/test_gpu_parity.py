@@ -191,6 +191,31 @@ def test_chain_wave_token_batches_and_auto():
     assert oracle.rel_frobenius(wave.cpu().double().numpy(), auto.cpu().double().numpy()) < 1e-4
 
 
+def test_chain_wave_offsets_past_4gib():
+    """2048 bf16 chains of 256 slots at r = 64: A spans 4.3 GB, so the last
+    chains sit past 2^32 bytes (64-bit chain bases, 32-bit per-tile offsets).
+    Tiles are I + N(0, 0.02^2) noise drawn on the GPU; sampled chains, the
+    last among them, are held to the oracle."""
+    B, K, r = 2048, 256, 64
+    _say(f"[wave] B={B} K={K} r={r} (A = {B * K * r * r * 2 / 1e9:.1f} GB)")
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev).manual_seed(97)
+    A = torch.empty((B, K, r, r), dtype=torch.bfloat16, device=dev)
+    eye = torch.eye(r, device=dev)
+    for c in range(0, B, 256):
+        A[c:c + 256] = (eye + 0.02 * torch.randn((256, K, r, r), generator=g, device=dev)).bfloat16()
+    b = (0.1 * torch.randn((B, K, r), generator=g, device=dev)).bfloat16()
+    lamK = torch.randn((B, r), generator=g, device=dev).bfloat16()
+    wl = synth.Workload("wave_4gib", B, K, r, "bf16", 0, "uniform", True)
+    x = synth.Inputs(A, b, lamK, (r,) * (K + 1), wl)
+    lam = run_gpu(x, algo="chain_wave")
+    idx = torch.tensor([0, 1, 1023, 1500, B - 2, B - 1])
+    sub = x.chains(idx.to(dev)).to("cpu")
+    assert_close(lam[idx.to(dev)].cpu().numpy(), oracle.recurrence(sub.A, sub.b, sub.lamK),
+                 BF16_EXPECTED, "wave past 4 GiB")
+    del A, b, lam
+
+
 @pytest.mark.parametrize("algo", ["chain", "two_level"])
 @pytest.mark.parametrize("arith", ["split", "mfma"])
 def test_long_contracting_chain_r16(arith, algo):
