@@ -50,7 +50,11 @@
 //     order, so one 16-byte LDS read yields a lane's 8 operand values.
 //   * Widths hint: loads of all-zero tile regions are skipped (out-of-range
 //     buffer offsets return zero without touching memory) and the combine
-//     runs a shape specialised to the slot's row and k blocks.
+//     runs a shape specialised to the slot's row and k blocks.  The width
+//     codes come from the kernel arguments through scalar loads, whose wait
+//     also drains the LDS queue; the slot loop therefore keeps the codes of
+//     the slots it touches in registers and fetches one new code per slot,
+//     a slot early, where the slot barrier's wait covers it.
 //
 // All HIP code here is built with packed fp32 math disabled.
 #ifndef LBI_CHAIN_CUH
@@ -421,10 +425,27 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
     if (cout)
         cout += first * (int64_t)R;
     auto ring = [&](int64_t s) { return (int)((K - s) & 3); };
-    // rows of slot s that can be nonzero, rounded up to 16 x a power of two
+    // width code of local slot x (its row blocks; x = K: lambda_K's), 0
+    // before the segment.  The slot loop keeps the codes it needs in a
+    // rolling window instead (see below): each lookup is a scalar load, whose
+    // wait also drains the LDS queue.
+    auto wlook = [&](int64_t x) -> int {
+        if constexpr (HINT)
+            return x >= 0 ? width_blocks(args, s0 + x) : 0;
+        else
+            return 0;
+    };
+    // rows of a slot with width code wc that can be nonzero, rounded up to
+    // 16 x a power of two
+    auto rows_of = [&](int wc) {
+        if constexpr (HINT)
+            return 16 * pow2_at_least(wc);
+        else
+            return R;
+    };
     auto live_rows = [&](int64_t s) {
         if constexpr (HINT)
-            return s >= 0 && s < K ? 16 * pow2_at_least(width_blocks(args, s0 + s)) : 0;
+            return s >= 0 && s < K ? rows_of(wlook(s)) : 0;
         else
             return R;
     };
@@ -442,12 +463,13 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
     // Loads are issued unconditionally (a slot that does not exist gets only
     // out-of-range offsets), so the compiler can count outstanding loads
     // exactly and wait only for the slot being stored.
-    auto load_tile = [&](u4 (&dst)[CPT], int64_t j, bool valid) {
+    // (wr, wc: width codes of slots j and j + 1, read with a widths hint)
+    auto load_tile = [&](u4 (&dst)[CPT], int64_t j, bool valid, int wr, int wc) {
         const int64_t jj = valid ? j : 0;
         int rows = valid ? R : 0, cols = R;
         if constexpr (HINT) {
-            rows = valid ? 16 * width_blocks(args, s0 + jj) : 0;
-            cols = 16 * width_blocks(args, s0 + jj + 1);
+            rows = valid ? 16 * wr : 0;
+            cols = 16 * wc;
         }
         if constexpr (compact) {
             // the r_j x r_{j+1} tile sits just below the previous one
@@ -478,14 +500,14 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
         }
     };
     // b_j at the row this lane owns after the staging reduce (raw bits)
-    auto load_b = [&](int64_t j, bool valid) -> uint32_t {
+    auto load_b = [&](int64_t j, bool valid, int wr) -> uint32_t {
         if constexpr (AFF) {
             int nrow = R, soff = 0;
             const E *base = bv + (valid ? j : 0) * (int64_t)R;
             int range = R * G::ESZ;
             if constexpr (compact) {
                 // one resource over the chain's b; b_j just below b_{j+1}
-                nrow = valid ? 16 * width_blocks(args, s0 + j) : 0;
+                nrow = valid ? 16 * wr : 0;
                 curB -= nrow;
                 base = bv;
                 range = args.totalR * G::ESZ;
@@ -519,7 +541,8 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
             }
         }
     };
-    auto stage_chunk = [&](const u4 &src, int i, int buf, int64_t j) {
+    // (lr: live rows of slot j, with a widths hint)
+    auto stage_chunk = [&](const u4 &src, int i, int buf, int64_t j, int lr) {
         const int c = i * T + tid;
         const int row = i * RPI + srow;
         float x[EPC];
@@ -535,7 +558,7 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
         if constexpr (AFF) {
             // with a widths hint, chunk rows at or past r_j are all zero
             float s = 0.0f;
-            if (!HINT || i * RPI < live_rows(j)) {
+            if (!HINT || i * RPI < lr) {
                 s = x[0] * st_cv[0];
 #pragma unroll
                 for (int e = 1; e < EPC; ++e)
@@ -571,11 +594,12 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
                 sC[ring(j)][orow] = st_part[0] + bitsf(braw);
         }
     };
-    auto stage = [&](const u4 (&src)[CPT], int buf, uint32_t braw, int64_t j, bool first) {
+    auto stage = [&](const u4 (&src)[CPT], int buf, uint32_t braw, int64_t j, bool first,
+                     int lr) {
         stage_begin(j, first);
 #pragma unroll
         for (int i = 0; i < CPT; ++i)
-            stage_chunk(src[i], i, buf, j);
+            stage_chunk(src[i], i, buf, j, lr);
         stage_end(braw, j);
     };
 
@@ -621,9 +645,10 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
             }
         }
     };
-    auto apply_partial = [&](const f4(&P)[NRB][CB], int pbuf, int64_t s) {
+    // (lr: live rows of slot s, with a widths hint)
+    auto apply_partial = [&](const f4(&P)[NRB][CB], int pbuf, int64_t s, int lr) {
         if constexpr (HINT) {
-            const int nb = live_rows(s) / 16;
+            const int nb = lr / 16;
             if (nb <= 1 || NRB == 1) {
                 apply_rows(P, pbuf, std::integral_constant<int, 1>{});
                 return;
@@ -665,7 +690,8 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
     // get an out-of-range offset, which the buffer store drops; every wave
     // then issues the same memory instructions, which keeps the compiler's
     // count of outstanding loads exact.
-    auto finalize = [&](int64_t s, bool valid, int pbuf) {
+    // (ws: width code of slot s, with a widths hint)
+    auto finalize = [&](int64_t s, bool valid, int pbuf, int ws) {
         const int64_t ss = valid ? s : 0;
         // (when streaming, one wave group stores every slot, so that only it
         // has to fence before a publication)
@@ -675,7 +701,7 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
         const int fi = mine ? ft : 0;
         // rows the apply did not write are zero rows of P_s
         float acc = 0.0f;
-        if (fi < live_rows(ss)) {
+        if (fi < (HINT ? (valid ? rows_of(ws) : 0) : R)) {
             acc = sPart[pbuf][0][fi];
 #pragma unroll
             for (int ww = 1; ww < NW; ++ww)
@@ -689,7 +715,7 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
         int range = R * (int)sizeof(float);
         if constexpr (compact) {
             // one resource over the chain's lambda; lambda_s just below lambda_{s+1}
-            nrow = valid ? 16 * width_blocks(args, s0 + ss) : 0;
+            nrow = valid ? 16 * ws : 0;
             curL -= nrow;
             base = lam;
             range = args.totalR * (int)sizeof(float);
@@ -748,14 +774,14 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
     uint32_t pfb[NPF];
     {
         u4 first[CPT];
-        const uint32_t firstb = load_b(K - 1, true);
-        load_tile(first, K - 1, true);
+        const uint32_t firstb = load_b(K - 1, true, wlook(K - 1));
+        load_tile(first, K - 1, true, wlook(K - 1), wlook(K));
 #pragma unroll
         for (int q = 1; q <= NPF; ++q) {
-            pfb[q % NPF] = load_b(K - 1 - q, K - 1 - q >= 0);
-            load_tile(pf[q % NPF], K - 1 - q, K - 1 - q >= 0);
+            pfb[q % NPF] = load_b(K - 1 - q, K - 1 - q >= 0, wlook(K - 1 - q));
+            load_tile(pf[q % NPF], K - 1 - q, K - 1 - q >= 0, wlook(K - 1 - q), wlook(K - q));
         }
-        stage(first, 0, firstb, K - 1, true);
+        stage(first, 0, firstb, K - 1, true, live_rows(K - 1));
     }
     __syncthreads();
 
@@ -775,9 +801,10 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
                     P[I][t][v] = to_f32(sA[0][pos]);
             }
     if (K >= 2) {
-        stage(pf[1 % NPF], 1, pfb[1 % NPF], K - 2, false);
-        pfb[1 % NPF] = load_b(K - 2 - NPF, K - 2 - NPF >= 0);
-        load_tile(pf[1 % NPF], K - 2 - NPF, K - 2 - NPF >= 0);
+        stage(pf[1 % NPF], 1, pfb[1 % NPF], K - 2, false, live_rows(K - 2));
+        pfb[1 % NPF] = load_b(K - 2 - NPF, K - 2 - NPF >= 0, wlook(K - 2 - NPF));
+        load_tile(pf[1 % NPF], K - 2 - NPF, K - 2 - NPF >= 0, wlook(K - 2 - NPF),
+                  wlook(K - 1 - NPF));
     }
 
     // ---- slots K-2 .. 0 ---------------------------------------------------------
@@ -787,6 +814,15 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
     // of slot j+1.  One barrier per slot: the buffer staged here was last
     // read by the previous iteration's MFMAs, and c_{j-1} overwrites c_{j+3}
     // in the ring of four, whose readers all ran before this barrier.
+    //
+    // With a widths hint, wq[d] holds the width code of slot j + 2 - d
+    // (d = 0 .. NPF + 3: every slot the iteration touches).  The window moves
+    // by one slot per iteration; the code it takes in is looked up an
+    // iteration early, before the barrier, whose wait covers the load.
+    int wq[NPF + 4];
+#pragma unroll
+    for (int d = 0; d < NPF + 4; ++d)
+        wq[d] = wlook(K - d);
     for (int64_t base = K - 2; base >= 0; base -= NPF) {
 #pragma unroll
         for (int s = 0; s < NPF; ++s) {
@@ -795,22 +831,24 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
                 break;
             const int buf = (int)((uint32_t)(K - 1 - j) & 1);
             const int nx = (s + 2) % NPF;  // register set of slot j-1 (constant once unrolled)
+            const int wnext = wlook(j - 2 - NPF);
             __syncthreads();
             publish_before(j + 3);
             if constexpr (OUT == kOutLambda)
-                finalize(j + 2, j + 2 <= K - 1, (int)((j + 2) & 1));
+                finalize(j + 2, j + 2 <= K - 1, (int)((j + 2) & 1), wq[0]);
+            const int lr_next = j - 1 >= 0 ? rows_of(wq[3]) : 0;  // live rows of slot j-1
             f4 Pn[NRB][CB];
             // The staging of slot j-1 below is unconditional: at j = 0 it
             // stages the all-zero registers of the nonexistent slot -1 into a
             // buffer nothing reads again, and its c lands in ring entry
             // (K + 1) mod 4, which no later reader uses.
             auto reload = [&]() {
-                pfb[nx] = load_b(j - 1 - NPF, j - 1 - NPF >= 0);
-                load_tile(pf[nx], j - 1 - NPF, j - 1 - NPF >= 0);
+                pfb[nx] = load_b(j - 1 - NPF, j - 1 - NPF >= 0, wq[NPF + 3]);
+                load_tile(pf[nx], j - 1 - NPF, j - 1 - NPF >= 0, wq[NPF + 3], wq[NPF + 2]);
             };
             auto emit = [&]() {
                 if constexpr (OUT == kOutLambda)
-                    apply_partial(P, (int)((j + 1) & 1), j + 1);
+                    apply_partial(P, (int)((j + 1) & 1), j + 1, rows_of(wq[1]));
                 else
                     store_composite(P, j + 1);
             };
@@ -821,7 +859,7 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
                 stage_begin(j - 1, false);
                 combine<R, M, NCA, NRB, NRB, true>(Pn, P, sA[buf], li, g, [&](int step) {
                     if (step < CPT)
-                        stage_chunk(pf[nx][step], step, buf ^ 1, j - 1);
+                        stage_chunk(pf[nx][step], step, buf ^ 1, j - 1, lr_next);
                     else if (step == CPT)
                         stage_end(pfb[nx], j - 1);
                     else if (step == CPT + 1)
@@ -831,13 +869,12 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
                 });
             } else {
                 if constexpr (HINT) {
-                    const int nr = pow2_at_least(width_blocks(args, s0 + j));
-                    const int nk = pow2_at_least(width_blocks(args, s0 + j + 1));
-                    combine_shape<R, M, NCA>(nr, nk, Pn, P, sA[buf], li, g);
+                    combine_shape<R, M, NCA>(pow2_at_least(wq[2]), pow2_at_least(wq[1]), Pn, P,
+                                             sA[buf], li, g);
                 } else {
                     combine<R, M, NCA, NRB, NRB>(Pn, P, sA[buf], li, g);
                 }
-                stage(pf[nx], buf ^ 1, pfb[nx], j - 1, false);
+                stage(pf[nx], buf ^ 1, pfb[nx], j - 1, false, lr_next);
                 reload();
                 emit();
             }
@@ -846,6 +883,10 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
 #pragma unroll
                 for (int t = 0; t < CB; ++t)
                     P[I][t] = Pn[I][t];
+#pragma unroll
+            for (int d = 0; d < NPF + 3; ++d)
+                wq[d] = wq[d + 1];
+            wq[NPF + 3] = wnext;
         }
     }
     if constexpr (OUT == kOutLambda) {
@@ -853,14 +894,14 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
         // iteration
         __syncthreads();
         publish_before(2);
-        apply_partial(P, 0, 0);
+        apply_partial(P, 0, 0, live_rows(0));
         __syncthreads();
-        finalize(1, K >= 2, 1);
+        finalize(1, K >= 2, 1, wlook(1));
         if (args.progress) {
             __syncthreads();
             publish_before(1);
         }
-        finalize(0, true, 0);
+        finalize(0, true, 0, wlook(0));
         if (args.progress) {
             __syncthreads();
             publish_before(0);
