@@ -60,19 +60,80 @@ template <int MASK> __device__ __forceinline__ float xchg(float x)
     }
 }
 
+// One halving stage for the partner masks 8 and 7, without selects: DPP's
+// bank mask (the 4-lane banks of a 16-lane row) limits which lanes write.
+// Lanes whose stage bit is 0 fill banks LO, the others banks HI (bit 3 of the
+// lane: banks 0-1 / 2-3; bit 2: banks 0, 2 / 1, 3).  For each pair
+// (a, b) = (q[i], b[i]): a <- a + partner's a in the LO lanes, then
+// a <- b + partner's b in the HI lanes; neither step reads what the other
+// writes.  A DPP read needs two wait states after a VALU write of the same
+// register, and the compiler does not see the writes inside an asm block, so
+// each block starts and ends with s_nop 1.
+#define LBI_HALF_PAIR(CTRL, LO, HI, A, B)                                                    \
+    "v_add_f32_dpp %" #A ", %" #A ", %" #A " " CTRL " row_mask:0xf bank_mask:" LO "\n\t" \
+    "v_add_f32_dpp %" #A ", %" #B ", %" #B " " CTRL " row_mask:0xf bank_mask:" HI "\n\t"
+#define LBI_HB8(C, L, U) LBI_HALF_PAIR(C, L, U, 0, 8) LBI_HALF_PAIR(C, L, U, 1, 9)             \
+    LBI_HALF_PAIR(C, L, U, 2, 10) LBI_HALF_PAIR(C, L, U, 3, 11) LBI_HALF_PAIR(C, L, U, 4, 12) \
+    LBI_HALF_PAIR(C, L, U, 5, 13) LBI_HALF_PAIR(C, L, U, 6, 14) LBI_HALF_PAIR(C, L, U, 7, 15)
+#define LBI_HB4(C, L, U) LBI_HALF_PAIR(C, L, U, 0, 4) LBI_HALF_PAIR(C, L, U, 1, 5)             \
+    LBI_HALF_PAIR(C, L, U, 2, 6) LBI_HALF_PAIR(C, L, U, 3, 7)
+#define LBI_HB2(C, L, U) LBI_HALF_PAIR(C, L, U, 0, 2) LBI_HALF_PAIR(C, L, U, 1, 3)
+#define LBI_HB1(C, L, U) LBI_HALF_PAIR(C, L, U, 0, 1)
+#define LBI_HB(PAIRS)                                                                         \
+    if constexpr (MASK == 8)                                                                  \
+        asm("s_nop 1\n\t" PAIRS("row_ror:8", "0x3", "0xc") "s_nop 1" : LBI_HB_OPS);          \
+    else                                                                                      \
+        asm("s_nop 1\n\t" PAIRS("row_half_mirror", "0x5", "0xa") "s_nop 1" : LBI_HB_OPS);
+template <int MASK, int H> __device__ __forceinline__ void halve_banked(float *q, const float *b)
+{
+    static_assert(MASK == 8 || MASK == 7, "bank-masked halving");
+    if constexpr (H == 8) {
+#define LBI_HB_OPS "+v"(q[0]), "+v"(q[1]), "+v"(q[2]), "+v"(q[3]), "+v"(q[4]), "+v"(q[5]), \
+                   "+v"(q[6]), "+v"(q[7]) : "v"(b[0]), "v"(b[1]), "v"(b[2]), "v"(b[3]),   \
+                   "v"(b[4]), "v"(b[5]), "v"(b[6]), "v"(b[7])
+        LBI_HB(LBI_HB8)
+#undef LBI_HB_OPS
+    } else if constexpr (H == 4) {
+#define LBI_HB_OPS "+v"(q[0]), "+v"(q[1]), "+v"(q[2]), "+v"(q[3]) : "v"(b[0]), "v"(b[1]), "v"(b[2]), "v"(b[3])
+        LBI_HB(LBI_HB4)
+#undef LBI_HB_OPS
+    } else if constexpr (H == 2) {
+#define LBI_HB_OPS "+v"(q[0]), "+v"(q[1]) : "v"(b[0]), "v"(b[1])
+        LBI_HB(LBI_HB2)
+#undef LBI_HB_OPS
+    } else {
+        static_assert(H == 1, "pairs per stage");
+#define LBI_HB_OPS "+v"(q[0]) : "v"(b[0])
+        LBI_HB(LBI_HB1)
+#undef LBI_HB_OPS
+    }
+}
+#undef LBI_HB
+#undef LBI_HB1
+#undef LBI_HB2
+#undef LBI_HB4
+#undef LBI_HB8
+#undef LBI_HALF_PAIR
+
 // Sum LIVE values per lane over an aligned group of N lanes (gi = lane index
-// in the group).  Each stage either halves the live values (lanes whose bit
-// BIT is 0 keep the lower half, summed with the partner's lower half, the
-// others the upper) or, with one value left, adds the partner's.  Afterwards
-// lane gi holds, in q[e] for e < max(1, LIVE / N), the full group sum of
-// original index (gi >> S) * max(1, LIVE / N) + e with
+// in the group, which is also the lane's index modulo N: the masks 8 and 7
+// go by hardware lane position).  Each stage either halves the live values
+// (lanes whose bit BIT is 0 keep the lower half, summed with the partner's
+// lower half, the others the upper) or, with one value left, adds the
+// partner's.  Afterwards lane gi holds, in q[e] for e < max(1, LIVE / N), the
+// full group sum of original index (gi >> S) * max(1, LIVE / N) + e with
 // S = log2(N) - log2(min(LIVE, N)).
 template <int N, int LIVE, int V> __device__ __forceinline__ void group_reduce(float (&q)[V], int gi)
 {
     if constexpr (N > 1) {
         constexpr int MASK = N == 32 ? 16 : (N == 16 ? 8 : (N == 8 ? 7 : (N == 4 ? 2 : 1)));
         constexpr int BIT = ilog2(N) - 1;
-        if constexpr (LIVE >= 2) {
+        if constexpr (LIVE >= 2 && (MASK == 8 || MASK == 7)) {
+#pragma unroll
+            for (int i = 0; i < LIVE / 2; i += 8)
+                halve_banked<MASK, (LIVE / 2 < 8 ? LIVE / 2 : 8)>(q + i, q + i + LIVE / 2);
+            group_reduce<N / 2, LIVE / 2>(q, gi);
+        } else if constexpr (LIVE >= 2) {
             const bool upper = (gi >> BIT) & 1;
 #pragma unroll
             for (int i = 0; i < LIVE / 2; ++i) {
