@@ -408,7 +408,8 @@ def main(argv=None) -> int:
     ap.add_argument("--math", choices=["split", "mfma"], default="split",
                     help="float32 arithmetic: three-part bf16 splits on the bf16 matrix "
                          "cores (the library default) or the fp32 matrix cores")
-    ap.add_argument("--algo", choices=["auto", "chain", "two_level", "chain_wave"], default="auto",
+    ap.add_argument("--algo", choices=["auto", "chain", "two_level", "chain_wave", "chain_splitk"],
+                    default="auto",
                     help="scan algorithm (auto: the library's choice)")
     ap.add_argument("--op", choices=["adjoints", "suffix_products", "streaming", "norms",
                                      "phase1"],
@@ -493,7 +494,8 @@ def main(argv=None) -> int:
     math = binding.LBI_MATH_F32_SPLIT if args.math == "split" else binding.LBI_MATH_F32_MFMA
     algo = {"auto": binding.LBI_ALGO_AUTO, "chain": binding.LBI_ALGO_CHAIN,
             "two_level": binding.LBI_ALGO_TWO_LEVEL,
-            "chain_wave": binding.LBI_ALGO_CHAIN_WAVE}[args.algo]
+            "chain_wave": binding.LBI_ALGO_CHAIN_WAVE,
+            "chain_splitk": binding.LBI_ALGO_CHAIN_SPLITK}[args.algo]
     need = binding.lbi_scan_backward_workspace_bytes_ex(wl.B, wl.K, wl.r,
                                                          0 if wl.dtype == "f32" else 1, algo)
     ws = torch.empty((need,), dtype=torch.uint8, device=dev) if need else None
@@ -578,11 +580,21 @@ def main(argv=None) -> int:
         return 0
     value = combines(wl) * args.steps / (total_ms / 1e3)
     f_alg = flops_combines(wl) if args.op == "suffix_products" else flops_alg(wl)
-    # the chain-scan mapping the library uses for adjoints (its AUTO rule: bf16,
-    # r <= 32, B <= 8192, unless the two-level scan is taken)
-    wave = args.op == "adjoints" and args.layout == "padded" and (
-        args.algo == "chain_wave" or (args.algo == "auto" and wl.dtype == "bf16"
-                                      and wl.r <= 32 and wl.B <= 8192))
+    # the chain mapping the library uses (for adjoints, its AUTO rule unless
+    # the two-level scan is taken: bf16 with r <= 32 and B <= 8192 one
+    # wavefront per chain; fp32 split arithmetic at r = 64 with B <= 256
+    # twelve waves per chain; else one workgroup per chain)
+    auto_adj = args.algo == "auto" and args.op == "adjoints" and args.layout == "padded"
+    if need:
+        mapping = "two-level scan (segments in parallel)"
+    elif args.algo == "chain_wave" or (auto_adj and wl.dtype == "bf16" and wl.r <= 32
+                                       and wl.B <= 8192):
+        mapping = "one wavefront per chain"
+    elif args.algo == "chain_splitk" or (auto_adj and wl.dtype == "f32" and args.math == "split"
+                                         and wl.r == 64 and wl.B <= 256):
+        mapping = "twelve waves per chain (split contraction, staging waves)"
+    else:
+        mapping = "one workgroup per chain"
     b_alg = (bytes_export(wl) if args.op == "suffix_products"
              else bytes_alg(wl, compact_out=args.layout == "compact"))
     tflops = f_alg / avg_launch_s / 1e12
@@ -622,12 +634,7 @@ def main(argv=None) -> int:
                    "algorithm": args.algo, "workspace_bytes": need, "op": args.op,
                    "layout": args.layout,
                    "widths": "cyclic 32/64/128" if wl.widths else "uniform",
-                   "parallelism": "1 GPU, " + ("two-level scan (segments in parallel)" if need
-                                               else "one wavefront per chain"
-                                               if args.algo == "chain_wave"
-                                               else "chain scan (one workgroup or wavefront "
-                                                    "per chain)" if args.algo == "auto"
-                                               else "one workgroup per chain")},
+                   "parallelism": "1 GPU, " + mapping},
         "roofline": roof,
         "extra": {
             "alg_tflops": tflops,

@@ -49,7 +49,7 @@ extern "C" {
 /* HIP stream handle (the same type as hipStream_t). */
 typedef struct ihipStream_t *lbi_stream_t;
 
-#define LBI_ABI_VERSION 7
+#define LBI_ABI_VERSION 8
 
 /* Largest K for which a widths hint is used (longer chains run unhinted,
  * which gives identical results). */
@@ -106,7 +106,20 @@ typedef enum {
                              * workgroup kernel for B <= 4096; at r = 64 it
                              * holds two waves per SIMD and is about 10%
                              * slower.  AUTO picks it for bf16, r <= 32,
-                             * B <= 8192                                       */
+                             * B <= 8192                                       */,
+    LBI_ALGO_CHAIN_SPLITK = 4 /* the chain scan with eight waves per chain
+                             * instead of four: each product A_j P_{j+1} is
+                             * split over the two halves of its contraction
+                             * index, and the partial sums are added in LDS.
+                             * The same arithmetic as LBI_ALGO_CHAIN with
+                             * LBI_MATH_F32_SPLIT, with the sums taken in
+                             * another order; for batches too small to give
+                             * every SIMD two chains, where a slot's latency
+                             * sets the time.  fp32 storage, LBI_MATH_DEFAULT
+                             * or LBI_MATH_F32_SPLIT, r = 64 only (else
+                             * LBI_ERR_DTYPE / LBI_ERR_UNSUPPORTED_R); a widths
+                             * hint is accepted and not needed; no
+                             * workspace                                       */
 } lbi_algo;
 
 typedef enum {
@@ -133,7 +146,8 @@ size_t lbi_scan_backward_workspace_bytes(int64_t B, int64_t K, int32_t r, lbi_dt
 
 /*
  * As lbi_scan_backward_workspace_bytes, for a given algorithm: 0 for
- * LBI_ALGO_CHAIN and LBI_ALGO_CHAIN_WAVE; for LBI_ALGO_TWO_LEVEL about
+ * LBI_ALGO_CHAIN, LBI_ALGO_CHAIN_WAVE and LBI_ALGO_CHAIN_SPLITK; for
+ * LBI_ALGO_TWO_LEVEL about
  * 4 B K r (r + 1) bytes (the
  * segment composites in float32, plus the carries).
  */

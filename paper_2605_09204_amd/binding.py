@@ -26,6 +26,7 @@ LBI_ALGO_AUTO = 0
 LBI_ALGO_CHAIN = 1
 LBI_ALGO_TWO_LEVEL = 2
 LBI_ALGO_CHAIN_WAVE = 3
+LBI_ALGO_CHAIN_SPLITK = 4
 
 _DTYPES = {torch.float32: LBI_F32, torch.bfloat16: LBI_BF16}
 

@@ -81,6 +81,9 @@ double slot_us(lbi_dtype dt, int32_t r)
     return dt == LBI_BF16 ? bf16[i] : f32[i];
 }
 
+// Chains per launch up to which AUTO takes LBI_ALGO_CHAIN_SPLITK: one per CU.
+constexpr int64_t kSplitKMaxB = 256;
+
 // LBI_ALGO_AUTO: the cheaper of the two by a cost model fitted to MI355X
 // timings (B = 1..512, K = 32..512, every r; within 13% of the faster choice
 // everywhere on that grid).  Chain scan: K serial slot steps, slower once the
@@ -91,13 +94,21 @@ double slot_us(lbi_dtype dt, int32_t r)
 // go to the wavefront-per-chain kernel (no barrier, no LDS staging), which
 // measured 1.3-1.9x faster than the workgroup kernel up to B = 4096 and no
 // slower up to 8192; at r = 64 its registers allow two waves per SIMD and the
-// workgroup kernel is faster.
-lbi_algo resolve_algo(lbi_algo algo, int64_t B, int64_t K, int32_t r, lbi_dtype dt)
+// workgroup kernel is faster.  fp32 chains at r = 64 in the split arithmetic,
+// at most one per CU, go to the twelve-wave kernel (split contraction,
+// specialised staging waves): 1.2x faster than the workgroup kernel at K = 32
+// and B <= 256, and slower once chains share CUs.  The choice between the
+// chain and two-level scans does not depend on the arithmetic, so the
+// workspace query needs none.
+lbi_algo resolve_algo(lbi_algo algo, int64_t B, int64_t K, int32_t r, lbi_dtype dt, lbi_math math)
 {
     if (algo != LBI_ALGO_AUTO)
         return algo;
     const lbi_algo chain =
-        dt == LBI_BF16 && r <= 32 && B <= 8192 ? LBI_ALGO_CHAIN_WAVE : LBI_ALGO_CHAIN;
+        dt == LBI_BF16 && r <= 32 && B <= 8192 ? LBI_ALGO_CHAIN_WAVE
+        : dt == LBI_F32 && math != LBI_MATH_F32_MFMA && r == 64 && B <= kSplitKMaxB
+            ? LBI_ALGO_CHAIN_SPLITK
+            : LBI_ALGO_CHAIN;
     if (K < 16 || !two_level_possible(B, K))
         return chain;
     const double ts = slot_us(dt, r), w = waves_for_r(r), cap = 1280.0;
@@ -163,13 +174,17 @@ lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam,
     if (st != LBI_OK)
         return st;
     if (algo != LBI_ALGO_AUTO && algo != LBI_ALGO_CHAIN && algo != LBI_ALGO_TWO_LEVEL &&
-        algo != LBI_ALGO_CHAIN_WAVE)
+        algo != LBI_ALGO_CHAIN_WAVE && algo != LBI_ALGO_CHAIN_SPLITK)
         return LBI_ERR_DTYPE;
     if (algo == LBI_ALGO_TWO_LEVEL && !two_level_possible(B, K))
         return LBI_ERR_SHAPE;
     if (algo == LBI_ALGO_CHAIN_WAVE && dt != LBI_BF16)
         return LBI_ERR_DTYPE;
     if (algo == LBI_ALGO_CHAIN_WAVE && r > 64)
+        return LBI_ERR_UNSUPPORTED_R;
+    if (algo == LBI_ALGO_CHAIN_SPLITK && (dt != LBI_F32 || math == LBI_MATH_F32_MFMA))
+        return LBI_ERR_DTYPE;
+    if (algo == LBI_ALGO_CHAIN_SPLITK && r != 64)
         return LBI_ERR_UNSUPPORTED_R;
     if (B == 0)
         return LBI_OK;
@@ -182,7 +197,7 @@ lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam,
     const size_t nl = (size_t)B * r * esz, nout = (size_t)B * K * r * sizeof(float);
     if (overlaps(lam, nout, A, nA) || overlaps(lam, nout, b, nb) || overlaps(lam, nout, lamK, nl))
         return LBI_ERR_ALIAS;
-    const lbi_algo use = resolve_algo(algo, B, K, r, dt);
+    const lbi_algo use = resolve_algo(algo, B, K, r, dt, math);
     const size_t need = lbi_scan_backward_workspace_bytes_ex(B, K, r, dt, use);
     if (need > 0 && (!ws || ws_bytes < need))
         return LBI_ERR_WORKSPACE;
@@ -203,13 +218,17 @@ lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam,
     if (!encode_widths(widths, K, r, c))
         return LBI_ERR_SHAPE;
 
-    if (use == LBI_ALGO_CHAIN || use == LBI_ALGO_CHAIN_WAVE) {
+    if (use == LBI_ALGO_CHAIN || use == LBI_ALGO_CHAIN_WAVE || use == LBI_ALGO_CHAIN_SPLITK) {
         c.args.lam = lam;
         c.args.L = K;
         c.args.S = 1;
         c.out = kOutLambda;
         if (use == LBI_ALGO_CHAIN_WAVE)
             return launch_chain_wave_bf16(c) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
+        if (use == LBI_ALGO_CHAIN_SPLITK) {
+            c.hint = false;  // zero-padded tiles need no hint
+            return launch_chain_ksplit_f32x(c) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
+        }
         return launch_chain_mode(c, dt, math) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
     }
 
@@ -287,9 +306,10 @@ size_t lbi_scan_backward_workspace_bytes_ex(int64_t B, int64_t K, int32_t r, lbi
     if (check_common(dt, LBI_MATH_DEFAULT, r, B, K) != LBI_OK || B == 0)
         return 0;
     if (algo != LBI_ALGO_AUTO && algo != LBI_ALGO_CHAIN && algo != LBI_ALGO_TWO_LEVEL &&
-        algo != LBI_ALGO_CHAIN_WAVE)
+        algo != LBI_ALGO_CHAIN_WAVE && algo != LBI_ALGO_CHAIN_SPLITK)
         return 0;
-    if (resolve_algo(algo, B, K, r, dt) != LBI_ALGO_TWO_LEVEL || !two_level_possible(B, K))
+    if (resolve_algo(algo, B, K, r, dt, LBI_MATH_DEFAULT) != LBI_ALGO_TWO_LEVEL ||
+        !two_level_possible(B, K))
         return 0;
     return two_level_plan(B, K, r).bytes;
 }

@@ -72,6 +72,12 @@ hipError_t launch_chain_bf16(const ChainLaunch &c);
 bool chain_wave_supported(const ChainLaunch &c);
 hipError_t launch_chain_wave_bf16(const ChainLaunch &c);
 
+// The chain scan with twelve waves per chain for small batches (fp32 storage,
+// split arithmetic, r = 64, whole chains, kOutLambda without progress counters
+// or a widths hint).
+bool chain_ksplit_supported(const ChainLaunch &c);
+hipError_t launch_chain_ksplit_f32x(const ChainLaunch &c);
+
 // Segment carries of the two-level scan: carry[beta][d] is lambda at the end
 // of segment d (lambda_K for the last), obtained by applying the segment
 // aggregates (the composites at each segment's first slot) right to left.

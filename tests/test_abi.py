@@ -56,7 +56,7 @@ def test_header_compiles_as_c():
 
 
 def test_version_and_status_strings():
-    assert binding.lbi_abi_version() == 7
+    assert binding.lbi_abi_version() == 8
     assert binding.lbi_status_string(0) == "LBI_OK"
     for code in range(1, 9):
         assert binding.lbi_status_string(code).startswith("LBI_ERR_")
@@ -137,6 +137,19 @@ def test_chain_wave_argument_errors():
     for r in (16, 32, 64):
         assert binding.lbi_scan_backward_workspace_bytes_ex(4096, 32, r, 1, 3) == 0
         assert binding.lbi_scan_backward_workspace_bytes_ex(2, 512, r, 1, 3) == 0
+
+
+def test_chain_splitk_argument_errors():
+    # eight waves per chain: fp32 storage in the split arithmetic, r = 64
+    # only, no workspace; rejected before any pointer is touched
+    assert call(dt=1, algo=4) == 3              # bf16 storage: LBI_ERR_DTYPE
+    assert call(math=1, algo=4) == 3            # fp32 matrix cores: LBI_ERR_DTYPE
+    assert call(r=32, algo=4) == 4              # LBI_ERR_UNSUPPORTED_R
+    assert call(r=128, algo=4) == 4
+    assert call(algo=4, A=None) == 1
+    assert call(algo=5) == 3                    # not an lbi_algo
+    assert binding.lbi_scan_backward_workspace_bytes_ex(256, 32, 64, 0, 4) == 0
+    assert binding.lbi_scan_backward_workspace_bytes_ex(2, 512, 64, 0, 4) == 0
 
 
 def test_suffix_products_argument_errors():

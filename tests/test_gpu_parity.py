@@ -45,7 +45,8 @@ MODE_IDS = ["f32-split", "f32-mfma", "bf16"]
 
 
 ALGO = {"auto": binding.LBI_ALGO_AUTO, "chain": binding.LBI_ALGO_CHAIN,
-        "two_level": binding.LBI_ALGO_TWO_LEVEL, "chain_wave": binding.LBI_ALGO_CHAIN_WAVE}
+        "two_level": binding.LBI_ALGO_TWO_LEVEL, "chain_wave": binding.LBI_ALGO_CHAIN_WAVE,
+        "chain_splitk": binding.LBI_ALGO_CHAIN_SPLITK}
 
 
 def run_gpu(x: synth.Inputs, widths=None, stream=None, math=None, algo=None):
@@ -216,6 +217,56 @@ def test_chain_wave_offsets_past_4gib():
     del A, b, lam
 
 
+@pytest.mark.parametrize("B,K", [(1, 1), (3, 2), (2, 3), (5, 31), (4, 33), (1, 130), (70, 9),
+                                 (300, 5)])
+def test_chain_splitk_shapes(B, K):
+    """The small-batch chain kernel (fp32 storage, split arithmetic, r = 64),
+    ragged K and B (B = 300: more chains than CUs), with and without b,
+    against the oracle.  A widths hint of full widths changes nothing."""
+    _say(f"[splitk] B={B} K={K}")
+    for affine in (True, False):
+        x = synth.random_chain(B, K, 64, dtype="f32", seed=K * 13 + B, affine=affine)
+        lam = run_gpu(x, algo="chain_splitk")
+        assert_close(lam.cpu().numpy(), ref(x), TOL["f32"], f"splitk B{B} K{K} affine={affine}")
+        hinted = run_gpu(x, widths=[64] * (K + 1), algo="chain_splitk")
+        assert torch.equal(lam, hinted)
+
+
+@pytest.mark.parametrize("B", [3, 300])
+def test_chain_splitk_permutation_exact(B):
+    for K in (1, 2, 7, 40):
+        x = synth.permutation_chain(B, K, 64, dtype="f32", seed=K + B)
+        got = run_gpu(x, algo="chain_splitk").cpu().numpy().astype(np.float64)
+        assert np.array_equal(got, ref(x)), f"B={B} K={K}"
+
+
+@pytest.mark.parametrize("name", ["paper_width", "long_chain"])
+def test_chain_splitk_full_size(name):
+    """The fp32 r = 64 workloads at full size through the small-batch kernel,
+    sampled chains against the oracle, and the whole output against the
+    workgroup chain kernel."""
+    wl = synth.WORKLOADS[name]
+    _say(f"[splitk] {name} B={wl.B} K={wl.K}")
+    x = synth.generate(wl, device="cuda:0")
+    lam = run_gpu(x, algo="chain_splitk")
+    idx = sample_chains(wl.B, n=24, seed=17)
+    assert_close(lam[idx.to(lam.device)].cpu().numpy(), ref(x.to("cpu"), idx), TOL["f32"],
+                 f"{name} splitk")
+    base = run_gpu(x, algo="chain")
+    assert oracle.rel_frobenius(lam.cpu().double().numpy(), base.cpu().double().numpy()) < 2e-6
+
+
+@pytest.mark.parametrize("B", [4])
+@pytest.mark.parametrize("spectrum,affine", [("uniform", False), ("uniform", True),
+                                             ("orthogonal", False)])
+def test_chain_splitk_long_undamped_chain(spectrum, affine, B):
+    K, r = 512, 64
+    _say(f"[splitk] {spectrum} affine={affine} K=512 B={B}")
+    x = synth.random_chain(B, K, r, dtype="f32", seed=7, spectrum=spectrum, affine=affine)
+    lam = run_gpu(x, algo="chain_splitk").cpu().numpy().astype(np.float64)
+    assert_close(lam, ref(x), TOL["f32"], f"splitk {spectrum} K512 B{B}")
+
+
 @pytest.mark.parametrize("algo", ["chain", "two_level"])
 @pytest.mark.parametrize("arith", ["split", "mfma"])
 def test_long_contracting_chain_r16(arith, algo):
@@ -266,7 +317,7 @@ def test_long_undamped_chain_meets_fp32_tolerance(arith, algo, spectrum, affine)
     assert_close(lam, ref(x), TOL["f32"], f"{spectrum} K512 {arith} {algo}")
 
 
-@pytest.mark.parametrize("algo", ["chain", "two_level"])
+@pytest.mark.parametrize("algo", ["chain", "two_level", "chain_splitk"])
 @pytest.mark.parametrize("arith", ["split", "mfma"])
 def test_products_with_identity_are_exact(arith, algo):
     """A product with an identity factor must return the other factor bit for
@@ -275,6 +326,8 @@ def test_products_with_identity_are_exact(arith, algo):
     lambda_K.  Then lambda_0 is a column of X or Y exactly, which pins the
     three-part split of both operands (A staged from memory, P carried in
     registers) to h + m + l == x."""
+    if algo == "chain_splitk" and arith == "mfma":
+        pytest.skip("the small-batch kernel has the split arithmetic only")
     r = 64
     gen = torch.Generator().manual_seed(83)
     n = 6
@@ -408,6 +461,20 @@ def test_two_level_orthogonal_long_chain(arith):
     x = synth.random_chain(2, K, r, dtype="f32", seed=19, spectrum="orthogonal", affine=False)
     lam = run_gpu(x, math=arith, algo="two_level").cpu().numpy().astype(np.float64)
     assert_close(lam, ref(x), 8 * math.sqrt(K * r) * U32, "two-level orthogonal K512")
+
+
+def test_auto_picks_splitk_for_small_fp32_batches():
+    """fp32 chains at r = 64 in the split arithmetic, at most one per CU and
+    not taken by the two-level scan, run on the twelve-wave kernel: AUTO
+    equals the explicit call bit for bit (K < 16, and paper_width's B = 256,
+    K = 32); the fp32 matrix cores and B = 300 keep the workgroup kernel."""
+    x = synth.random_chain(5, 9, 64, dtype="f32", seed=29)
+    assert torch.equal(run_gpu(x), run_gpu(x, algo="chain_splitk"))
+    assert torch.equal(run_gpu(x, math="mfma", algo="auto"), run_gpu(x, math="mfma", algo="chain"))
+    y = synth.generate(synth.WORKLOADS["paper_width"], device="cuda:0")
+    assert torch.equal(run_gpu(y), run_gpu(y, algo="chain_splitk"))
+    z = synth.random_chain(300, 9, 64, dtype="f32", seed=30)
+    assert torch.equal(run_gpu(z), run_gpu(z, algo="chain"))
 
 
 def test_auto_picks_two_level_for_few_long_chains():
