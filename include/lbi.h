@@ -82,7 +82,9 @@ typedef enum {
                              * steps and 8 B K r^2 bytes of composite traffic;
                              * few long chains go two-level.  K < 16: chain.
                              * Otherwise bf16 with r <= 32 and B <= 8192 goes
-                             * to LBI_ALGO_CHAIN_WAVE                           */
+                             * to LBI_ALGO_CHAIN_WAVE, and fp32 with r = 64 in
+                             * the split arithmetic and B <= 256 to
+                             * LBI_ALGO_CHAIN_SPLITK                             */
     LBI_ALGO_CHAIN = 1,     /* one workgroup folds each whole chain right to
                              * left (K-1 combines, span K) and applies every
                              * composite to lambda_K as it forms; no workspace */
@@ -107,19 +109,24 @@ typedef enum {
                              * holds two waves per SIMD and is about 10%
                              * slower.  AUTO picks it for bf16, r <= 32,
                              * B <= 8192                                       */,
-    LBI_ALGO_CHAIN_SPLITK = 4 /* the chain scan with eight waves per chain
-                             * instead of four: each product A_j P_{j+1} is
-                             * split over the two halves of its contraction
-                             * index, and the partial sums are added in LDS.
-                             * The same arithmetic as LBI_ALGO_CHAIN with
-                             * LBI_MATH_F32_SPLIT, with the sums taken in
-                             * another order; for batches too small to give
-                             * every SIMD two chains, where a slot's latency
-                             * sets the time.  fp32 storage, LBI_MATH_DEFAULT
-                             * or LBI_MATH_F32_SPLIT, r = 64 only (else
+    LBI_ALGO_CHAIN_SPLITK = 4 /* the chain scan with twelve waves per chain
+                             * for small batches: eight waves form the
+                             * products, each product A_j P_{j+1} split over
+                             * the two halves of its contraction index with
+                             * the partial sums added in LDS, and four waves
+                             * stage A and store lambda.  The same arithmetic
+                             * as LBI_ALGO_CHAIN with LBI_MATH_F32_SPLIT, with
+                             * the sums taken in another order; one chain per
+                             * CU, for batches where a slot's latency sets the
+                             * time (measured 1.15-1.2x faster than
+                             * LBI_ALGO_CHAIN for B <= 256, slower beyond).
+                             * fp32 storage, LBI_MATH_DEFAULT or
+                             * LBI_MATH_F32_SPLIT, r = 64 only (else
                              * LBI_ERR_DTYPE / LBI_ERR_UNSUPPORTED_R); a widths
-                             * hint is accepted and not needed; no
-                             * workspace                                       */
+                             * hint is accepted and not needed; no workspace.
+                             * AUTO picks it for fp32 r = 64 in the split
+                             * arithmetic with B <= 256 when it does not pick
+                             * LBI_ALGO_TWO_LEVEL                              */
 } lbi_algo;
 
 typedef enum {

@@ -31,7 +31,7 @@
 //     b_{j-1} from the same registers, and store lambda_{j+2}, summed over the
 //     four column blocks.
 //   * One barrier per slot, in code that every wave runs; the partial sums of
-//     consecutive slots alternate between two LDS buffers.  82 KB of LDS: one
+//     consecutive slots alternate between two LDS buffers.  83 KB of LDS: one
 //     chain per CU.
 //
 // All HIP code here is built with packed fp32 math disabled.
