@@ -583,7 +583,7 @@ def main(argv=None) -> int:
     # the chain mapping the library uses (for adjoints, its AUTO rule unless
     # the two-level scan is taken: bf16 with r <= 32 and B <= 8192 one
     # wavefront per chain; fp32 split arithmetic at r = 64 with B <= 256
-    # twelve waves per chain; else one workgroup per chain)
+    # sixteen waves per chain; else one workgroup per chain)
     auto_adj = args.algo == "auto" and args.op == "adjoints" and args.layout == "padded"
     if need:
         mapping = "two-level scan (segments in parallel)"
@@ -592,7 +592,7 @@ def main(argv=None) -> int:
         mapping = "one wavefront per chain"
     elif args.algo == "chain_splitk" or (auto_adj and wl.dtype == "f32" and args.math == "split"
                                          and wl.r == 64 and wl.B <= 256):
-        mapping = "twelve waves per chain (split contraction, staging waves)"
+        mapping = "sixteen waves per chain (split contraction, staging waves)"
     else:
         mapping = "one workgroup per chain"
     b_alg = (bytes_export(wl) if args.op == "suffix_products"

@@ -109,16 +109,16 @@ typedef enum {
                              * holds two waves per SIMD and is about 10%
                              * slower.  AUTO picks it for bf16, r <= 32,
                              * B <= 8192                                       */,
-    LBI_ALGO_CHAIN_SPLITK = 4 /* the chain scan with twelve waves per chain
+    LBI_ALGO_CHAIN_SPLITK = 4 /* the chain scan with sixteen waves per chain
                              * for small batches: eight waves form the
                              * products, each product A_j P_{j+1} split over
                              * the two halves of its contraction index with
-                             * the partial sums added in LDS, and four waves
+                             * the partial sums added in LDS, and eight waves
                              * stage A and store lambda.  The same arithmetic
                              * as LBI_ALGO_CHAIN with LBI_MATH_F32_SPLIT, with
                              * the sums taken in another order; one chain per
                              * CU, for batches where a slot's latency sets the
-                             * time (measured 1.15-1.2x faster than
+                             * time (measured 1.07-1.29x faster than
                              * LBI_ALGO_CHAIN for B <= 256, slower beyond).
                              * fp32 storage, LBI_MATH_DEFAULT or
                              * LBI_MATH_F32_SPLIT, r = 64 only (else

@@ -95,9 +95,9 @@ constexpr int64_t kSplitKMaxB = 256;
 // measured 1.3-1.9x faster than the workgroup kernel up to B = 4096 and no
 // slower up to 8192; at r = 64 its registers allow two waves per SIMD and the
 // workgroup kernel is faster.  fp32 chains at r = 64 in the split arithmetic,
-// at most one per CU, go to the twelve-wave kernel (split contraction,
-// specialised staging waves): 1.2x faster than the workgroup kernel at K = 32
-// and B <= 256, and slower once chains share CUs.  The choice between the
+// at most one per CU, go to the sixteen-wave kernel (split contraction,
+// specialised staging waves): 1.2-1.3x faster than the workgroup kernel for
+// B <= 128 and 1.07-1.2x at B = 256, and slower once chains share CUs.  The choice between the
 // chain and two-level scans does not depend on the arithmetic, so the
 // workspace query needs none.
 lbi_algo resolve_algo(lbi_algo algo, int64_t B, int64_t K, int32_t r, lbi_dtype dt, lbi_math math)

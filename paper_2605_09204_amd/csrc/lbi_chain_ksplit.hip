@@ -1,6 +1,6 @@
 // The chain scan for batches too small to give every SIMD two chains, for
-// fp32 storage in the split arithmetic at r = 64: twelve waves per chain, of
-// which eight form the products and four move data.
+// fp32 storage in the split arithmetic at r = 64: sixteen waves per chain, of
+// which eight form the products and eight move data.
 //
 // It computes what the workgroup chain kernel computes (the suffix composites
 // P_j = A_j P_{j+1} of the scan formulation, Proposition "Scan Formulation of
@@ -26,11 +26,13 @@
 //   * Specialised waves.  The matrix waves do only what depends on P: the
 //     exchange, the split, the MFMAs and the apply of slot j+1 (own rows of
 //     P_{j+1} times lambda_K over the column block, in the MFMAs' shadow).
-//     Four staging waves load A_{j-1} NPF slots ahead (16-byte buffer loads),
+//     Eight staging waves load A_{j-1} NPF slots ahead (16-byte buffer loads),
 //     split it into three bf16 planes in LDS, form c_{j-1} = A_{j-1} c_j +
 //     b_{j-1} from the same registers, and store lambda_{j+2}, summed over the
 //     four column blocks.
-//   * One barrier per slot, in code that every wave runs; the partial sums of
+//   * One barrier per slot.  Each role runs its own slot loop with the same
+//     barriers, so neither role's loop-carried registers are live in the
+//     other's loop (121 VGPRs: four waves per SIMD).  The partial sums of
 //     consecutive slots alternate between two LDS buffers.  83 KB of LDS: one
 //     chain per CU.
 //
@@ -42,11 +44,12 @@ namespace lbi {
 namespace {
 
 template <bool AFF>
-__global__ __launch_bounds__(768) void scan_ksplit_kernel(const ScanArgs args)
+__global__ __launch_bounds__(1024) void scan_ksplit_kernel(const ScanArgs args)
 {
     constexpr int R = 64;
     constexpr int NMW = 8;                   // matrix waves
-    constexpr int TH = 256;                  // staging threads (four waves)
+    constexpr int NSW = 8;                   // staging waves
+    constexpr int TH = 64 * NSW;             // staging threads
     using G = Geo<R, kF32X, 4>;              // the LDS plane layout of the chain kernel
     constexpr int PLANE = G::PLANE, PITCH = G::PITCH;
     constexpr int NPF = 2;                   // slots prefetched
@@ -54,7 +57,9 @@ __global__ __launch_bounds__(768) void scan_ksplit_kernel(const ScanArgs args)
     constexpr int LPR = R / 4;               // staging lanes per tile row
     constexpr int RPI = TH / LPR;            // tile rows per chunk index
     constexpr int TILE_BYTES = R * R * 4;
-    static_assert(G::SWZ && G::PERM && PLANE == R * R && CPT == 4, "tile layout");
+    constexpr int SHIFT = ilog2(LPR) - ilog2(CPT);  // staging reduce layout
+    static_assert(G::SWZ && G::PERM && PLANE == R * R && CPT * TH * 4 == R * R && CPT <= LPR,
+                  "tile layout");
 
     __shared__ __attribute__((aligned(16))) __bf16 sA[2][3 * PLANE];
     // partial sums handed over: [slot parity][column block][receiving k half][row block][lane]
@@ -80,13 +85,13 @@ __global__ __launch_bounds__(768) void scan_ksplit_kernel(const ScanArgs args)
 
     // staging roles (staging waves): chunk i of thread ht covers tile row
     // i * RPI + srow, columns scol .. scol + 3; after the row reduce, lane
-    // sgi = 4 i owns the affine sum of row i * RPI + srow
+    // sgi = i 2^SHIFT owns the affine sum of row i * RPI + srow
     const int ht = mw ? 0 : tid - 64 * NMW;
     const int sgi = ht % LPR;
     const int srow = ht / LPR;
     const int scol = 4 * sgi;
-    const int orow = (sgi >> 2) * RPI + srow;
-    const bool oown = (sgi & 3) == 0;
+    const int orow = (sgi >> SHIFT) * RPI + srow;
+    const bool oown = (sgi & ((1 << SHIFT) - 1)) == 0;
 
     // ---- loads (branch-free: a slot outside the chain gets out-of-range
     // offsets, which read zeros without touching memory) --------------------
@@ -167,7 +172,7 @@ __global__ __launch_bounds__(768) void scan_ksplit_kernel(const ScanArgs args)
     // one of them stores, in turn) ------------------------------------------
     auto finalize = [&](int64_t s, bool valid, int pbuf) {
         const int64_t ss = valid ? s : 0;
-        const int ft = ht - 64 * (int)((uint64_t)ss % 4);
+        const int ft = ht - 64 * (int)((uint64_t)ss % NSW);
         const bool mine = valid && ft >= 0 && ft < R;
         const int fi = mine ? ft : 0;
         float acc = ((sPart[pbuf][0][fi] + sPart[pbuf][1][fi]) + sPart[pbuf][2][fi]) + sPart[pbuf][3][fi];
@@ -225,15 +230,16 @@ __global__ __launch_bounds__(768) void scan_ksplit_kernel(const ScanArgs args)
     // read before this barrier.
     f4 Pk[2];  // own row blocks of the last partial product
     const int rot = 2 * kh;
-    for (int64_t base = K - 2; base >= 0; base -= NPF) {
+    // (each role in its own loop, with the same barriers)
+    if (mw) {
+        for (int64_t base = K - 2; base >= 0; base -= NPF) {
 #pragma unroll
-        for (int s = 0; s < NPF; ++s) {
-            const int64_t j = base - s;
-            if (j < 0)
-                break;
-            const int buf = (int)((uint32_t)(K - 1 - j) & 1);
-            __syncthreads();
-            if (mw) {
+            for (int s = 0; s < NPF; ++s) {
+                const int64_t j = base - s;
+                if (j < 0)
+                    break;
+                const int buf = (int)((uint32_t)(K - 1 - j) & 1);
+                __syncthreads();
                 if (j < K - 2) {
 #pragma unroll
                     for (int I = 0; I < 2; ++I)
@@ -286,7 +292,17 @@ __global__ __launch_bounds__(768) void scan_ksplit_kernel(const ScanArgs args)
                     sX[j & 1][cb][kh ^ 1][I][lane] = Pn[2 + I];
                     Pk[I] = Pn[I];
                 }
-            } else {
+            }
+        }
+    } else {
+        for (int64_t base = K - 2; base >= 0; base -= NPF) {
+#pragma unroll
+            for (int s = 0; s < NPF; ++s) {
+                const int64_t j = base - s;
+                if (j < 0)
+                    break;
+                const int buf = (int)((uint32_t)(K - 1 - j) & 1);
+                __syncthreads();
                 finalize(j + 2, j + 2 <= K - 1, (int)((j + 2) & 1));
                 const int nx = (s + 2) % NPF;  // register set of slot j-1
                 stage(pf[nx], buf ^ 1, pfb[nx], j - 1, false);
@@ -316,7 +332,7 @@ __global__ __launch_bounds__(768) void scan_ksplit_kernel(const ScanArgs args)
 template <bool AFF> hipError_t launch_ks(const ChainLaunch &c)
 {
     void *params[] = {(void *)&c.args};
-    return hipLaunchKernel((const void *)&scan_ksplit_kernel<AFF>, dim3((unsigned)c.B), dim3(768),
+    return hipLaunchKernel((const void *)&scan_ksplit_kernel<AFF>, dim3((unsigned)c.B), dim3(1024),
                            params, 0, c.stream);
 }
 

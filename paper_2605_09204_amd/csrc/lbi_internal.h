@@ -72,7 +72,7 @@ hipError_t launch_chain_bf16(const ChainLaunch &c);
 bool chain_wave_supported(const ChainLaunch &c);
 hipError_t launch_chain_wave_bf16(const ChainLaunch &c);
 
-// The chain scan with twelve waves per chain for small batches (fp32 storage,
+// The chain scan with sixteen waves per chain for small batches (fp32 storage,
 // split arithmetic, r = 64, whole chains, kOutLambda without progress counters
 // or a widths hint).
 bool chain_ksplit_supported(const ChainLaunch &c);

@@ -465,7 +465,7 @@ def test_two_level_orthogonal_long_chain(arith):
 
 def test_auto_picks_splitk_for_small_fp32_batches():
     """fp32 chains at r = 64 in the split arithmetic, at most one per CU and
-    not taken by the two-level scan, run on the twelve-wave kernel: AUTO
+    not taken by the two-level scan, run on the sixteen-wave kernel: AUTO
     equals the explicit call bit for bit (K < 16, and paper_width's B = 256,
     K = 32); the fp32 matrix cores and B = 300 keep the workgroup kernel."""
     x = synth.random_chain(5, 9, 64, dtype="f32", seed=29)
