@@ -89,13 +89,13 @@ typedef enum {
                              * left (K-1 combines, span K) and applies every
                              * composite to lambda_K as it forms; no workspace */
     LBI_ALGO_TWO_LEVEL = 2, /* each chain is cut into S ~ sqrt(2K) segments; a
-                             * workgroup per segment folds it into its local
-                             * composites (kept in the workspace), a carry pass
-                             * applies the segment aggregates right to left to
-                             * lambda_K, and an apply pass forms every
-                             * lambda_j = P_j carry + c_j at once (span K/S
-                             * combines + S matrix-vector products); needs
-                             * workspace, B * K < 2^31                           */
+                             * workgroup per segment folds it to its aggregate
+                             * (kept in the workspace), a carry pass applies
+                             * the aggregates right to left to lambda_K, and a
+                             * workgroup per segment scans it again from its
+                             * carry, forming every lambda_j = P_j carry + c_j
+                             * (span 2K/S combines + S matrix-vector products);
+                             * needs workspace, B * K < 2^31                     */
     LBI_ALGO_CHAIN_WAVE = 3 /* the chain scan with one 64-lane wavefront per
                              * chain instead of a workgroup: the same combines
                              * and apply, with A_j loaded straight into
@@ -154,9 +154,8 @@ size_t lbi_scan_backward_workspace_bytes(int64_t B, int64_t K, int32_t r, lbi_dt
 /*
  * As lbi_scan_backward_workspace_bytes, for a given algorithm: 0 for
  * LBI_ALGO_CHAIN, LBI_ALGO_CHAIN_WAVE and LBI_ALGO_CHAIN_SPLITK; for
- * LBI_ALGO_TWO_LEVEL about
- * 4 B K r (r + 1) bytes (the
- * segment composites in float32, plus the carries).
+ * LBI_ALGO_TWO_LEVEL about 4 B S r (r + 2) bytes with S ~ sqrt(2K) (the
+ * segment aggregates in float32, plus the carries).
  */
 size_t lbi_scan_backward_workspace_bytes_ex(int64_t B, int64_t K, int32_t r, lbi_dtype dt,
                                             lbi_algo algo);

@@ -39,13 +39,24 @@ bool misaligned(const void *p) { return p && ((uintptr_t)p & 15u); }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Segments of the two-level scan: S ~ sqrt(2K) balances the K/S fold steps
-// (each a chain-kernel slot step, plus a pipeline start per workgroup) against
-// the S carry steps; a sweep over S on MI355X (B = 1..128, K = 128..2048, r =
-// 64) puts the optimum there, within 5% or a flat region.
+// Segments of the two-level scan: S ~ sqrt(2K) balances the K/S slot steps of
+// a segment pass (each a chain-kernel slot step, plus a pipeline start per
+// workgroup) against the S carry steps; a sweep over S on MI355X (B = 1..128,
+// K = 128..2048, r = 64) puts the optimum there, within 5% or a flat region.
+// Two forms:
+//   * every composite kept (fp32, 4 B K r^2 bytes written and read again),
+//     then one parallel apply pass: the shorter span, for small batches;
+//   * aggregates only, then each segment scanned again from its carry: the
+//     composites never reach memory (A is read twice instead), for batches
+//     whose composites would not fit the 256 MB last-level cache.  Measured
+//     at r = 64 fp32, K = 512, same box: 2% slower at B = 16 (134 MB of
+//     composites), 14% faster at B = 64 (537 MB), 33% slower at B = 1.
+constexpr double kRescanBytes = 256.0 * (1 << 20);
+
 struct TwoLevelPlan {
     int64_t L;
     int32_t S;
+    bool rescan;
     size_t offP, offc, offcarry, bytes;
 };
 
@@ -59,8 +70,10 @@ TwoLevelPlan two_level_plan(int64_t B, int64_t K, int32_t r)
         S = 1;
     p.L = (K + S - 1) / S;
     p.S = (int32_t)((K + p.L - 1) / p.L);
-    const size_t nP = (size_t)B * K * r * r * sizeof(float);
-    const size_t nc = (size_t)B * K * r * sizeof(float);
+    p.rescan = 4.0 * (double)B * K * r * r > kRescanBytes;
+    const int64_t nslots = p.rescan ? (int64_t)p.S : K;  // composites kept per chain
+    const size_t nP = (size_t)B * nslots * r * r * sizeof(float);
+    const size_t nc = (size_t)B * nslots * r * sizeof(float);
     const size_t ncar = (size_t)B * p.S * r * sizeof(float);
     p.offP = 0;
     p.offc = align256(nP);
@@ -69,7 +82,7 @@ TwoLevelPlan two_level_plan(int64_t B, int64_t K, int32_t r)
     return p;
 }
 
-// The grid of the apply pass is B*K workgroups.
+// The apply pass launches up to B*K workgroups.
 bool two_level_possible(int64_t B, int64_t K) { return B * K < ((int64_t)1 << 31) - 1; }
 
 // Microseconds per slot of one chain-kernel workgroup on an otherwise idle
@@ -232,23 +245,39 @@ lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam,
         return launch_chain_mode(c, dt, math) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
     }
 
+    // two-level scan: each segment folded (every composite kept, or its
+    // aggregate only); the carries right to left; then every lambda_j at once
+    // from the composites, or each segment scanned again from its carry
     const TwoLevelPlan p = two_level_plan(B, K, r);
     char *w = (char *)ws;
     float *Pc = (float *)(w + p.offP);
     float *cc = b ? (float *)(w + p.offc) : nullptr;
     float *carry = (float *)(w + p.offcarry);
-    c.args.Pout = Pc;
-    c.args.cout = cc;
     c.args.L = p.L;
     c.args.S = p.S;
+    c.args.Pout = Pc;
+    c.args.cout = cc;
+    c.args.agg_only = p.rescan ? 1 : 0;
     c.out = kOutComposite;
-    c.ncol = r / 16;  // segment composites have the width of their segment's end
+    // a segment's composites (and its lambda pass) have the width of the
+    // segment's end, not lambda_K's: every column block
+    c.ncol = r / 16;
     if (launch_chain_mode(c, dt, math) != hipSuccess)
         return LBI_ERR_HIP;
-    if (launch_carry(Pc, cc, lamK, dt == LBI_BF16, carry, B, K, p.L, p.S, r, c.stream) !=
-        hipSuccess)
+    if (launch_carry(Pc, cc, lamK, dt == LBI_BF16, carry, B, p.S, p.rescan ? p.S : K,
+                     p.rescan ? 1 : p.L, r, c.stream) != hipSuccess)
         return LBI_ERR_HIP;
-    if (launch_apply(Pc, cc, carry, lam, B, K, p.L, p.S, r, c.stream) != hipSuccess)
+    if (!p.rescan)
+        return launch_apply(Pc, cc, carry, lam, B, K, p.L, p.S, r, c.stream) == hipSuccess
+                   ? LBI_OK
+                   : LBI_ERR_HIP;
+    c.args.Pout = nullptr;
+    c.args.cout = nullptr;
+    c.args.agg_only = 0;
+    c.args.lam = lam;
+    c.args.lamSeg = carry;
+    c.out = kOutLambda;
+    if (launch_chain_mode(c, dt, math) != hipSuccess)
         return LBI_ERR_HIP;
     return LBI_OK;
 }

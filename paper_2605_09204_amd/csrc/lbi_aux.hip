@@ -1,15 +1,16 @@
 // Carry and apply passes of the two-level interface-adjoint scan (gfx950).
 //
-// The chain kernel folds each segment of Lseg slots into its local suffix
-// composites (P_j, c_j) = (A_j, b_j) o ... o (A_{e-1}, b_{e-1}), e the
+// The chain kernel first folds each segment of Lseg slots into its local
+// suffix composites (P_j, c_j) = (A_j, b_j) o ... o (A_{e-1}, b_{e-1}), e the
 // segment's end (Proposition "Scan Formulation of Backpropagation": any
-// bracketing of the associative combine gives the same composites).  Then:
-//   carry: lambda at each segment end, right to left, from the segment
-//          aggregates (the composites at each segment's first slot):
+// bracketing of the associative combine gives the same composites): all of
+// them, or only the aggregate at the segment's first slot s_d.  Then:
+//   carry: lambda at each segment end, right to left, from the aggregates:
 //          lambda_{e_{S-1}} = lambda_K, lambda_{s_d} = P_{s_d} lambda_{e_d} + c_{s_d};
-//   apply: lambda_j = P_j lambda_{e(j)} + c_j for every slot at once
-//          (Phase 2 of Algorithm "Bounded-Interface Backpropagation", with the
-//          segment's carry in place of mbar_K).
+//   apply (when every composite was kept): lambda_j = P_j lambda_{e(j)} + c_j
+//          for every slot at once (Phase 2 of Algorithm "Bounded-Interface
+//          Backpropagation", with the segment's carry in place of mbar_K).
+//          Otherwise the chain kernel scans each segment again from its carry.
 // Both are matrix-vector work on fp32 composites: TPR lanes per row, each
 // lane CPR consecutive columns (16-byte loads, coalesced across the row's
 // lanes), the row sum reduced by DPP within the lane group.  The carry gives
@@ -70,9 +71,9 @@ __device__ __forceinline__ void load_row(float (&p)[CPR], const float *Prow)
 }
 
 template <int R, bool BF16>
-__global__ __launch_bounds__(kThreads) void carry_kernel(const float *Pc, const float *cc,
-                                                        const void *lamK, float *carry,
-                                                        int64_t K, int64_t Lseg, int32_t S)
+__global__ __launch_bounds__(kThreads) void carry_kernel(const float *Pa, const float *ca,
+                                                        const void *lamK, float *carry, int32_t S,
+                                                        int64_t cstride, int64_t dstride)
 {
     constexpr int TPR = MatVec<R>::TPR, CPR = MatVec<R>::CPR;
     __shared__ __attribute__((aligned(16))) float sl[2][R];
@@ -90,9 +91,9 @@ __global__ __launch_bounds__(kThreads) void carry_kernel(const float *Pc, const 
     // loads are independent of lambda; only the products wait for it)
     auto fetch = [&](int32_t d, float(&p)[CPR], float &c) {
         if (d >= 1) {
-            const int64_t slot = beta * K + (int64_t)d * Lseg;  // first slot of segment d
-            load_row<CPR>(p, Pc + (slot * R + row) * R + col0);
-            c = cc && owner ? cc[slot * R + row] : 0.0f;
+            const int64_t agg = beta * cstride + d * dstride;  // aggregate of segment d
+            load_row<CPR>(p, Pa + (agg * R + row) * R + col0);
+            c = ca && owner ? ca[agg * R + row] : 0.0f;
         }
     };
     int cur = 0;
@@ -165,15 +166,15 @@ __global__ __launch_bounds__(kThreads) void apply_kernel(const float *Pc, const 
 }
 
 template <int R>
-hipError_t carry_r(const float *Pc, const float *cc, const void *lamK, bool bf16, float *carry,
-                   int64_t B, int64_t K, int64_t Lseg, int32_t S, hipStream_t st)
+hipError_t carry_r(const float *Pa, const float *ca, const void *lamK, bool bf16, float *carry,
+                   int64_t B, int32_t S, int64_t cstride, int64_t dstride, hipStream_t st)
 {
     if (bf16)
-        hipLaunchKernelGGL((carry_kernel<R, true>), dim3((unsigned)B), dim3(kThreads), 0, st, Pc,
-                           cc, lamK, carry, K, Lseg, S);
+        hipLaunchKernelGGL((carry_kernel<R, true>), dim3((unsigned)B), dim3(kThreads), 0, st, Pa,
+                           ca, lamK, carry, S, cstride, dstride);
     else
-        hipLaunchKernelGGL((carry_kernel<R, false>), dim3((unsigned)B), dim3(kThreads), 0, st, Pc,
-                           cc, lamK, carry, K, Lseg, S);
+        hipLaunchKernelGGL((carry_kernel<R, false>), dim3((unsigned)B), dim3(kThreads), 0, st, Pa,
+                           ca, lamK, carry, S, cstride, dstride);
     return hipGetLastError();
 }
 
@@ -188,17 +189,18 @@ hipError_t apply_r(const float *Pc, const float *cc, const float *carry, float *
     return hipGetLastError();
 }
 
+
 }  // namespace
 
-hipError_t launch_carry(const float *Pc, const float *cc, const void *lamK, bool lamK_bf16,
-                        float *carry, int64_t B, int64_t K, int64_t L, int32_t S, int32_t r,
-                        hipStream_t stream)
+hipError_t launch_carry(const float *Pa, const float *ca, const void *lamK, bool lamK_bf16,
+                        float *carry, int64_t B, int32_t S, int64_t cstride, int64_t dstride,
+                        int32_t r, hipStream_t stream)
 {
     switch (r) {
-    case 16: return carry_r<16>(Pc, cc, lamK, lamK_bf16, carry, B, K, L, S, stream);
-    case 32: return carry_r<32>(Pc, cc, lamK, lamK_bf16, carry, B, K, L, S, stream);
-    case 64: return carry_r<64>(Pc, cc, lamK, lamK_bf16, carry, B, K, L, S, stream);
-    default: return carry_r<128>(Pc, cc, lamK, lamK_bf16, carry, B, K, L, S, stream);
+    case 16: return carry_r<16>(Pa, ca, lamK, lamK_bf16, carry, B, S, cstride, dstride, stream);
+    case 32: return carry_r<32>(Pa, ca, lamK, lamK_bf16, carry, B, S, cstride, dstride, stream);
+    case 64: return carry_r<64>(Pa, ca, lamK, lamK_bf16, carry, B, S, cstride, dstride, stream);
+    default: return carry_r<128>(Pa, ca, lamK, lamK_bf16, carry, B, S, cstride, dstride, stream);
     }
 }
 
@@ -212,5 +214,6 @@ hipError_t launch_apply(const float *Pc, const float *cc, const float *carry, fl
     default: return apply_r<128>(Pc, cc, carry, lam, B, K, L, S, stream);
     }
 }
+
 
 }  // namespace lbi

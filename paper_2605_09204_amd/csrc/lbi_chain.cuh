@@ -9,8 +9,9 @@
 // Phase 2 of Algorithm "Bounded-Interface Backpropagation" (apply the suffix
 // products to mbar_K, every slot).  A workgroup folds one segment of one
 // chain: the whole chain (then it writes every lambda_j), or, in the
-// two-level scan, a segment whose composites it writes for the carry and
-// apply passes.
+// two-level scan, a segment: first to its aggregate (the composite at its
+// first slot), for the carry pass, then again from the segment's carry in
+// place of lambda_K, writing its lambda_j.
 //
 // Kernel design (one workgroup per chain segment, NW waves):
 //   * The running suffix composite P (R x R, fp32) is split by 16-column
@@ -420,10 +421,12 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
     // goes in the scalar offset of each access)
     const __amdgpu_buffer_rsrc_t rsA_c = __builtin_amdgcn_make_buffer_rsrc(
         (void *)A, 0, compact ? args.totalA * G::ESZ : 0, kBufferWord3);
-    float *Pout = OUT == kOutComposite ? args.Pout + first * (int64_t)(R * R) : nullptr;
+    // composites at [B][K], or only the segment aggregates at [B][S]
+    const int64_t cslot = args.agg_only ? (int64_t)blockIdx.x : first;
+    float *Pout = OUT == kOutComposite ? args.Pout + cslot * (int64_t)(R * R) : nullptr;
     float *cout = OUT == kOutComposite ? args.cout : nullptr;  // NULL: not written
     if (cout)
-        cout += first * (int64_t)R;
+        cout += cslot * (int64_t)R;
     auto ring = [&](int64_t s) { return (int)((K - s) & 3); };
     // width code of local slot x (its row blocks; x = K: lambda_K's), 0
     // before the segment.  The slot loop keeps the codes it needs in a
@@ -611,9 +614,10 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
 #pragma unroll
         for (int t = 0; t < CB; ++t) {
             const int idx = 16 * (w + NW * t) + li;
-            lk[t] = OUT == kOutLambda && idx < rK
-                        ? to_f32(((const E *)args.lamK)[beta * rK + idx])
-                        : 0.0f;
+            // (segments: lambda at this segment's end, from the carry pass)
+            lk[t] = OUT != kOutLambda || idx >= rK ? 0.0f
+                    : args.lamSeg ? args.lamSeg[(int64_t)blockIdx.x * R + idx]
+                                  : to_f32(((const E *)args.lamK)[beta * rK + idx]);
         }
     }
 
@@ -744,6 +748,8 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
     // (branch-free buffer stores; each lane writes its rows of its columns)
     auto store_composite = [&](const f4 (&P)[NRB][CB], int64_t s) {
         if constexpr (OUT == kOutComposite) {
+            if (args.agg_only && s != 0)
+                return;
             const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
                 (void *)(Pout + s * (int64_t)(R * R)), 0, R * R * (int)sizeof(float), kBufferWord3);
 #pragma unroll

@@ -37,6 +37,11 @@ struct ScanArgs {
                        // d*L .. min(K, (d+1)*L) - 1 into composites local to
                        // the segment (L = K: whole chains)
     int32_t S;         // segments per chain, ceil(K / L)
+    int32_t agg_only;  // kOutComposite: write only each segment's aggregate
+                       // (its composite at the first slot), to Pout / cout
+                       // indexed [B][S] instead of [B][K]
+    const float *lamSeg;  // kOutLambda with segments: lambda at the end of each
+                          // segment, [B][S][R] fp32 (NULL: lamK, whole chains)
     uint32_t *progress;  // [B] or NULL (kOutLambda, whole chains): raised to the
                          // number of final adjoints after every pchunk slots
     int32_t pchunk;
@@ -80,12 +85,16 @@ hipError_t launch_chain_ksplit_f32x(const ChainLaunch &c);
 
 // Segment carries of the two-level scan: carry[beta][d] is lambda at the end
 // of segment d (lambda_K for the last), obtained by applying the segment
-// aggregates (the composites at each segment's first slot) right to left.
-hipError_t launch_carry(const float *Pc, const float *cc, const void *lamK, bool lamK_bf16,
-                        float *carry, int64_t B, int64_t K, int64_t L, int32_t S, int32_t r,
-                        hipStream_t stream);
+// aggregates right to left; the aggregate of segment d of chain beta sits at
+// index beta * cstride + d * dstride of Pa (r x r) and ca (r; NULL: no
+// affine term): (K, L) when every composite was kept, (S, 1) for aggregates
+// only.
+hipError_t launch_carry(const float *Pa, const float *ca, const void *lamK, bool lamK_bf16,
+                        float *carry, int64_t B, int32_t S, int64_t cstride, int64_t dstride,
+                        int32_t r, hipStream_t stream);
 
-// lambda_j = Pc_j carry[segment of j] + cc_j for every slot of every chain.
+// lambda_j = Pc_j carry[segment of j] + cc_j for every slot of every chain
+// (every composite kept, [B][K]).
 hipError_t launch_apply(const float *Pc, const float *cc, const float *carry, float *lam,
                         int64_t B, int64_t K, int64_t L, int32_t S, int32_t r,
                         hipStream_t stream);

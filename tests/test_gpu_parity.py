@@ -453,6 +453,22 @@ def test_two_level_parity(B, K, r, dtype, arith):
                      f"two-level B{B} K{K} r{r} {dtype} {arith} affine={affine}")
 
 
+@pytest.mark.parametrize("affine", [True, False])
+@pytest.mark.parametrize("B", [81, 82])
+def test_two_level_both_forms(B, affine):
+    """At r = 64 and K = 200, B = 81 keeps every segment composite (253.1 MiB
+    of fp32) and applies them in one pass; B = 82 (256.3 MiB) keeps only the
+    segment aggregates and scans each segment again from its carry.  Both against the
+    oracle on every chain, with and without b, and the widths hint changing
+    nothing."""
+    K, r = 200, 64
+    _say(f"[two-level] B={B} K={K} affine={affine}")
+    x = synth.random_chain(B, K, r, dtype="f32", seed=61 + B, affine=affine, device="cuda:0")
+    lam = run_gpu(x, algo="two_level")
+    assert_close(lam.cpu().numpy(), ref(x.to("cpu")), TOL["f32"], f"two-level B{B}")
+    assert torch.equal(lam, run_gpu(x, widths=[r] * (K + 1), algo="two_level"))
+
+
 @pytest.mark.parametrize("arith", ["split", "mfma"])
 def test_two_level_orthogonal_long_chain(arith):
     """Nothing decays: every segment's carry and every apply must be right."""
