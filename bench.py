@@ -362,26 +362,26 @@ def bench_phase1(args) -> int:
 # CPU baseline: the oracle on a bounded sample of the same workload
 # ----------------------------------------------------------------------------
 
-def cpu_baseline(x, target_s: float = 10.0):
+def cpu_baseline(x, target_s: float = 10.0, nthreads: int = 0):
     import oracle
     import torch
 
     wl = x.workload
-    threads = oracle.threads(0)
+    threads = oracle.threads(nthreads)
     n_cal = min(wl.B, max(1, threads))
     host = x.chains(torch.arange(n_cal)).to("cpu")
     t0 = time.perf_counter()
-    oracle.recurrence(host.A, host.b, host.lamK)
+    oracle.recurrence(host.A, host.b, host.lamK, nthreads)
     t_cal = max(time.perf_counter() - t0, 1e-6)
     n = int(min(wl.B, max(n_cal, n_cal * target_s / t_cal)))
     host = x.chains(torch.arange(n)).to("cpu")
     t0 = time.perf_counter()
-    oracle.recurrence(host.A, host.b, host.lamK)
+    oracle.recurrence(host.A, host.b, host.lamK, nthreads)
     t = time.perf_counter() - t0
     reps = 1
     while t < target_s and reps < 4096:  # whole batch is quick: repeat it
         t0 = time.perf_counter()
-        oracle.recurrence(host.A, host.b, host.lamK)
+        oracle.recurrence(host.A, host.b, host.lamK, nthreads)
         t += time.perf_counter() - t0
         reps += 1
     return {
@@ -657,6 +657,10 @@ def main(argv=None) -> int:
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle baseline", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(x)
+        # the same oracle on one core (a smaller sample)
+        one = cpu_baseline(x, target_s=4.0, nthreads=1)
+        out["extra"]["cpu_oracle_one_core"] = {"value": one["value"], "unit": one["unit"],
+                                               "sample": one["sample"]}
     print(json.dumps(out), flush=True)
     return 0
 
