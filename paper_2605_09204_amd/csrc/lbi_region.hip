@@ -54,7 +54,9 @@ constexpr int BM = 128, BN = 128, BK = 64;
 constexpr int TILE = 128 * BK;  // bf16 elements of one LDS tile (no padding)
 constexpr float kLnEps = 1e-5f;
 
-__device__ __forceinline__ float sigm(float h) { return 1.0f / (1.0f + __expf(-h)); }
+// The logistic function through the hardware reciprocal (1 ulp): it needs no
+// correctly rounded division, and rcp(inf) = 0 keeps the saturated end exact.
+__device__ __forceinline__ float sigm(float h) { return __builtin_amdgcn_rcpf(1.0f + __expf(-h)); }
 __device__ __forceinline__ float silu(float h) { return h * sigm(h); }
 __device__ __forceinline__ float dsilu(float h)
 {
@@ -280,6 +282,8 @@ __global__ __launch_bounds__(kT) void xpart_kernel(RegionArgs q)
         return;
     const __bf16 *x = (const __bf16 *)q.x_embed + b * q.L * q.D + c;
     float s[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+    // (unrolled: eight token loads in flight rather than one)
+#pragma unroll 8
     for (int64_t l = l0; l < l1; ++l) {
         const bf16x8 v = *(const bf16x8 *)(x + l * q.D);
 #pragma unroll
@@ -301,6 +305,7 @@ __global__ __launch_bounds__(kT) void xfin_kernel(RegionArgs q)
         return;
     const int64_t nch = (q.L + 63) / 64;
     float s = 0.0f;
+#pragma unroll 8
     for (int64_t ch = 0; ch < nch; ++ch)
         s += q.xpart[(b * nch + ch) * q.D + c];
     q.xbar[b * q.D + c] = s / (float)q.L;
