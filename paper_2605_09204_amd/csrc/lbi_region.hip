@@ -495,7 +495,7 @@ __global__ __launch_bounds__(64) void ln_fwd_kernel(RegionArgs q)
 }
 
 // ---- gemm_nt: C[M][N] = A[M][K] B[N][K]^T per batch, with the epilogue
-//      v = acc * scale[batch][row / grp][col] + add[batch][row][col] ------------
+//      v = acc * scale[batch][row >> grp_shift][col] + add[batch][row][col] ------
 struct GemmOp {
     const __bf16 *A;
     int64_t lda, sA;
@@ -507,7 +507,7 @@ struct GemmOp {
     int K;
     const float *scale;  // NULL: 1
     int64_t s_scale_b, s_scale_g;
-    int grp;
+    int grp_shift;  // rows per scale row: 2^grp_shift (1, or the interface width)
     const __bf16 *add;  // NULL: 0 (ld ldc, batch stride sC)
     bool out_bf16;
 };
@@ -578,7 +578,7 @@ __global__ __launch_bounds__(kT) void gemm_nt_kernel(GemmOp g)
                     continue;
                 float val = acc[i][j][v];
                 if (g.scale)
-                    val *= g.scale[z * g.s_scale_b + (row / g.grp) * g.s_scale_g + col];
+                    val *= g.scale[z * g.s_scale_b + (row >> g.grp_shift) * g.s_scale_g + col];
                 const int64_t o = z * g.sC + row * g.ldc + col;
                 if (g.add)
                     val += (float)g.add[o];
@@ -703,30 +703,32 @@ hipError_t launch_region_jacobians(const RegionArgs &q, hipStream_t st)
     const __bf16 *Wd2 = (const __bf16 *)q.W_d2, *W1 = (const __bf16 *)q.W1;
     const __bf16 *W2 = (const __bf16 *)q.W2, *We1 = (const __bf16 *)q.W_e1;
     const __bf16 *We2 = (const __bf16 *)q.W_e2;
+    // the interface width is a power of two (16 .. 128): scale rows by shift
+    const int rs = r == 16 ? 4 : (r == 32 ? 5 : (r == 64 ? 6 : 7));
     GemmOp g;
     // Jdec^T[k] = P1[k] W_d2[k]^T                      (B r x D, K = D)
     g = GemmOp{q.P1, D, Br * D, Wd2, D, (int64_t)D * D, q.JdT, D, Br * D, Br, D, D,
-               nullptr, 0, 0, 1, nullptr, true};
+               nullptr, 0, 0, 0, nullptr, true};
     if ((e = gemm(g, q.K, st)) != hipSuccess)
         return e;
     // U'^T[k] = (Jdec^T W1[k]^T) * gbar[b][k][x]        (B r x X, K = D)
     g = GemmOp{q.JdT, D, Br * D, W1, D, (int64_t)X * D, q.UT, X, Br * X, Br, X, D,
-               q.gbar, X, q.K * (int64_t)X, r, nullptr, true};
+               q.gbar, X, q.K * (int64_t)X, rs, nullptr, true};
     if ((e = gemm(g, q.K, st)) != hipSuccess)
         return e;
     // dp^T[k] = U'^T W2[k]^T + Jdec^T                   (B r x D, K = X)
     g = GemmOp{q.UT, X, Br * X, W2, X, (int64_t)D * X, q.dpT, D, Br * D, Br, D, X,
-               nullptr, 0, 0, 1, q.JdT, true};
+               nullptr, 0, 0, 0, q.JdT, true};
     if ((e = gemm(g, q.K, st)) != hipSuccess)
         return e;
     // T'^T[k] = (dp^T W_e1[k]^T) * silu'(e)[b][k][h]    (B r x D, K = D)
     g = GemmOp{q.dpT, D, Br * D, We1, D, (int64_t)D * D, q.TT, D, Br * D, Br, D, D,
-               q.se, D, q.K * (int64_t)D, r, nullptr, true};
+               q.se, D, q.K * (int64_t)D, rs, nullptr, true};
     if ((e = gemm(g, q.K, st)) != hipSuccess)
         return e;
     // Jenc^T[k] = T'^T W_e2[k]^T                        (B r x r, K = D), fp32
     g = GemmOp{q.TT, D, Br * D, We2, D, (int64_t)r * D, q.JencT, r, Br * r, Br, r, D,
-               nullptr, 0, 0, 1, nullptr, false};
+               nullptr, 0, 0, 0, nullptr, false};
     if ((e = gemm(g, q.K, st)) != hipSuccess)
         return e;
     hipLaunchKernelGGL(ln_jac_kernel, dim3((unsigned)BKn), dim3(kT), (size_t)3 * r * sizeof(float),
