@@ -7,7 +7,7 @@ line.  Default workload: ``long_chain`` (B=512 chains, K=512 regions, r=64,
 fp32), the largest batched r=64 workload.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                  [--math split|mfma] [--no-cpu-baseline] [--copy-calibration MiB]
+                  [--math split|mfma|bf16single] [--no-cpu-baseline] [--copy-calibration MiB]
 
 Accounting (flop = 2 per multiply-add; the paper counts r^3 per r x r
 product, i.e. one per multiply-add, in its scan-negligibility estimate):
@@ -142,7 +142,7 @@ def mfma_flops_executed(wl, math: str) -> int:
     w = widths_of(wl)
     rK = w[wl.K]
     mode = mode_of(wl, math)
-    reps = {"f32-mfma": 1, "bf16": 2, "f32-split": 6}[mode]
+    reps = {"f32-mfma": 1, "bf16": 2, "bf16-single": 1, "f32-split": 6}[mode]
 
     def blk(x):
         return 16 * (1 << max(0, (-(-x // 16) - 1).bit_length()))
@@ -160,7 +160,7 @@ def mfma_flops_executed(wl, math: str) -> int:
 
 def mode_of(wl, math: str) -> str:
     if wl.dtype == "bf16":
-        return "bf16"
+        return "bf16-single" if math == "bf16single" else "bf16"
     if math == "split" and wl.r <= 64:
         return "f32-split"
     return "f32-mfma"
@@ -405,9 +405,11 @@ def main(argv=None) -> int:
     ap.add_argument("--warmup", type=int, default=None,
                     help="untimed launches (default: >= 5 and >= %.2f s of launches)" % WARMUP_MIN_S)
     ap.add_argument("--workload", default="long_chain")
-    ap.add_argument("--math", choices=["split", "mfma"], default="split",
+    ap.add_argument("--math", choices=["split", "mfma", "bf16single"], default="split",
                     help="float32 arithmetic: three-part bf16 splits on the bf16 matrix "
-                         "cores (the library default) or the fp32 matrix cores")
+                         "cores (the library default) or the fp32 matrix cores; for bf16 "
+                         "storage, bf16single feeds the running composite back rounded "
+                         "once to bf16 (opt-in, lower accuracy)")
     ap.add_argument("--algo", choices=["auto", "chain", "two_level", "chain_wave", "chain_splitk"],
                     default="auto",
                     help="scan algorithm (auto: the library's choice)")
@@ -491,7 +493,8 @@ def main(argv=None) -> int:
     lam = torch.empty((wl.B, wl.K, wl.r), dtype=torch.float32, device=dev)
     hint = wl.widths
 
-    math = binding.LBI_MATH_F32_SPLIT if args.math == "split" else binding.LBI_MATH_F32_MFMA
+    math = {"split": binding.LBI_MATH_F32_SPLIT, "mfma": binding.LBI_MATH_F32_MFMA,
+            "bf16single": binding.LBI_MATH_BF16_SINGLE}[args.math]
     algo = {"auto": binding.LBI_ALGO_AUTO, "chain": binding.LBI_ALGO_CHAIN,
             "two_level": binding.LBI_ALGO_TWO_LEVEL,
             "chain_wave": binding.LBI_ALGO_CHAIN_WAVE,
@@ -588,7 +591,7 @@ def main(argv=None) -> int:
     if need:
         mapping = "two-level scan (segments in parallel)"
     elif args.algo == "chain_wave" or (auto_adj and wl.dtype == "bf16" and wl.r <= 32
-                                       and wl.B <= 8192):
+                                       and wl.B <= 8192 and args.math != "bf16single"):
         mapping = "one wavefront per chain"
     elif args.algo == "chain_splitk" or (auto_adj and wl.dtype == "f32" and args.math == "split"
                                          and wl.r == 64 and wl.B <= 256):
@@ -614,7 +617,8 @@ def main(argv=None) -> int:
         roof = {"bound": "hbm", "achieved": gbs, "peak": PEAK["hbm_gbs"], "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof["traffic"] = (load_traffic(wl.name) if args.op == "adjoints" and
-                       (args.math == "split" or wl.dtype == "bf16") else None)
+                       (args.math == "split" or (wl.dtype == "bf16" and
+                                                 args.math != "bf16single")) else None)
     out = {
         "metric": METRIC,
         "value": value,

@@ -49,7 +49,7 @@ extern "C" {
 /* HIP stream handle (the same type as hipStream_t). */
 typedef struct ihipStream_t *lbi_stream_t;
 
-#define LBI_ABI_VERSION 8
+#define LBI_ABI_VERSION 9
 
 /* Largest K for which a widths hint is used (longer chains run unhinted,
  * which gives identical results). */
@@ -60,17 +60,31 @@ typedef enum {
     LBI_BF16 = 1  /* stored as bfloat16; bf16 MFMA products, fp32 sums      */
 } lbi_dtype;
 
-/* How float32 inputs are multiplied (lbi_scan_backward_ex,
- * lbi_scan_suffix_products).  bf16 inputs always use the bf16 matrix cores. */
+/* How the products are formed (lbi_scan_backward_ex,
+ * lbi_scan_suffix_products, lbi_scan_backward_streaming,
+ * lbi_scan_backward_ragged).  bf16 inputs always use the bf16 matrix cores. */
 typedef enum {
     LBI_MATH_DEFAULT = 0,   /* the library's choice: LBI_MATH_F32_SPLIT for
-                             * r <= 64, LBI_MATH_F32_MFMA for r = 128           */
+                             * fp32 at r <= 64, LBI_MATH_F32_MFMA for fp32 at
+                             * r = 128; for bf16 the running fp32 composite is
+                             * fed back to the matrix cores as bf16 hi + lo
+                             * (two products), so the only bf16 rounding is
+                             * the inputs'                                      */
     LBI_MATH_F32_MFMA = 1,  /* fp32 products on the fp32 matrix cores            */
-    LBI_MATH_F32_SPLIT = 2  /* fp32 products from exact three-part bf16 splits
+    LBI_MATH_F32_SPLIT = 2, /* fp32 products from exact three-part bf16 splits
                              * of both operands on the bf16 matrix cores (the
                              * six partial products down to 2^-16 of the leading
                              * one), fp32 accumulation; r = 128 falls back to
                              * LBI_MATH_F32_MFMA                                 */
+    LBI_MATH_BF16_SINGLE = 3 /* bf16 inputs only (else LBI_ERR_DTYPE): the
+                             * running composite is fed back rounded once to
+                             * bf16 (one product instead of two).  Faster; the
+                             * relative error grows with the chain, about
+                             * 2^-9 per slot (measured about 7e-3 at K = 32 on
+                             * the bf16 token-batch recipe, against 2e-6 for
+                             * the default).  Not taken by the wavefront-per-
+                             * chain scan (LBI_ALGO_CHAIN_WAVE: LBI_ERR_DTYPE;
+                             * AUTO then uses the workgroup kernel)            */
 } lbi_math;
 
 /* How the slots of a chain are scanned (lbi_scan_backward_ex). */

@@ -22,6 +22,7 @@ LBI_MAX_HINT_K = 2047
 LBI_MATH_DEFAULT = 0
 LBI_MATH_F32_MFMA = 1
 LBI_MATH_F32_SPLIT = 2
+LBI_MATH_BF16_SINGLE = 3
 LBI_ALGO_AUTO = 0
 LBI_ALGO_CHAIN = 1
 LBI_ALGO_TWO_LEVEL = 2
@@ -215,7 +216,7 @@ def lbi_scan_backward_ex(A: torch.Tensor, b: Optional[torch.Tensor], lambda_K: t
                          widths: Optional[Sequence[int]] = None, math: int = LBI_MATH_DEFAULT,
                          algo: int = LBI_ALGO_AUTO, lam: Optional[torch.Tensor] = None,
                          workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """As lbi_scan_backward_widths, with the float32 arithmetic chosen by ``math``
+    """As lbi_scan_backward_widths, with the arithmetic chosen by ``math``
     and the scan by ``algo``."""
     lam, args = _marshal(A, b, lambda_K, lam, workspace, stream, algo)
     warr, wptr = _widths_arg(widths, int(A.shape[1]))

@@ -118,7 +118,7 @@ lbi_algo resolve_algo(lbi_algo algo, int64_t B, int64_t K, int32_t r, lbi_dtype 
     if (algo != LBI_ALGO_AUTO)
         return algo;
     const lbi_algo chain =
-        dt == LBI_BF16 && r <= 32 && B <= 8192 ? LBI_ALGO_CHAIN_WAVE
+        dt == LBI_BF16 && math != LBI_MATH_BF16_SINGLE && r <= 32 && B <= 8192 ? LBI_ALGO_CHAIN_WAVE
         : dt == LBI_F32 && math != LBI_MATH_F32_MFMA && r == 64 && B <= kSplitKMaxB
             ? LBI_ALGO_CHAIN_SPLITK
             : LBI_ALGO_CHAIN;
@@ -136,7 +136,10 @@ lbi_status check_common(lbi_dtype dt, lbi_math math, int32_t r, int64_t B, int64
 {
     if (dt != LBI_F32 && dt != LBI_BF16)
         return LBI_ERR_DTYPE;
-    if (math != LBI_MATH_DEFAULT && math != LBI_MATH_F32_MFMA && math != LBI_MATH_F32_SPLIT)
+    if (math != LBI_MATH_DEFAULT && math != LBI_MATH_F32_MFMA && math != LBI_MATH_F32_SPLIT &&
+        math != LBI_MATH_BF16_SINGLE)
+        return LBI_ERR_DTYPE;
+    if (math == LBI_MATH_BF16_SINGLE && dt != LBI_BF16)
         return LBI_ERR_DTYPE;
     if (!supported_r(r))
         return LBI_ERR_UNSUPPORTED_R;
@@ -173,7 +176,7 @@ bool encode_widths(const int32_t *widths, int64_t K, int32_t r, ChainLaunch &c)
 hipError_t launch_chain_mode(const ChainLaunch &c, lbi_dtype dt, lbi_math math)
 {
     if (dt == LBI_BF16)
-        return launch_chain_bf16(c);
+        return math == LBI_MATH_BF16_SINGLE ? launch_chain_bf16r1(c) : launch_chain_bf16(c);
     if (math == LBI_MATH_F32_MFMA || c.r == 128)
         return launch_chain_f32(c);
     return launch_chain_f32x(c);
@@ -191,7 +194,7 @@ lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam,
         return LBI_ERR_DTYPE;
     if (algo == LBI_ALGO_TWO_LEVEL && !two_level_possible(B, K))
         return LBI_ERR_SHAPE;
-    if (algo == LBI_ALGO_CHAIN_WAVE && dt != LBI_BF16)
+    if (algo == LBI_ALGO_CHAIN_WAVE && (dt != LBI_BF16 || math == LBI_MATH_BF16_SINGLE))
         return LBI_ERR_DTYPE;
     if (algo == LBI_ALGO_CHAIN_WAVE && r > 64)
         return LBI_ERR_UNSUPPORTED_R;

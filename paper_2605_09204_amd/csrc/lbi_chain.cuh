@@ -39,6 +39,9 @@
 //       kBF16  bf16 storage, v_mfma_f32_16x16x32_bf16; the fp32 composite is
 //              fed back as bf16 hi + lo (two MFMAs), so the only bf16
 //              rounding is the inputs';
+//       kBF16R1  the same, with the composite fed back rounded once to bf16
+//              (one MFMA): a relative error of about 2^-9 per slot, which
+//              grows with the chain's length (opt-in);
 //       kF32X  fp32 storage on the bf16 matrix cores: A_j and P are each cut
 //              into three bf16 parts whose sum is exactly the fp32 value
 //              (the value rounded to nearest, then its remainder, twice), and
@@ -82,6 +85,7 @@ template <> struct Mode<kBF16> {
     typedef __bf16 L;
     static constexpr int PLANES = 1, PAD = 8;
 };
+template <> struct Mode<kBF16R1> : Mode<kBF16> {};
 template <> struct Mode<kF32X> {
     typedef float E;
     typedef __bf16 L;
@@ -115,7 +119,7 @@ template <int R, int M, int NCA> struct Geo {
     static constexpr int SHIFT_S = ilog2(LPR) - ilog2(CPT);      // staging reduce layout
     // slots prefetched (bf16 at r <= 32 takes a third; at r = 64 the third
     // costs the fifth wave per SIMD, which is worth more)
-    static constexpr int NPF = (M == kBF16 && R <= 32) ? 3 : 2;
+    static constexpr int NPF = ((M == kBF16 || M == kBF16R1) && R <= 32) ? 3 : 2;
     static constexpr int WPF = R > 64 ? R / 64 : 1;              // waves per finalize
     static constexpr int NWF = NW / WPF;                         // finalizing wave groups
     static_assert(NCA % NW == 0 && CB >= 1, "tile geometry");
@@ -223,7 +227,26 @@ __device__ __forceinline__ void combine(f4 (&Pn)[R / 16][NCA / waves_for(R)],
                     x[t][v] = P[2 * p][t][v];
                     x[t][v + 4] = kPairs ? P[kPairs ? 2 * p + 1 : 0][t][v] : 0.0f;
                 }
-            if constexpr (M == kBF16) {
+            if constexpr (M == kBF16R1) {
+                // P rounded once to bf16 (RNE), two values per instruction
+                bf16x8 bh[CB];
+#pragma unroll
+                for (int t = 0; t < CB; ++t) {
+                    u4 hh;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        hh[e] = __builtin_bit_cast(
+                            uint32_t, __builtin_convertvector(f2{x[t][2 * e], x[t][2 * e + 1]}, bf16x2));
+                    bh[t] = __builtin_bit_cast(bf16x8, hh);
+                }
+#pragma unroll
+                for (int I = 0; I < NR; ++I) {
+                    const bf16x8 a = a_operand<R, PITCH>(sAbuf, I, p, li, g);
+#pragma unroll
+                    for (int t = 0; t < CB; ++t)
+                        Pn[I][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bh[t], Pn[I][t], 0, 0, 0);
+                }
+            } else if constexpr (M == kBF16) {
                 // P = hi + lo (RNE hi, exact remainder, RNE lo), converted
                 // two values per instruction
                 bf16x8 bh[CB], bl[CB];
@@ -573,7 +596,7 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
             L *dst = sA[buf];
             if constexpr (M == kF32) {
                 *(u4 *)&dst[tpos(row, scol)] = src;
-            } else if constexpr (M == kBF16) {
+            } else if constexpr (M == kBF16 || M == kBF16R1) {
                 if constexpr (PERM) {
                     *(u2 *)&dst[tpos(row, lds_col<PERM>(scol))] = u2{src[0], src[1]};
                     *(u2 *)&dst[tpos(row, lds_col<PERM>(scol + 4))] = u2{src[2], src[3]};

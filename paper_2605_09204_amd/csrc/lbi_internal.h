@@ -11,9 +11,10 @@
 namespace lbi {
 
 // Arithmetic of the chain kernel: fp32 storage on the fp32 matrix cores; bf16
-// storage on the bf16 matrix cores; fp32 storage as exact three-part bf16
-// splits on the bf16 matrix cores.
-enum : int { kF32 = 0, kBF16 = 1, kF32X = 2 };
+// storage on the bf16 matrix cores (the fp32 composite fed back as hi + lo, or
+// rounded once); fp32 storage as exact three-part bf16 splits on the bf16
+// matrix cores.
+enum : int { kF32 = 0, kBF16 = 1, kF32X = 2, kBF16R1 = 3 };
 
 // What the chain kernel writes: every adjoint lambda_j, or every suffix
 // composite (P_j, c_j) of its segment.
@@ -71,6 +72,7 @@ struct ChainLaunch {
 hipError_t launch_chain_f32(const ChainLaunch &c);
 hipError_t launch_chain_f32x(const ChainLaunch &c);
 hipError_t launch_chain_bf16(const ChainLaunch &c);
+hipError_t launch_chain_bf16r1(const ChainLaunch &c);
 
 // The chain scan with one wavefront per chain (bf16 storage, r <= 64, whole
 // chains, kOutLambda without progress counters; a widths hint is ignored).

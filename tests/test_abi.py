@@ -56,7 +56,7 @@ def test_header_compiles_as_c():
 
 
 def test_version_and_status_strings():
-    assert binding.lbi_abi_version() == 8
+    assert binding.lbi_abi_version() == 9
     assert binding.lbi_status_string(0) == "LBI_OK"
     for code in range(1, 9):
         assert binding.lbi_status_string(code).startswith("LBI_ERR_")
@@ -78,7 +78,7 @@ def call(A=PA, b=PB, L=PL, out=POUT, B=2, K=3, r=64, dt=0, ws=None, wsb=0, width
 
 def test_argument_errors():
     assert call(dt=7) == 3                      # LBI_ERR_DTYPE
-    assert call(math=3) == 3 and call(math=-1) == 3 and call(dt=1, math=9) == 3
+    assert call(math=4) == 3 and call(math=-1) == 3 and call(dt=1, math=9) == 3
     for r in (0, 8, 48, 96, 256):
         assert call(r=r) == 4                   # LBI_ERR_UNSUPPORTED_R
     assert call(K=0) == 2 and call(B=-1) == 2   # LBI_ERR_SHAPE
@@ -150,6 +150,18 @@ def test_chain_splitk_argument_errors():
     assert call(algo=5) == 3                    # not an lbi_algo
     assert binding.lbi_scan_backward_workspace_bytes_ex(256, 32, 64, 0, 4) == 0
     assert binding.lbi_scan_backward_workspace_bytes_ex(2, 512, 64, 0, 4) == 0
+
+
+def test_bf16_single_argument_errors():
+    # single-rounding arithmetic: bf16 storage only, not on the wavefront-per-
+    # chain scan; rejected before any pointer is touched
+    assert call(math=3) == 3                    # fp32 storage: LBI_ERR_DTYPE
+    assert call(dt=1, r=32, math=3, algo=3) == 3
+    assert call(dt=1, r=32, math=3, A=None) == 1
+    assert call(dt=1, r=32, math=3, algo=1, A=None) == 1
+    f = binding.load().lbi_scan_suffix_products
+    assert f(PA, PB, POUT, PL, 2, 3, 64, 0, None, None, 3) == 3
+    assert f(None, PB, POUT, PL, 2, 3, 64, 1, None, None, 3) == 1
 
 
 def test_suffix_products_argument_errors():

@@ -1,0 +1,132 @@
+"""The single-rounding bf16 arithmetic (LBI_MATH_BF16_SINGLE) against the
+oracle, through the C-ABI (needs a GPU).
+
+In this arithmetic the running fp32 composite is rounded once to bf16 before
+each product (round to nearest even, a relative error of at most 2^-9 per
+element), instead of being fed back as an exact hi + lo pair.  Those
+roundings add up along the chain like a random walk, so the relative
+Frobenius error of lambda grows like sqrt(K) 2^-9 times a constant of order
+one; the tolerance below is the bf16 storage tolerance, 2e-2, up to K = 32
+and 2e-2 sqrt(K / 32) beyond.  Permutation inputs (every composite a 0/1
+matrix, exact in bf16) must still match bit for bit.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2605_09204_amd import binding, synth
+
+pytestmark = pytest.mark.gpu
+
+SINGLE = binding.LBI_MATH_BF16_SINGLE
+ALGO_CHAIN = binding.LBI_ALGO_CHAIN
+ALGO_TWO = binding.LBI_ALGO_TWO_LEVEL
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def tol_for(K):
+    return 2e-2 * math.sqrt(max(1.0, K / 32.0))
+
+
+def scan(x, algo=binding.LBI_ALGO_AUTO, math_=SINGLE, widths=None):
+    dev = torch.device("cuda:0")
+    lam = binding.lbi_scan_backward_ex(x.A.to(dev), None if x.b is None else x.b.to(dev),
+                                       x.lamK.to(dev), widths, math_, algo)
+    torch.cuda.synchronize()
+    return lam
+
+
+def ref(x, idx=None):
+    if idx is not None:
+        x = x.chains(idx)
+    return oracle.recurrence(x.A, x.b, x.lamK)
+
+
+def check(got, want, tol, what):
+    got = np.asarray(got, dtype=np.float64)
+    err = oracle.rel_frobenius(got, want)
+    _say(f"  {what}: rel-Frobenius {err:.3e} (tol {tol:.1e})")
+    assert err <= tol, f"{what}: relative Frobenius error {err:.3e} > {tol:.1e}"
+    scale = np.abs(want).reshape(want.shape[0], -1).max(axis=1)
+    diff = np.abs(got - want).reshape(want.shape[0], -1).max(axis=1)
+    bad = diff > 4 * tol * np.maximum(scale, 1e-30)
+    assert not bad.any(), f"{what}: elementwise error in chains {np.nonzero(bad)[0][:8]}"
+    return err
+
+
+@pytest.mark.parametrize("B,K,r", [(1, 1, 16), (3, 2, 64), (5, 17, 32), (2, 32, 64),
+                                   (4, 40, 16), (3, 33, 128), (2, 96, 64)])
+@pytest.mark.parametrize("affine", [True, False])
+def test_single_rounding_shapes(B, K, r, affine):
+    _say(f"[bf16-single] B={B} K={K} r={r} affine={affine}")
+    x = synth.random_chain(B, K, r, dtype="bf16", seed=7 * K + r, affine=affine)
+    lam = scan(x, algo=ALGO_CHAIN)
+    check(lam.cpu().numpy(), ref(x), tol_for(K), f"B{B} K{K} r{r}")
+    # AUTO (the workgroup kernel or the two-level scan, never the wavefront-
+    # per-chain kernel, which rejects this arithmetic) meets the same bound
+    check(scan(x).cpu().numpy(), ref(x), tol_for(K), f"B{B} K{K} r{r} auto")
+
+
+@pytest.mark.parametrize("r", [16, 32, 64, 128])
+def test_single_rounding_permutations_exact(r):
+    for K in (1, 7, 40):
+        x = synth.permutation_chain(3, K, r, dtype="bf16", seed=K + 3 * r)
+        got = scan(x, algo=ALGO_CHAIN).cpu().numpy().astype(np.float64)
+        assert np.array_equal(got, ref(x)), f"r={r} K={K}"
+
+
+def test_single_rounding_token_batches_full_size():
+    """The bf16 token-batch workload (B = 4096 chains of K = 32 slots at
+    r = 64, b = NULL) at full size, in the launch the bench times: sampled
+    chains against the oracle, and the whole output against the default
+    (hi + lo) arithmetic."""
+    wl = synth.WORKLOADS["bf16_tokens"]
+    _say(f"[bf16-single] {wl.name} B={wl.B} K={wl.K} r={wl.r}")
+    x = synth.generate(wl, device="cuda:0")
+    lam = scan(x)
+    g = torch.Generator().manual_seed(9)
+    idx = torch.cat([torch.tensor([0, wl.B - 1]),
+                     torch.randperm(wl.B - 2, generator=g)[:46] + 1]).sort().values
+    check(lam[idx.to(lam.device)].cpu().numpy(), ref(x.to("cpu"), idx), tol_for(wl.K),
+          "bf16_tokens single")
+    base = scan(x, math_=binding.LBI_MATH_DEFAULT)
+    d = oracle.rel_frobenius(lam.cpu().double().numpy(), base.cpu().double().numpy())
+    _say(f"  against hi + lo: {d:.3e}")
+    assert 0 < d <= tol_for(wl.K)
+
+
+@pytest.mark.parametrize("B,K,r", [(2, 130, 16), (1, 513, 64)])
+def test_single_rounding_two_level(B, K, r):
+    _say(f"[bf16-single two-level] B={B} K={K} r={r}")
+    x = synth.random_chain(B, K, r, dtype="bf16", seed=K + r, affine=True,
+                           spectrum="concentrated" if K > 200 else "uniform")
+    lam = scan(x, algo=ALGO_TWO)
+    check(lam.cpu().numpy(), ref(x), tol_for(K), f"two-level B{B} K{K} r{r}")
+
+
+def test_single_rounding_export_and_streaming():
+    """The same arithmetic through the composite export and the streaming
+    scan: the export applied to lambda_K gives the adjoints, and the
+    streaming scan equals the chain scan bit for bit."""
+    B, K, r = 3, 21, 64
+    x = synth.random_chain(B, K, r, dtype="bf16", seed=77)
+    dev = torch.device("cuda:0")
+    A, b, lk = x.A.to(dev), x.b.to(dev), x.lamK.to(dev)
+    P, c = binding.lbi_scan_suffix_products(A, b, math=SINGLE)
+    torch.cuda.synchronize()
+    lam = np.einsum("bkij,bj->bki", P.cpu().double().numpy(), x.lamK.double().numpy()) \
+        + c.cpu().double().numpy()
+    check(lam, ref(x), tol_for(K), "export applied")
+    progress = torch.zeros(B, dtype=torch.int32, device=dev)
+    s = binding.lbi_scan_backward_streaming(A, b, lk, progress, 4, math=SINGLE)
+    torch.cuda.synchronize()
+    assert torch.equal(s, scan(x, algo=ALGO_CHAIN))
+    assert progress.tolist() == [K] * B
