@@ -130,3 +130,29 @@ def test_single_rounding_export_and_streaming():
     torch.cuda.synchronize()
     assert torch.equal(s, scan(x, algo=ALGO_CHAIN))
     assert progress.tolist() == [K] * B
+
+
+@pytest.mark.parametrize("algo", [ALGO_CHAIN, ALGO_TWO], ids=["chain", "two_level"])
+@pytest.mark.parametrize("r", [64, 128])
+def test_single_rounding_widths_hint_and_ragged(r, algo):
+    """Mixed widths: the widths hint changes nothing (zero padding rounds
+    exactly), the padding stays zero, and the compact entry point equals the
+    padded hinted chain scan bit for bit."""
+    K = 23
+    widths = synth.cyclic_widths(K, (16, 32, 64) if r == 64 else (32, 64, 128))
+    _say(f"[bf16-single widths] r={r} algo={algo}")
+    x = synth.random_chain(6, K, r, dtype="bf16", seed=4 + r, widths=widths)
+    plain = scan(x, algo=algo)
+    hinted = scan(x, algo=algo, widths=widths)
+    assert torch.equal(plain, hinted)
+    for j in range(K):
+        if widths[j] < r:
+            assert float(hinted[:, j, widths[j]:].abs().max()) == 0.0
+    check(hinted.cpu().numpy(), ref(x), tol_for(K), f"hinted r{r}")
+    if algo == ALGO_CHAIN:
+        dev = torch.device("cuda:0")
+        p = synth.pack_ragged(x)
+        lam_c = binding.lbi_scan_backward_ragged(p.A.to(dev), p.b.to(dev), p.lamK.to(dev),
+                                                 p.widths, SINGLE)
+        torch.cuda.synchronize()
+        assert torch.equal(synth.unpack_ragged(lam_c, p.widths, r).cpu(), hinted.cpu())
