@@ -219,11 +219,14 @@ lbi_status lbi_scan_backward_widths(const void *A, const void *b, const void *la
 
 /*
  * As lbi_scan_backward_widths (widths_host may be NULL), with the arithmetic
- * for float32 inputs chosen by `math` and the scan by `algo`; the workspace
- * must hold lbi_scan_backward_workspace_bytes_ex(B, K, r, dt, algo) bytes.
- * For LBI_BF16 inputs `math` must still be a valid lbi_math and has no
- * effect.  All choices agree to float32 rounding (they accumulate in float32
- * in different orders); they are not bitwise equal to each other.
+ * chosen by `math` and the scan by `algo`; the workspace must hold
+ * lbi_scan_backward_workspace_bytes_ex(B, K, r, dt, algo) bytes (the same for
+ * every `math`).  For LBI_BF16 inputs the float32 choices
+ * (LBI_MATH_F32_MFMA, LBI_MATH_F32_SPLIT) act as LBI_MATH_DEFAULT, and
+ * LBI_MATH_BF16_SINGLE selects the single rounding of the composite; for
+ * LBI_F32 inputs LBI_MATH_BF16_SINGLE is LBI_ERR_DTYPE.  The float32 choices
+ * agree to float32 rounding (they accumulate in float32 in different
+ * orders); they are not bitwise equal to each other.
  */
 lbi_status lbi_scan_backward_ex(const void *A, const void *b, const void *lambda_K,
                                 float *lambda, int64_t B, int64_t K, int32_t r, lbi_dtype dt,
