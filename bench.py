@@ -456,6 +456,13 @@ def main(argv=None) -> int:
               "(chains are independent, so B shards across GPUs with no communication)",
               file=sys.stderr)
         return 2
+    if args.math == "bf16single" and args.op != "phase1":
+        from paper_2605_09204_amd import synth as _synth
+        wl0 = _synth.WORKLOADS.get(args.workload)
+        if wl0 is not None and wl0.dtype != "bf16":
+            print(f"--math bf16single needs bf16 storage; workload {args.workload} is "
+                  f"{wl0.dtype}", file=sys.stderr)
+            return 2
 
     import torch
     from paper_2605_09204_amd import binding, synth

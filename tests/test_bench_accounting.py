@@ -67,3 +67,8 @@ def test_mode_names():
 def test_more_than_one_gpu_is_refused(capsys):
     assert bench.main(["--gpus", "2"]) != 0
     assert "one GPU only" in capsys.readouterr().err
+
+
+def test_single_rounding_needs_bf16_storage(capsys):
+    assert bench.main(["--workload", "long_chain", "--math", "bf16single"]) == 2
+    assert "needs bf16 storage" in capsys.readouterr().err
