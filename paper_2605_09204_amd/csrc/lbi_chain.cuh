@@ -885,6 +885,9 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
                 // split arithmetic: the staging chunks, the loads and the
                 // apply go between the 6 (r = 16, 32) or 12 (r = 64) MFMA
                 // groups of the combine
+                // (the wave in its combine issues ahead of the other wave on
+                // its SIMD: measured 0.6-1.4% faster on 512 chains of 512)
+                __builtin_amdgcn_s_setprio(2);
                 stage_begin(j - 1, false);
                 combine<R, M, NCA, NRB, NRB, true>(Pn, P, sA[buf], li, g, [&](int step) {
                     if (step < CPT)
@@ -896,6 +899,7 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
                     else if (step == CPT + 2)
                         emit();
                 });
+                __builtin_amdgcn_s_setprio(0);
             } else {
                 if constexpr (HINT) {
                     combine_shape<R, M, NCA>(pow2_at_least(wq[2]), pow2_at_least(wq[1]), Pn, P,
