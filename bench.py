@@ -362,7 +362,24 @@ def bench_phase1(args) -> int:
 # CPU baseline: the oracle on a bounded sample of the same workload
 # ----------------------------------------------------------------------------
 
-def cpu_baseline(x, target_s: float = 10.0, nthreads: int = 0):
+def cpu_model() -> str:
+    """The host CPU's model name (from /proc/cpuinfo), or the platform's."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.lower().startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or platform.machine()
+
+
+def cpu_baseline(x, run_s: float = 5.0, nthreads: int = 0, runs: int = 3):
+    """The fp64 oracle recurrence on the host, timed as the median of ``runs``
+    runs of about ``run_s`` seconds each over a bounded sample of the same
+    chains (the first n chains, n sized by a calibration run; a batch too
+    small to last run_s is repeated within each run)."""
     import oracle
     import torch
 
@@ -373,25 +390,99 @@ def cpu_baseline(x, target_s: float = 10.0, nthreads: int = 0):
     t0 = time.perf_counter()
     oracle.recurrence(host.A, host.b, host.lamK, nthreads)
     t_cal = max(time.perf_counter() - t0, 1e-6)
-    n = int(min(wl.B, max(n_cal, n_cal * target_s / t_cal)))
+    n = int(min(wl.B, max(n_cal, n_cal * run_s / t_cal)))
     host = x.chains(torch.arange(n)).to("cpu")
     t0 = time.perf_counter()
     oracle.recurrence(host.A, host.b, host.lamK, nthreads)
-    t = time.perf_counter() - t0
-    reps = 1
-    while t < target_s and reps < 4096:  # whole batch is quick: repeat it
+    t_one = max(time.perf_counter() - t0, 1e-6)
+    reps = max(1, min(4096, int(round(run_s / t_one))))
+    times = []
+    for _ in range(runs):
         t0 = time.perf_counter()
-        oracle.recurrence(host.A, host.b, host.lamK, nthreads)
-        t += time.perf_counter() - t0
-        reps += 1
+        for _ in range(reps):
+            oracle.recurrence(host.A, host.b, host.lamK, nthreads)
+        times.append(time.perf_counter() - t0)
+    med = sorted(times)[len(times) // 2]
     return {
-        "value": reps * n * (wl.K - 1) / t,
+        "value": reps * n * (wl.K - 1) / med,
         "unit": "combines/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": f"{n} of {wl.B} chains x {reps} pass(es), all K={wl.K} slots, "
-                  f"fp64 recurrence over the same {wl.dtype} inputs ({t:.1f} s)",
+        "sample": f"{n} of {wl.B} chains x {reps} pass(es) per run, all K={wl.K} slots, "
+                  f"fp64 recurrence over the same {wl.dtype} inputs; median of {runs} runs "
+                  f"({', '.join(f'{t:.2f}' for t in times)} s)",
+        "cpu_model": cpu_model(),
+        "threads": threads,
+        "runs_s": times,
     }
+
+
+# ----------------------------------------------------------------------------
+# one adjoint-type measurement (the JSON line without the CPU baseline)
+# ----------------------------------------------------------------------------
+
+def time_launches(step, steps, warmup, torch, dev):
+    """Warm-up, then ``steps`` timed launches bracketed by HIP events on the
+    launch stream.  Returns (per-launch ms, first-start to last-end ms, wall
+    s, warm-up launches)."""
+    class _W:
+        pass
+    wa = _W()
+    wa.warmup = warmup
+    nwarm = warm_up(step, wa, torch)
+    stream = torch.cuda.current_stream(dev)
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    for i in range(steps):
+        starts[i].record(stream)
+        step(i)
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    per_launch_ms = [st.elapsed_time(en) for st, en in zip(starts, ends)]
+    return per_launch_ms, starts[0].elapsed_time(ends[-1]), t_wall, nwarm
+
+
+def chain_mapping(wl, op, layout, math_name, algo_name, need) -> str:
+    """The chain mapping the library uses (for adjoints, its AUTO rule unless
+    the two-level scan is taken: bf16 with r <= 32 and B <= 8192 one
+    wavefront per chain; fp32 split arithmetic at r = 64 with B <= 256
+    sixteen waves per chain; else one workgroup per chain)."""
+    auto_adj = algo_name == "auto" and op == "adjoints" and layout == "padded"
+    if need:
+        return "two-level scan (segments in parallel)"
+    if algo_name == "chain_wave" or (auto_adj and wl.dtype == "bf16" and wl.r <= 32
+                                     and wl.B <= 8192 and math_name != "bf16single"):
+        return "one wavefront per chain"
+    if algo_name == "chain_splitk" or (auto_adj and wl.dtype == "f32" and math_name == "split"
+                                       and wl.r == 64 and wl.B <= 256):
+        return "sixteen waves per chain (split contraction, staging waves)"
+    return "one workgroup per chain"
+
+
+def roofline(wl, math_name, b_alg, avg_launch_s, f_alg):
+    """(roofline dict without traffic, executed matrix-core flops, peak, ideal
+    matrix-core s, ideal HBM s) of one launch: the bound is whichever of HBM
+    and the matrix cores gives the larger ideal time."""
+    mode = mode_of(wl, math_name)
+    f_exec = mfma_flops_executed(wl, math_name)
+    mfma_peak = PEAK["mfma_f32_tflops"] if mode == "f32-mfma" else PEAK["mfma_bf16_tflops"]
+    t_mfma = f_exec / (mfma_peak * 1e12)
+    t_hbm = b_alg / (PEAK["hbm_gbs"] * 1e9)
+    tflops = f_alg / avg_launch_s / 1e12
+    gbs = b_alg / avg_launch_s / 1e9
+    if t_mfma >= t_hbm:
+        # matrix-core bound: algorithmic flops against the fp32 peak when the
+        # products run on the fp32 matrix cores, else executed bf16 flops
+        # against the bf16 peak
+        ach = tflops if mode == "f32-mfma" else f_exec / avg_launch_s / 1e12
+        roof = {"bound": "mfma", "achieved": ach, "peak": mfma_peak, "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": gbs, "peak": PEAK["hbm_gbs"], "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    return roof, f_exec, mfma_peak, t_mfma, t_hbm
 
 
 # ----------------------------------------------------------------------------
@@ -431,6 +522,9 @@ def main(argv=None) -> int:
     ap.add_argument("--K", type=int, default=0, help="override the workload's slot count")
     ap.add_argument("--r", type=int, default=0, help="override the workload's interface width")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-configs", action="store_true",
+                    help="time only the chosen workload (by default a headline run also "
+                         "times every other workload of the table, under extra.configs)")
     ap.add_argument("--per-launch", action="store_true",
                     help="print every timed launch's duration (µs) to stderr")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -484,7 +578,62 @@ def main(argv=None) -> int:
             return 2
         wl = wl.with_(B=args.B or wl.B, K=args.K or wl.K, r=args.r or wl.r,
                       name=f"{wl.name}_B{args.B or wl.B}_K{args.K or wl.K}_r{args.r or wl.r}")
+    if args.layout == "compact" and (args.op != "adjoints" or args.algo == "two_level" or any(
+            wk % 16 for wk in wl.interface_widths())):
+        print("--layout compact: adjoints, chain scan, widths multiples of 16", file=sys.stderr)
+        return 2
     dev = torch.device("cuda:0")
+    out, x = measure(wl, args.op, args.layout, args.math, args.algo, args.steps, args.warmup,
+                     args.chunk, torch, binding, synth, dev,
+                     copy_calibration=args.copy_calibration, per_launch=args.per_launch)
+    args.warmup = out["warmup"]
+    if not args.no_cpu_baseline and args.op != "norms":
+        print("[bench] timing the CPU oracle baseline", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(x)
+        # the same oracle on one core (a smaller sample)
+        one = cpu_baseline(x, run_s=1.5, nthreads=1)
+        out["extra"]["cpu_oracle_one_core"] = {"value": one["value"], "unit": one["unit"],
+                                               "sample": one["sample"]}
+    # the other workloads of the table, timed in the same run (one line, the
+    # headline's; each of the others as an entry of extra.configs)
+    headline = (args.op == "adjoints" and args.layout == "padded" and args.math == "split"
+                and args.algo == "auto" and not (args.B or args.K or args.r)
+                and not args.no_other_configs)
+    if headline:
+        del x
+        torch.cuda.empty_cache()
+        others = {}
+        for name in synth.WORKLOAD_ORDER:
+            if name == wl.name:
+                continue
+            w2 = synth.WORKLOADS[name]
+            steps2 = 200 if w2.B * w2.K <= 4096 else 30
+            o2, x2 = measure(w2, "adjoints", "padded", "split", "auto", steps2, None,
+                             args.chunk, torch, binding, synth, dev)
+            rec = {"ms_per_step": o2["ms_per_step"],
+                   "avg_launch_ms": o2["extra"]["avg_launch_ms"],
+                   "value": o2["value"], "unit": o2["unit"], "steps": steps2,
+                   "warmup": o2["warmup"], "dtype": o2["dtype"], "config": o2["config"],
+                   "roofline": o2["roofline"], "alg_tflops": o2["extra"]["alg_tflops"],
+                   "alg_hbm_gbs": o2["extra"]["alg_hbm_gbs"],
+                   "work_inflation_vs_sequential":
+                       o2["extra"]["work_inflation_vs_sequential"]}
+            if not args.no_cpu_baseline:
+                print(f"[bench] timing the CPU oracle baseline on {name}", file=sys.stderr,
+                      flush=True)
+                rec["cpu_baseline"] = cpu_baseline(x2, run_s=1.5)
+            others[name] = rec
+            del x2
+            torch.cuda.empty_cache()
+        out["extra"]["configs"] = others
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def measure(wl, op, layout, math_name, algo_name, steps, warmup, chunk, torch, binding, synth,
+            dev, copy_calibration=0, per_launch=False):
+    """Times ``steps`` launches of one operation on workload ``wl``; returns
+    (the JSON record without the CPU baseline, the inputs)."""
     print(f"[bench] generating {wl.name}: B={wl.B} K={wl.K} r={wl.r} {wl.dtype}",
           file=sys.stderr, flush=True)
     t0 = time.time()
@@ -501,43 +650,38 @@ def main(argv=None) -> int:
     hint = wl.widths
 
     math = {"split": binding.LBI_MATH_F32_SPLIT, "mfma": binding.LBI_MATH_F32_MFMA,
-            "bf16single": binding.LBI_MATH_BF16_SINGLE}[args.math]
+            "bf16single": binding.LBI_MATH_BF16_SINGLE}[math_name]
     algo = {"auto": binding.LBI_ALGO_AUTO, "chain": binding.LBI_ALGO_CHAIN,
             "two_level": binding.LBI_ALGO_TWO_LEVEL,
             "chain_wave": binding.LBI_ALGO_CHAIN_WAVE,
-            "chain_splitk": binding.LBI_ALGO_CHAIN_SPLITK}[args.algo]
+            "chain_splitk": binding.LBI_ALGO_CHAIN_SPLITK}[algo_name]
     need = binding.lbi_scan_backward_workspace_bytes_ex(wl.B, wl.K, wl.r,
                                                          0 if wl.dtype == "f32" else 1, algo)
     ws = torch.empty((need,), dtype=torch.uint8, device=dev) if need else None
 
-    if args.op == "streaming":
+    if op == "streaming":
         progress = torch.zeros(wl.B, dtype=torch.int32, device=dev)
 
         def step(i):
             c = copies[i % ncopy]
             progress.zero_()
-            binding.lbi_scan_backward_streaming(c.A, c.b, c.lamK, progress, args.chunk, hint,
+            binding.lbi_scan_backward_streaming(c.A, c.b, c.lamK, progress, chunk, hint,
                                                 math, lam=lam)
-    elif args.op == "norms":
+    elif op == "norms":
         spec = torch.empty((wl.B, wl.K), dtype=torch.float32, device=dev)
         fro = torch.empty((wl.B, wl.K), dtype=torch.float32, device=dev)
 
         def step(i):
             c = copies[i % ncopy]
             binding.lbi_matrix_norms(c.A, spec=spec, fro=fro)
-    elif args.op == "suffix_products":
+    elif op == "suffix_products":
         Pout = torch.empty((wl.B, wl.K, wl.r, wl.r), dtype=torch.float32, device=dev)
         cout = torch.empty((wl.B, wl.K, wl.r), dtype=torch.float32, device=dev)
 
         def step(i):
             c = copies[i % ncopy]
             binding.lbi_scan_suffix_products(c.A, c.b, hint, math, P=Pout, c=cout)
-    elif args.layout == "compact":
-        if args.op != "adjoints" or args.algo == "two_level" or any(
-                wk % 16 for wk in wl.interface_widths()):
-            print("--layout compact: adjoints, chain scan, widths multiples of 16",
-                  file=sys.stderr)
-            return 2
+    elif layout == "compact":
         packed = [synth.pack_ragged(c) for c in copies]
         lam_c = torch.empty((wl.B, sum(wl.interface_widths()[:wl.K])), dtype=torch.float32,
                             device=dev)
@@ -551,11 +695,11 @@ def main(argv=None) -> int:
             binding.lbi_scan_backward_ex(c.A, c.b, c.lamK, hint, math, algo, lam=lam,
                                          workspace=ws)
 
-    if args.copy_calibration > 0:
+    if copy_calibration > 0:
         # A plain streaming kernel of known size (torch's elementwise negation:
         # reads and writes MiB << 20 bytes each) against which the PMC byte
         # counters of the scan kernel are scaled.
-        n = (args.copy_calibration << 20) // 4
+        n = (copy_calibration << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
         for _ in range(3):
@@ -563,76 +707,38 @@ def main(argv=None) -> int:
         torch.cuda.synchronize()
         del src, dst
 
-    warm_up(step, args, torch)
-
-    stream = torch.cuda.current_stream(dev)
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    for i in range(args.steps):
-        starts[i].record(stream)
-        step(i)
-        ends[i].record(stream)
-    torch.cuda.synchronize()
-    t_wall = time.perf_counter() - t_wall
-    per_launch_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
-    if args.per_launch:
+    per_launch_ms, total_ms, t_wall, nwarm = time_launches(step, steps, warmup, torch, dev)
+    if per_launch:
         print("[bench] per-launch µs: " + " ".join(f"{t * 1e3:.1f}" for t in per_launch_ms),
               file=sys.stderr, flush=True)
-    total_ms = starts[0].elapsed_time(ends[-1])
     avg_launch_s = sum(per_launch_ms) / len(per_launch_ms) / 1e3
-    ms_per_step = total_ms / args.steps
+    ms_per_step = total_ms / steps
 
-    if args.op == "norms":
-        print(json.dumps(norms_record(wl, args, total_ms, avg_launch_s, per_launch_ms, ncopy)),
-              flush=True)
-        return 0
-    value = combines(wl) * args.steps / (total_ms / 1e3)
-    f_alg = flops_combines(wl) if args.op == "suffix_products" else flops_alg(wl)
-    # the chain mapping the library uses (for adjoints, its AUTO rule unless
-    # the two-level scan is taken: bf16 with r <= 32 and B <= 8192 one
-    # wavefront per chain; fp32 split arithmetic at r = 64 with B <= 256
-    # sixteen waves per chain; else one workgroup per chain)
-    auto_adj = args.algo == "auto" and args.op == "adjoints" and args.layout == "padded"
-    if need:
-        mapping = "two-level scan (segments in parallel)"
-    elif args.algo == "chain_wave" or (auto_adj and wl.dtype == "bf16" and wl.r <= 32
-                                       and wl.B <= 8192 and args.math != "bf16single"):
-        mapping = "one wavefront per chain"
-    elif args.algo == "chain_splitk" or (auto_adj and wl.dtype == "f32" and args.math == "split"
-                                         and wl.r == 64 and wl.B <= 256):
-        mapping = "sixteen waves per chain (split contraction, staging waves)"
-    else:
-        mapping = "one workgroup per chain"
-    b_alg = (bytes_export(wl) if args.op == "suffix_products"
-             else bytes_alg(wl, compact_out=args.layout == "compact"))
+    if op == "norms":
+        class _A:
+            pass
+        na = _A()
+        na.steps, na.warmup = steps, nwarm
+        return norms_record(wl, na, total_ms, avg_launch_s, per_launch_ms, ncopy), x
+    value = combines(wl) * steps / (total_ms / 1e3)
+    f_alg = flops_combines(wl) if op == "suffix_products" else flops_alg(wl)
+    mapping = chain_mapping(wl, op, layout, math_name, algo_name, need)
+    b_alg = (bytes_export(wl) if op == "suffix_products"
+             else bytes_alg(wl, compact_out=layout == "compact"))
     tflops = f_alg / avg_launch_s / 1e12
     gbs = b_alg / avg_launch_s / 1e9
-    mode = mode_of(wl, args.math)
-    f_exec = mfma_flops_executed(wl, args.math)
-    mfma_peak = PEAK["mfma_f32_tflops"] if mode == "f32-mfma" else PEAK["mfma_bf16_tflops"]
-    t_mfma = f_exec / (mfma_peak * 1e12)
-    t_hbm = b_alg / (PEAK["hbm_gbs"] * 1e9)
-    if t_mfma >= t_hbm:
-        # matrix-core bound: algorithmic flops against the fp32 peak when the
-        # products run on the fp32 matrix cores, else executed bf16 flops
-        # against the bf16 peak
-        ach = tflops if mode == "f32-mfma" else f_exec / avg_launch_s / 1e12
-        roof = {"bound": "mfma", "achieved": ach, "peak": mfma_peak, "unit": "TFLOP/s"}
-    else:
-        roof = {"bound": "hbm", "achieved": gbs, "peak": PEAK["hbm_gbs"], "unit": "GB/s"}
-    roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = (load_traffic(wl.name) if args.op == "adjoints" and
-                       (args.math == "split" or (wl.dtype == "bf16" and
-                                                 args.math != "bf16single")) else None)
+    mode = mode_of(wl, math_name)
+    roof, f_exec, mfma_peak, t_mfma, t_hbm = roofline(wl, math_name, b_alg, avg_launch_s, f_alg)
+    roof["traffic"] = (load_traffic(wl.name) if op == "adjoints" and layout == "padded" and
+                       (math_name == "split" or (wl.dtype == "bf16" and
+                                                 math_name != "bf16single")) else None)
     out = {
         "metric": METRIC,
         "value": value,
         "unit": "combines/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "steps": steps,
+        "warmup": nwarm,
         "ms_per_step": ms_per_step,
         "higher_is_better": True,
         "scaling": "weak",
@@ -642,8 +748,8 @@ def main(argv=None) -> int:
                 "Jacobians; no dataset or checkpoint)",
         "config": {"workload": wl.name, "B": wl.B, "K": wl.K, "r": wl.r,
                    "storage": wl.dtype, "affine": wl.affine, "arithmetic": mode,
-                   "algorithm": args.algo, "workspace_bytes": need, "op": args.op,
-                   "layout": args.layout,
+                   "algorithm": algo_name, "workspace_bytes": need, "op": op,
+                   "layout": layout,
                    "widths": "cyclic 32/64/128" if wl.widths else "uniform",
                    "parallelism": "1 GPU, " + mapping},
         "roofline": roof,
@@ -665,16 +771,7 @@ def main(argv=None) -> int:
             "wall_s_timed_region": t_wall,
         },
     }
-    if not args.no_cpu_baseline:
-        print("[bench] timing the CPU oracle baseline", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(x)
-        # the same oracle on one core (a smaller sample)
-        one = cpu_baseline(x, target_s=4.0, nthreads=1)
-        out["extra"]["cpu_oracle_one_core"] = {"value": one["value"], "unit": one["unit"],
-                                               "sample": one["sample"]}
-    print(json.dumps(out), flush=True)
-    return 0
-
+    return out, x
 
 if __name__ == "__main__":
     sys.exit(main())

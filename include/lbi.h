@@ -49,11 +49,17 @@ extern "C" {
 /* HIP stream handle (the same type as hipStream_t). */
 typedef struct ihipStream_t *lbi_stream_t;
 
-#define LBI_ABI_VERSION 9
+#define LBI_ABI_VERSION 10
 
 /* Largest K for which a widths hint is used (longer chains run unhinted,
  * which gives identical results). */
 #define LBI_MAX_HINT_K 2047
+
+/* Longest chain LBI_MATH_BF16_SINGLE accepts (longer chains: LBI_ERR_SHAPE).
+ * Its relative error grows like 1.2e-3 sqrt(K) (about 9.5e-3 at K = 64,
+ * 1.4e-2 at K = 128 on Haar-orthogonal x diag(U[0.9, 1.1]) chains at r = 64),
+ * so up to this length it stays within half the bf16 tolerance of 2e-2. */
+#define LBI_BF16_SINGLE_MAX_K 64
 
 typedef enum {
     LBI_F32 = 0,  /* A, b, lambda_K stored as float32; float32 arithmetic   */
@@ -76,15 +82,18 @@ typedef enum {
                              * six partial products down to 2^-16 of the leading
                              * one), fp32 accumulation; r = 128 falls back to
                              * LBI_MATH_F32_MFMA                                 */
-    LBI_MATH_BF16_SINGLE = 3 /* bf16 inputs only (else LBI_ERR_DTYPE): the
-                             * running composite is fed back rounded once to
-                             * bf16 (one product instead of two).  Faster; the
-                             * relative error grows with the chain, about
-                             * 2^-9 per slot (measured about 7e-3 at K = 32 on
+    LBI_MATH_BF16_SINGLE = 3 /* bf16 inputs only (else LBI_ERR_DTYPE) and
+                             * K <= LBI_BF16_SINGLE_MAX_K (else
+                             * LBI_ERR_SHAPE): the running composite is fed
+                             * back rounded once to bf16 (one product instead
+                             * of two).  Faster; each slot adds a relative
+                             * rounding of up to 2^-9, and these add up like a
+                             * random walk (measured about 7e-3 at K = 32 on
                              * the bf16 token-batch recipe, against 2e-6 for
-                             * the default).  Not taken by the wavefront-per-
-                             * chain scan (LBI_ALGO_CHAIN_WAVE: LBI_ERR_DTYPE;
-                             * AUTO then uses the workgroup kernel)            */
+                             * the default), hence the length limit.  Not
+                             * taken by the wavefront-per-chain scan
+                             * (LBI_ALGO_CHAIN_WAVE: LBI_ERR_DTYPE; AUTO then
+                             * uses the workgroup kernel)                      */
 } lbi_math;
 
 /* How the slots of a chain are scanned (lbi_scan_backward_ex). */
@@ -146,7 +155,9 @@ typedef enum {
 typedef enum {
     LBI_OK = 0,
     LBI_ERR_NULL = 1,          /* a required pointer is NULL                */
-    LBI_ERR_SHAPE = 2,         /* B < 0, K < 1, size overflow, bad widths   */
+    LBI_ERR_SHAPE = 2,         /* B < 0, K < 1, size overflow, bad widths,  *
+                                * K past LBI_BF16_SINGLE_MAX_K for         *
+                                * LBI_MATH_BF16_SINGLE                     */
     LBI_ERR_DTYPE = 3,         /* dtype not an lbi_dtype, math not an       *
                                 * lbi_math, or algo not an lbi_algo         */
     LBI_ERR_UNSUPPORTED_R = 4, /* r not in {16, 32, 64, 128}                */

@@ -145,6 +145,10 @@ lbi_status check_common(lbi_dtype dt, lbi_math math, int32_t r, int64_t B, int64
         return LBI_ERR_UNSUPPORTED_R;
     if (B < 0 || K < 1)
         return LBI_ERR_SHAPE;
+    // the single rounding's error grows like sqrt(K): only chains short
+    // enough to stay within half the bf16 tolerance
+    if (math == LBI_MATH_BF16_SINGLE && K > LBI_BF16_SINGLE_MAX_K)
+        return LBI_ERR_SHAPE;
     // sizes must fit comfortably in 64 bits and the launch grid
     const int64_t kMax = (int64_t)1 << 40;
     if (B > (int64_t)INT32_MAX || K > kMax / ((int64_t)r * r) || B > kMax / (K * (int64_t)r * r))

@@ -56,7 +56,7 @@ def test_header_compiles_as_c():
 
 
 def test_version_and_status_strings():
-    assert binding.lbi_abi_version() == 9
+    assert binding.lbi_abi_version() == 10
     assert binding.lbi_status_string(0) == "LBI_OK"
     for code in range(1, 9):
         assert binding.lbi_status_string(code).startswith("LBI_ERR_")
@@ -162,6 +162,20 @@ def test_bf16_single_argument_errors():
     f = binding.load().lbi_scan_suffix_products
     assert f(PA, PB, POUT, PL, 2, 3, 64, 0, None, None, 3) == 3
     assert f(None, PB, POUT, PL, 2, 3, 64, 1, None, None, 3) == 1
+    # chains longer than LBI_BF16_SINGLE_MAX_K (64): LBI_ERR_SHAPE, in every
+    # entry point that takes the arithmetic
+    assert call(dt=1, K=65, math=3) == 2
+    assert call(dt=1, K=65, math=3, algo=1) == 2
+    assert call(dt=1, K=65, math=3, algo=2) == 2
+    assert call(dt=1, K=64, math=3, A=None) == 1
+    assert call(dt=1, K=65, math=0, A=None) == 1
+    assert f(PA, PB, POUT, PL, 2, 65, 64, 1, None, None, 3) == 2
+    g = binding.load().lbi_scan_backward_streaming
+    assert g(PA, PB, PL, POUT, 2, 65, 64, 1, None, None, 3, 0x60000000, 4) == 2
+    h = binding.load().lbi_scan_backward_ragged
+    w65 = (ctypes.c_int32 * 66)(*([64] * 66))
+    assert h(PA, PB, PL, POUT, 2, 65, w65, 1, None, 3) == 2
+    assert h(None, PB, PL, POUT, 2, 64, w65, 1, None, 3) == 1
 
 
 def test_suffix_products_argument_errors():
