@@ -282,10 +282,19 @@ lbi_status lbi_scan_suffix_products(const void *A, const void *b, float *P, floa
  *                   that reads it with acquire ordering), lambda_{K-n} ..
  *                   lambda_{K-1} of chain beta are stored and visible.  It
  *                   ends at K.
+ *                   The count is raised with a system-scope atomic, so it
+ *                   reaches memory as it is made (not only at the kernel's
+ *                   end).  K must be below 2^32.
  *   chunk >= 1      slots per publication; each costs the chain's storing
  *                   wave a wait for its outstanding memory operations and an
  *                   L2 write-back, so larger chunks cost less (measured in
  *                   the design notes).
+ *   publish_clock   [B][ceil(K / chunk)] uint64 in DEVICE memory, or NULL:
+ *                   entry p of chain beta receives the GPU's constant-rate
+ *                   real-time counter (s_memrealtime, 100 MHz on MI355X) when
+ *                   the count (p + 1) chunk (K for the last entry) is
+ *                   published; readable after the call completes.  8-byte
+ *                   aligned, not overlapping any other argument.
  *
  * Results equal lbi_scan_backward_ex(..., LBI_ALGO_CHAIN) bit for bit.
  */
@@ -293,7 +302,31 @@ lbi_status lbi_scan_backward_streaming(const void *A, const void *b, const void 
                                        float *lambda, int64_t B, int64_t K, int32_t r,
                                        lbi_dtype dt, lbi_stream_t stream,
                                        const int32_t *widths_host, lbi_math math,
-                                       uint32_t *progress, int32_t chunk);
+                                       uint32_t *progress, int32_t chunk,
+                                       uint64_t *publish_clock);
+
+/*
+ * The consumer side of lbi_scan_backward_streaming: enqueues on `stream` a
+ * wait until progress[beta] >= target for every beta < B, so that work
+ * enqueued after it on that stream (the region-local backward of the latest
+ * regions, Algorithm "Bounded-Interface Backpropagation", Phase 3) starts as
+ * soon as lambda_{K-target} .. lambda_{K-1} of every chain are final, while
+ * the scan still runs on another stream.  One wavefront polls the counters
+ * (system-scope acquire loads, a short sleep between polls) and gives up
+ * after max_polls polls, so the wait always ends; a poll with its sleep takes
+ * on the order of a microsecond.
+ *
+ *   progress       [B] uint32, DEVICE memory (the streaming scan's counters).
+ *   B >= 0, target any value, max_polls >= 1.
+ *   released       [1] uint32 DEVICE memory, or NULL: 1 when every counter
+ *                  reached target, 0 when the wait gave up.
+ *   release_clock  [1] uint64 DEVICE memory, or NULL: the real-time counter
+ *                  (the clock of publish_clock) when the wait ended.
+ * Outputs must not overlap progress or each other.
+ */
+lbi_status lbi_wait_progress(const uint32_t *progress, int64_t B, uint32_t target,
+                             int64_t max_polls, uint32_t *released, uint64_t *release_clock,
+                             lbi_stream_t stream);
 
 /*
  * lbi_scan_backward for interfaces of different widths, stored compactly with

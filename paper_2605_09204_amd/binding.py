@@ -28,6 +28,7 @@ LBI_ALGO_CHAIN = 1
 LBI_ALGO_TWO_LEVEL = 2
 LBI_ALGO_CHAIN_WAVE = 3
 LBI_ALGO_CHAIN_SPLITK = 4
+LBI_BF16_SINGLE_MAX_K = 64
 
 _DTYPES = {torch.float32: LBI_F32, torch.bfloat16: LBI_BF16}
 
@@ -98,8 +99,10 @@ def load() -> ctypes.CDLL:
     lib.lbi_scan_suffix_products.restype = ctypes.c_int
     lib.lbi_scan_backward_streaming.argtypes = [vp, vp, vp, vp, i64, i64, i32, ctypes.c_int, vp,
                                                 ctypes.POINTER(ctypes.c_int32), ctypes.c_int,
-                                                vp, i32]
+                                                vp, i32, vp]
     lib.lbi_scan_backward_streaming.restype = ctypes.c_int
+    lib.lbi_wait_progress.argtypes = [vp, i64, ctypes.c_uint32, i64, vp, vp, vp]
+    lib.lbi_wait_progress.restype = ctypes.c_int
     lib.lbi_scan_backward_ragged.argtypes = [vp, vp, vp, vp, i64, i64,
                                              ctypes.POINTER(ctypes.c_int32), ctypes.c_int, vp,
                                              ctypes.c_int]
@@ -258,9 +261,12 @@ def lbi_scan_backward_streaming(A: torch.Tensor, b: Optional[torch.Tensor],
                                 lambda_K: torch.Tensor, progress: torch.Tensor, chunk: int,
                                 widths: Optional[Sequence[int]] = None,
                                 math: int = LBI_MATH_DEFAULT, lam: Optional[torch.Tensor] = None,
-                                stream=None) -> torch.Tensor:
+                                stream=None,
+                                publish_clock: Optional[torch.Tensor] = None) -> torch.Tensor:
     """The chain scan, raising progress[beta] (int32/uint32 [B] GPU tensor, zeroed by
-    the caller) to the count of final adjoints every ``chunk`` slots."""
+    the caller) to the count of final adjoints every ``chunk`` slots; with
+    ``publish_clock`` (int64 [B, ceil(K / chunk)] GPU tensor) the real-time
+    counter of each publication is recorded there."""
     lam, args = _marshal(A, b, lambda_K, lam, None, stream, LBI_ALGO_CHAIN)
     B = int(A.shape[0])
     if (progress.dim() != 1 or progress.shape[0] != B or progress.dtype not in
@@ -269,10 +275,41 @@ def lbi_scan_backward_streaming(A: torch.Tensor, b: Optional[torch.Tensor],
         raise ValueError(f"progress must be a contiguous 32-bit [{B}] tensor on A's device")
     warr, wptr = _widths_arg(widths, int(A.shape[1]))
     Aptr, bptr, lkptr, lamptr, B_, K, r, dt, _ws, _wsb, sptr = args
+    cptr = None
+    if publish_clock is not None:
+        npub = -(-int(A.shape[1]) // int(chunk)) if int(chunk) > 0 else 0
+        if (publish_clock.dtype not in (torch.int64, torch.uint64)
+                or tuple(publish_clock.shape) != (B, npub)
+                or not publish_clock.is_contiguous() or publish_clock.device != A.device):
+            raise ValueError(f"publish_clock must be a contiguous 64-bit [{B}, {npub}] tensor "
+                             "on A's device")
+        cptr = publish_clock.data_ptr()
     _check(load().lbi_scan_backward_streaming(Aptr, bptr, lkptr, lamptr, B_, K, r, dt, sptr,
                                               wptr, int(math), progress.data_ptr(),
-                                              int(chunk)))
+                                              int(chunk), cptr))
     return lam
+
+
+def lbi_wait_progress(progress: torch.Tensor, target: int, max_polls: int,
+                      released: Optional[torch.Tensor] = None,
+                      release_clock: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Enqueue on ``stream`` (default: the current stream) a wait until every
+    progress[beta] >= target, giving up after ``max_polls`` polls.  ``released``
+    (32-bit [1] GPU tensor) receives 1 / 0 (satisfied / gave up),
+    ``release_clock`` (64-bit [1] GPU tensor) the real-time counter at the end."""
+    if (progress.dim() != 1 or progress.dtype not in (torch.int32, torch.uint32)
+            or not progress.is_contiguous() or not progress.is_cuda):
+        raise ValueError("progress must be a contiguous 32-bit [B] GPU tensor")
+    for t, dts, name in ((released, (torch.int32, torch.uint32), "released"),
+                         (release_clock, (torch.int64, torch.uint64), "release_clock")):
+        if t is not None and (t.dtype not in dts or t.numel() < 1 or not t.is_cuda
+                              or t.device != progress.device):
+            raise ValueError(f"{name} must be a GPU tensor of {dts} on progress's device")
+    _check(load().lbi_wait_progress(
+        progress.data_ptr(), int(progress.shape[0]), int(target) & 0xFFFFFFFF, int(max_polls),
+        None if released is None else released.data_ptr(),
+        None if release_clock is None else release_clock.data_ptr(),
+        _stream_ptr(stream, progress.device)))
 
 
 def lbi_matrix_norms(M: torch.Tensor, want_spec: bool = True, want_fro: bool = True,

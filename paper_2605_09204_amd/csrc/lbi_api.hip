@@ -218,6 +218,7 @@ lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam,
     if (overlaps(lam, nout, A, nA) || overlaps(lam, nout, b, nb) || overlaps(lam, nout, lamK, nl))
         return LBI_ERR_ALIAS;
     const lbi_algo use = resolve_algo(algo, B, K, r, dt, math);
+    const TwoLevelPlan p = two_level_plan(B, K, r);
     const size_t need = lbi_scan_backward_workspace_bytes_ex(B, K, r, dt, use);
     if (need > 0 && (!ws || ws_bytes < need))
         return LBI_ERR_WORKSPACE;
@@ -255,7 +256,6 @@ lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam,
     // two-level scan: each segment folded (every composite kept, or its
     // aggregate only); the carries right to left; then every lambda_j at once
     // from the composites, or each segment scanned again from its carry
-    const TwoLevelPlan p = two_level_plan(B, K, r);
     char *w = (char *)ws;
     float *Pc = (float *)(w + p.offP);
     float *cc = b ? (float *)(w + p.offc) : nullptr;
@@ -586,28 +586,33 @@ lbi_status lbi_scan_backward_streaming(const void *A, const void *b, const void 
                                        float *lambda, int64_t B, int64_t K, int32_t r,
                                        lbi_dtype dt, lbi_stream_t stream,
                                        const int32_t *widths_host, lbi_math math,
-                                       uint32_t *progress, int32_t chunk)
+                                       uint32_t *progress, int32_t chunk,
+                                       uint64_t *publish_clock)
 {
     lbi_status st = check_common(dt, math, r, B, K);
     if (st != LBI_OK)
         return st;
-    if (chunk < 1)
+    if (chunk < 1 || K > (int64_t)UINT32_MAX)  // the counts are 32-bit
         return LBI_ERR_SHAPE;
     if (B == 0)
         return LBI_OK;
     if (!A || !lambda_K || !lambda || !progress)
         return LBI_ERR_NULL;
     if (misaligned(A) || misaligned(b) || misaligned(lambda_K) || misaligned(lambda) ||
-        ((uintptr_t)progress & 3u))
+        ((uintptr_t)progress & 3u) || ((uintptr_t)publish_clock & 7u))
         return LBI_ERR_ALIGN;
     const size_t esz = dt == LBI_F32 ? 4 : 2;
     const size_t nA = (size_t)B * K * r * r * esz, nb = b ? (size_t)B * K * r * esz : 0;
     const size_t nl = (size_t)B * r * esz, nout = (size_t)B * K * r * sizeof(float);
     const size_t np = (size_t)B * sizeof(uint32_t);
+    const int64_t npub = (K + chunk - 1) / chunk;
+    const size_t nc = publish_clock ? (size_t)B * npub * sizeof(uint64_t) : 0;
     if (overlaps(lambda, nout, A, nA) || overlaps(lambda, nout, b, nb) ||
         overlaps(lambda, nout, lambda_K, nl) || overlaps(progress, np, A, nA) ||
         overlaps(progress, np, b, nb) || overlaps(progress, np, lambda_K, nl) ||
-        overlaps(progress, np, lambda, nout))
+        overlaps(progress, np, lambda, nout) || overlaps(publish_clock, nc, A, nA) ||
+        overlaps(publish_clock, nc, b, nb) || overlaps(publish_clock, nc, lambda_K, nl) ||
+        overlaps(publish_clock, nc, lambda, nout) || overlaps(publish_clock, nc, progress, np))
         return LBI_ERR_ALIAS;
     ChainLaunch c;
     memset(&c, 0, sizeof c);
@@ -620,6 +625,8 @@ lbi_status lbi_scan_backward_streaming(const void *A, const void *b, const void 
     c.args.S = 1;
     c.args.progress = progress;
     c.args.pchunk = chunk;
+    c.args.npub = npub;
+    c.args.pub_clock = publish_clock;
     c.B = B;
     c.r = r;
     c.aff = b != nullptr;
@@ -628,6 +635,27 @@ lbi_status lbi_scan_backward_streaming(const void *A, const void *b, const void 
     if (!encode_widths(widths_host, K, r, c))
         return LBI_ERR_SHAPE;
     return launch_chain_mode(c, dt, math) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
+}
+
+lbi_status lbi_wait_progress(const uint32_t *progress, int64_t B, uint32_t target,
+                             int64_t max_polls, uint32_t *released, uint64_t *release_clock,
+                             lbi_stream_t stream)
+{
+    if (B < 0 || max_polls < 1)
+        return LBI_ERR_SHAPE;
+    if (B > 0 && !progress)
+        return LBI_ERR_NULL;
+    if (((uintptr_t)progress & 3u) || ((uintptr_t)released & 3u) ||
+        ((uintptr_t)release_clock & 7u))
+        return LBI_ERR_ALIGN;
+    const size_t np = (size_t)B * sizeof(uint32_t);
+    if (overlaps(released, 4, progress, np) || overlaps(release_clock, 8, progress, np) ||
+        overlaps(released, 4, release_clock, 8))
+        return LBI_ERR_ALIAS;
+    return launch_wait_progress(progress, B, target, max_polls, released, release_clock,
+                                (hipStream_t)stream) == hipSuccess
+               ? LBI_OK
+               : LBI_ERR_HIP;
 }
 
 const char *lbi_status_string(lbi_status s)

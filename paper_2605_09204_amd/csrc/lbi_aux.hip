@@ -190,7 +190,49 @@ hipError_t apply_r(const float *Pc, const float *cc, const float *carry, float *
 }
 
 
+// The consumer side of the streaming scan: one wave waits until the progress
+// counter of every chain has reached target.  It polls with system-scope
+// acquire loads (the counters are raised with system-scope atomics, so both
+// meet in memory, past every XCD's L2), with a short sleep between polls, for
+// at most max_polls polls, so that the wait always ends.  The loop's exit is
+// uniform across the wave (a wave-wide vote), and lane 0 records the outcome.
+__global__ __launch_bounds__(64) void wait_progress_kernel(const uint32_t *progress, int64_t B,
+                                                           uint32_t target, int64_t max_polls,
+                                                           uint32_t *released,
+                                                           uint64_t *release_clock)
+{
+    const int lane = (int)threadIdx.x;
+    int64_t polls = 0;
+    bool ok = false;
+    for (;;) {
+        bool mine = true;
+        for (int64_t i = lane; i < B; i += 64)
+            mine = mine && __hip_atomic_load(&progress[i], __ATOMIC_ACQUIRE,
+                                             __HIP_MEMORY_SCOPE_SYSTEM) >= target;
+        ok = __all(mine);
+        if (ok || ++polls >= max_polls)
+            break;
+        __builtin_amdgcn_s_sleep(8);
+    }
+    const uint64_t t = __builtin_amdgcn_s_memrealtime();
+    if (lane == 0) {
+        if (released)
+            released[0] = ok ? 1u : 0u;
+        if (release_clock)
+            release_clock[0] = t;
+    }
+}
+
 }  // namespace
+
+hipError_t launch_wait_progress(const uint32_t *progress, int64_t B, uint32_t target,
+                                int64_t max_polls, uint32_t *released, uint64_t *release_clock,
+                                hipStream_t stream)
+{
+    hipLaunchKernelGGL(wait_progress_kernel, dim3(1), dim3(64), 0, stream, progress, B, target,
+                       max_polls, released, release_clock);
+    return hipGetLastError();
+}
 
 hipError_t launch_carry(const float *Pa, const float *ca, const void *lamK, bool lamK_bf16,
                         float *carry, int64_t B, int32_t S, int64_t cstride, int64_t dstride,

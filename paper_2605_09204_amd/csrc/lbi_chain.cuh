@@ -705,10 +705,20 @@ __global__ __launch_bounds__(64 * waves_for(R)) void scan_chain_kernel(const Sca
     // Called after a barrier that follows finalize(x): the storing wave group
     // fenced its stores of slots x .. K-1 before it, so the count K - x can be
     // published.
+    // The count is raised with a system-scope atomic, so that it lands in
+    // memory rather than in this XCD's L2: agents outside the XCD (another
+    // XCD's waves, the command processor) poll it there.  With pub_clock the
+    // same lane then records the real-time counter of the publication.
     auto publish_before = [&](int64_t x) {
         if constexpr (OUT == kOutLambda) {
-            if (args.progress && pub_now && tid == 0)
-                atomicMax(&args.progress[beta], (uint32_t)(K - x));
+            if (args.progress && pub_now && tid == 0) {
+                const uint32_t n = (uint32_t)(K - x);
+                __hip_atomic_fetch_max(&args.progress[beta], n, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_SYSTEM);
+                if (args.pub_clock)
+                    args.pub_clock[beta * args.npub + (n + args.pchunk - 1) / args.pchunk - 1] =
+                        __builtin_amdgcn_s_memrealtime();
+            }
             pub_now = false;
         }
     };

@@ -46,6 +46,9 @@ struct ScanArgs {
     uint32_t *progress;  // [B] or NULL (kOutLambda, whole chains): raised to the
                          // number of final adjoints after every pchunk slots
     int32_t pchunk;
+    int64_t npub;        // publications per chain, ceil(K / pchunk)
+    uint64_t *pub_clock;  // [B][npub] or NULL: the real-time counter at each
+                          // publication (entry ceil(n / pchunk) - 1 for count n)
     // Compact (ragged) storage, hinted whole-chain kOutLambda launches only:
     // slot j of a chain holds A_j as r_j x r_{j+1} row-major, b_j and lambda_j
     // as r_j values, back to back; lambda_K as r_K values per chain.  totalA
@@ -84,6 +87,14 @@ hipError_t launch_chain_wave_bf16(const ChainLaunch &c);
 // or a widths hint).
 bool chain_ksplit_supported(const ChainLaunch &c);
 hipError_t launch_chain_ksplit_f32x(const ChainLaunch &c);
+
+// One wave polls progress[0..B-1] (acquire, device scope) until every entry
+// is at least target or max_polls polls have passed; then writes released[0]
+// (1: satisfied, 0: gave up) and release_clock[0] (the real-time counter),
+// either may be NULL.
+hipError_t launch_wait_progress(const uint32_t *progress, int64_t B, uint32_t target,
+                                int64_t max_polls, uint32_t *released, uint64_t *release_clock,
+                                hipStream_t stream);
 
 // Segment carries of the two-level scan: carry[beta][d] is lambda at the end
 // of segment d (lambda_K for the last), obtained by applying the segment

@@ -34,7 +34,7 @@ def test_header_declares_entry_points():
                             "lbi_scan_suffix_products", "lbi_scan_backward_streaming",
                             "lbi_matrix_norms", "lbi_scan_backward_ragged",
                             "lbi_region_jacobians_workspace_bytes", "lbi_region_jacobians",
-                            "lbi_status_string", "lbi_abi_version"])
+                            "lbi_wait_progress", "lbi_status_string", "lbi_abi_version"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -171,7 +171,7 @@ def test_bf16_single_argument_errors():
     assert call(dt=1, K=65, math=0, A=None) == 1
     assert f(PA, PB, POUT, PL, 2, 65, 64, 1, None, None, 3) == 2
     g = binding.load().lbi_scan_backward_streaming
-    assert g(PA, PB, PL, POUT, 2, 65, 64, 1, None, None, 3, 0x60000000, 4) == 2
+    assert g(PA, PB, PL, POUT, 2, 65, 64, 1, None, None, 3, 0x60000000, 4, None) == 2
     h = binding.load().lbi_scan_backward_ragged
     w65 = (ctypes.c_int32 * 66)(*([64] * 66))
     assert h(PA, PB, PL, POUT, 2, 65, w65, 1, None, 3) == 2
@@ -194,12 +194,35 @@ def test_suffix_products_argument_errors():
 def test_streaming_argument_errors():
     f = binding.load().lbi_scan_backward_streaming
     PP = 0x60000000
-    assert f(PA, PB, PL, POUT, 2, 3, 64, 0, None, None, 0, PP, 0) == 2     # chunk < 1
-    assert f(PA, PB, PL, POUT, 2, 3, 64, 0, None, None, 0, None, 4) == 1   # no progress
-    assert f(PA, PB, PL, POUT, 2, 3, 64, 0, None, None, 0, PP + 2, 4) == 7
-    assert f(PA, PB, PL, POUT, 2, 3, 64, 0, None, None, 0, PA + 64, 4) == 8
-    assert f(PA, PB, PL, POUT, 2, 3, 64, 3, None, None, 0, PP, 4) == 3
-    assert f(None, None, None, None, 0, 3, 64, 0, None, None, 0, None, 4) == 0
+    assert f(PA, PB, PL, POUT, 2, 3, 64, 0, None, None, 0, PP, 0, None) == 2     # chunk < 1
+    assert f(PA, PB, PL, POUT, 2, 3, 64, 0, None, None, 0, None, 4, None) == 1   # no progress
+    assert f(PA, PB, PL, POUT, 2, 3, 64, 0, None, None, 0, PP + 2, 4, None) == 7
+    assert f(PA, PB, PL, POUT, 2, 3, 64, 0, None, None, 0, PA + 64, 4, None) == 8
+    assert f(PA, PB, PL, POUT, 2, 3, 64, 3, None, None, 0, PP, 4, None) == 3
+    assert f(None, None, None, None, 0, 3, 64, 0, None, None, 0, None, 4, None) == 0
+
+
+def test_streaming_clock_argument_errors():
+    f = binding.load().lbi_scan_backward_streaming
+    PP, PC = 0x60000000, 0x68000000
+    assert f(PA, PB, PL, POUT, 2, 3, 64, 0, None, None, 0, PP, 4, PC + 4) == 7   # 8-byte
+    assert f(PA, PB, PL, POUT, 2, 3, 64, 0, None, None, 0, PP, 4, PP) == 8       # on progress
+    assert f(PA, PB, PL, POUT, 2, 3, 64, 0, None, None, 0, PP, 4, POUT + 8) == 8
+    assert f(None, PB, PL, POUT, 2, 3, 64, 0, None, None, 0, PP, 4, PC) == 1
+    assert f(PA, PB, PL, POUT, 1, 2**32, 16, 0, None, None, 0, PP, 4, PC) == 2   # 32-bit counts
+
+
+def test_wait_progress_argument_errors():
+    f = binding.load().lbi_wait_progress
+    PP, PR, PC = 0x60000000, 0x64000000, 0x68000000
+    assert f(PP, -1, 1, 10, PR, PC, None) == 2              # B < 0
+    assert f(PP, 2, 1, 0, PR, PC, None) == 2                # max_polls < 1
+    assert f(None, 2, 1, 10, PR, PC, None) == 1
+    assert f(PP + 2, 2, 1, 10, PR, PC, None) == 7
+    assert f(PP, 2, 1, 10, PR + 2, PC, None) == 7
+    assert f(PP, 2, 1, 10, PR, PC + 4, None) == 7
+    assert f(PP, 2, 1, 10, PP + 4, PC, None) == 8           # released on progress
+    assert f(PP, 2, 1, 10, PR, PR, None) == 8               # outputs overlap
 
 
 def test_matrix_norms_argument_errors():

@@ -576,26 +576,92 @@ def test_suffix_products_exact_on_permutations():
 
 @pytest.mark.parametrize("dtype,arith", MODES, ids=MODE_IDS)
 @pytest.mark.parametrize("B,K,r,chunk", [(3, 40, 64, 8), (2, 33, 16, 1), (1, 130, 128, 16),
-                                         (4, 7, 32, 64)])
-def test_streaming_matches_chain_scan(B, K, r, chunk, dtype, arith):
+                                         (4, 7, 32, 64), (5, 96, 64, 5)])
+def test_streaming_matches_oracle_and_chain_scan(B, K, r, chunk, dtype, arith):
+    """The streaming scan's adjoints against the oracle (element by element, at
+    the storage dtype's tolerance), equal to the chain scan's bit for bit, its
+    counters at K, and one publication clock per chunk, in order."""
     _say(f"[streaming] B={B} K={K} r={r} chunk={chunk} {dtype} {arith}")
     x = synth.random_chain(B, K, r, dtype=dtype, seed=43 + K)
     dev = torch.device("cuda:0")
     progress = torch.zeros(B, dtype=torch.int32, device=dev)
+    npub = -(-K // chunk)
+    clock = torch.zeros((B, npub), dtype=torch.int64, device=dev)
     lam = binding.lbi_scan_backward_streaming(x.A.to(dev), x.b.to(dev), x.lamK.to(dev), progress,
-                                              chunk, math=MATH[arith] if arith else 0)
+                                              chunk, math=MATH[arith] if arith else 0,
+                                              publish_clock=clock)
     torch.cuda.synchronize()
+    err = assert_close(lam.cpu().numpy(), ref(x), TOL[dtype], f"streaming {dtype} {arith}")
+    if dtype == "bf16":
+        assert err <= BF16_EXPECTED
     assert torch.equal(lam, run_gpu(x, math=arith, algo="chain"))
     assert progress.tolist() == [K] * B
+    c = clock.cpu()
+    assert bool((c > 0).all()), "a publication recorded no clock"
+    assert bool((c[:, 1:] >= c[:, :-1]).all()), "publications out of order"
 
 
-def test_streaming_exposes_adjoints_before_the_scan_ends():
-    """A second stream waits (hipStreamWaitValue32, >=) until 1024 adjoints of
-    every chain are published, then copies them while the scan still runs:
-    the copy must hold the final values.  Whether it also finishes before the
-    scan depends on how soon the command processor's wait sees the counter,
-    which the library does not control: that lead is reported, and a copy
-    that ends after the scan raises a warning, not a failure."""
+def test_streaming_releases_a_consumer_before_the_scan_ends():
+    """Phase 3's consumer pattern: a wait (lbi_wait_progress) is queued on a
+    second stream ahead of a copy of the 1024 adjoints of the latest regions;
+    the scan of 2 chains of 4096 slots runs on the first stream.  The library
+    controls both sides (the publications with system-scope atomics, the
+    wait's polls with system-scope acquire loads), so the test asserts:
+      * the wait was satisfied, and the copy holds the final adjoints;
+      * the adjoints meet the oracle (orthogonal chains: the fp32 rounding
+        walk bound 8 sqrt(K r) 2^-24) and equal the chain scan's;
+      * every chain published one clock per chunk, in order, spread evenly
+        over the run (the middle one between 30% and 70% of the span), not
+        bunched at the end;
+      * the wait ended after the publication that reached 1024 and before the
+        scan's last publication: the consumer started while the scan ran."""
+    B, K, r, n, chunk = 2, 4096, 64, 1024, 64
+    dev = torch.device("cuda:0")
+    x = synth.random_chain(B, K, r, dtype="f32", seed=47, spectrum="orthogonal", device=dev)
+    progress = torch.zeros(B, dtype=torch.int32, device=dev)
+    npub = K // chunk
+    clock = torch.zeros((B, npub), dtype=torch.int64, device=dev)
+    released = torch.zeros(1, dtype=torch.int32, device=dev)
+    rel_clock = torch.zeros(1, dtype=torch.int64, device=dev)
+    lam = torch.empty((B, K, r), dtype=torch.float32, device=dev)
+    snap = torch.empty((B, n, r), dtype=torch.float32, device=dev)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    # the consumer first: it waits (bounded) for the scan's publications
+    binding.lbi_wait_progress(progress, n, 1 << 20, released=released,
+                              release_clock=rel_clock, stream=s2)
+    with torch.cuda.stream(s2):
+        snap.copy_(lam[:, K - n:])
+    binding.lbi_scan_backward_streaming(x.A, x.b, x.lamK, progress, chunk, lam=lam, stream=s1,
+                                        publish_clock=clock)
+    torch.cuda.synchronize()
+    assert int(released.item()) == 1, "the wait gave up before the counters reached the target"
+    assert progress.tolist() == [K] * B
+    assert torch.equal(snap, lam[:, K - n:])
+    xh = x.to("cpu")
+    err = oracle.rel_frobenius(lam.cpu().numpy().astype(np.float64), ref(xh))
+    _say(f"  adjoints vs oracle: {err:.3e}")
+    assert err <= 8 * math.sqrt(K * r) * U32
+    assert torch.equal(lam, run_gpu(xh, math="split", algo="chain"))
+    c = clock.cpu().numpy().astype(np.int64)
+    assert (c > 0).all() and (np.diff(c, axis=1) >= 0).all()
+    span = c[:, -1] - c[:, 0]
+    mid = (c[:, npub // 2] - c[:, 0]) / np.maximum(span, 1)
+    t_rel = int(rel_clock.item())
+    reach = c[:, n // chunk - 1].max()   # both chains had published n adjoints
+    _say(f"  publications span {span.tolist()} ticks, middle at {mid.round(3).tolist()} of it; "
+         f"wait released {t_rel - reach} ticks after the target publication, "
+         f"{c[:, -1].max() - t_rel} ticks before the last one")
+    assert (span > 0).all() and ((mid > 0.3) & (mid < 0.7)).all(), "publications not spread"
+    assert reach <= t_rel < c[:, -1].max(), "the consumer was not released while the scan ran"
+
+
+def test_streaming_command_processor_wait_report():
+    """The same pattern with the command processor's wait
+    (hipStreamWaitValue32, >=) in place of lbi_wait_progress.  How soon the
+    command processor sees the counter is outside the library, so this only
+    reports the lead of the copy over the scan's end; the copy must hold the
+    final values."""
     import ctypes
     hip = ctypes.CDLL("libamdhip64.so")
     hip.hipStreamWaitValue32.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint32,
@@ -626,7 +692,5 @@ def test_streaming_exposes_adjoints_before_the_scan_ends():
     assert progress.tolist() == [K] * B
     assert torch.equal(snap, lam[:, K - n:])
     lead_ms = done_copy.elapsed_time(done_scan)
-    _say(f"  the copy of the first {n} adjoints finished {lead_ms:.3f} ms before the scan")
-    if lead_ms <= 0:
-        import warnings
-        warnings.warn(f"the waiting stream was released {-lead_ms:.3f} ms after the scan ended")
+    _say(f"  command-processor wait: the copy of the first {n} adjoints finished "
+         f"{lead_ms:.3f} ms before the scan's end (negative: after)")
