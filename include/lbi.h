@@ -34,7 +34,8 @@
  *   - Layout is C-contiguous row-major; every base pointer is 16-byte aligned.
  *   - bf16 is the upper half of an IEEE binary32 (torch.bfloat16).
  *   - Non-finite inputs propagate; nothing is checked for them.
- *   - Thread-safe: no mutable global state.
+ *   - Thread-safe: no mutable global state, except the scratch array of
+ *     lbi_scan_backward_noalloc (below), which its calls on one GPU share.
  */
 #ifndef LBI_H
 #define LBI_H
@@ -60,6 +61,10 @@ typedef struct ihipStream_t *lbi_stream_t;
  * 1.4e-2 at K = 128 on Haar-orthogonal x diag(U[0.9, 1.1]) chains at r = 64),
  * so up to this length it stays within half the bf16 tolerance of 2e-2. */
 #define LBI_BF16_SINGLE_MAX_K 64
+
+/* Bytes of the static device scratch array of lbi_scan_backward_noalloc (one
+ * per GPU the library runs on, held until the process ends). */
+#define LBI_NOALLOC_SCRATCH_BYTES (64u << 20)
 
 typedef enum {
     LBI_F32 = 0,  /* A, b, lambda_K stored as float32; float32 arithmetic   */
@@ -164,8 +169,10 @@ typedef enum {
     LBI_ERR_WORKSPACE = 5,     /* workspace missing or too small            */
     LBI_ERR_HIP = 6,           /* the HIP runtime refused the launch        */
     LBI_ERR_ALIGN = 7,         /* a pointer is not 16-byte aligned          */
-    LBI_ERR_ALIAS = 8          /* an output (or the workspace) overlaps an  *
+    LBI_ERR_ALIAS = 8,         /* an output (or the workspace) overlaps an  *
                                 * input                                     */
+    LBI_ERR_SCRATCH = 9        /* lbi_scan_backward_noalloc: the call needs *
+                                * more than LBI_NOALLOC_SCRATCH_BYTES       */
 } lbi_status;
 
 /*
@@ -243,6 +250,34 @@ lbi_status lbi_scan_backward_ex(const void *A, const void *b, const void *lambda
                                 float *lambda, int64_t B, int64_t K, int32_t r, lbi_dtype dt,
                                 void *workspace, size_t workspace_bytes, lbi_stream_t stream,
                                 const int32_t *widths_host, lbi_math math, lbi_algo algo);
+
+/*
+ * lbi_scan_backward_ex without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  The caller still passes the inputs and
+ * the output; the two-level scan's workspace is a static device array of
+ * LBI_NOALLOC_SCRATCH_BYTES (64 MiB) inside the library, one per GPU, held
+ * until the process ends.  The call allocates and frees nothing.
+ *
+ *   A, b, lambda_K, lambda, B, K, r, dt, stream, widths_host, math, algo: as
+ *   for lbi_scan_backward_ex.
+ * The algorithm is the one lbi_scan_backward_ex would run.  A two-level scan
+ * whose composites would not fit the array keeps only the segment aggregates
+ * and scans each segment again from its carry (the form lbi_scan_backward_ex
+ * takes past 256 MiB of composites); its results then agree with
+ * lbi_scan_backward_ex's to float32 rounding rather than bit for bit.  A call
+ * whose aggregates do not fit either returns LBI_ERR_SCRATCH before anything
+ * is enqueued.  The chain algorithms use no scratch and give exactly the
+ * results of lbi_scan_backward_ex.
+ * Every call on one GPU uses that GPU's one array, and the array keeps the
+ * last call's contents (nothing in it needs to start at zero): calls that
+ * overlap on one GPU (concurrent streams, or threads) race, and must be
+ * ordered by the caller.
+ */
+lbi_status lbi_scan_backward_noalloc(const void *A, const void *b, const void *lambda_K,
+                                     float *lambda, int64_t B, int64_t K, int32_t r,
+                                     lbi_dtype dt, lbi_stream_t stream,
+                                     const int32_t *widths_host, lbi_math math, lbi_algo algo);
 
 /*
  * The suffix composites themselves (Proposition "Scan Formulation of

@@ -28,7 +28,9 @@ LBI_ALGO_CHAIN = 1
 LBI_ALGO_TWO_LEVEL = 2
 LBI_ALGO_CHAIN_WAVE = 3
 LBI_ALGO_CHAIN_SPLITK = 4
+LBI_ERR_SCRATCH = 9
 LBI_BF16_SINGLE_MAX_K = 64
+LBI_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 _DTYPES = {torch.float32: LBI_F32, torch.bfloat16: LBI_BF16}
 
@@ -103,6 +105,10 @@ def load() -> ctypes.CDLL:
     lib.lbi_scan_backward_streaming.restype = ctypes.c_int
     lib.lbi_wait_progress.argtypes = [vp, i64, ctypes.c_uint32, i64, vp, vp, vp]
     lib.lbi_wait_progress.restype = ctypes.c_int
+    lib.lbi_scan_backward_noalloc.argtypes = [vp, vp, vp, vp, i64, i64, i32, ctypes.c_int, vp,
+                                              ctypes.POINTER(ctypes.c_int32), ctypes.c_int,
+                                              ctypes.c_int]
+    lib.lbi_scan_backward_noalloc.restype = ctypes.c_int
     lib.lbi_scan_backward_ragged.argtypes = [vp, vp, vp, vp, i64, i64,
                                              ctypes.POINTER(ctypes.c_int32), ctypes.c_int, vp,
                                              ctypes.c_int]
@@ -224,6 +230,21 @@ def lbi_scan_backward_ex(A: torch.Tensor, b: Optional[torch.Tensor], lambda_K: t
     lam, args = _marshal(A, b, lambda_K, lam, workspace, stream, algo)
     warr, wptr = _widths_arg(widths, int(A.shape[1]))
     _check(load().lbi_scan_backward_ex(*args, wptr, int(math), int(algo)))
+    return lam
+
+
+def lbi_scan_backward_noalloc(A: torch.Tensor, b: Optional[torch.Tensor],
+                              lambda_K: torch.Tensor, widths: Optional[Sequence[int]] = None,
+                              math: int = LBI_MATH_DEFAULT, algo: int = LBI_ALGO_AUTO,
+                              lam: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """As lbi_scan_backward_ex, with the library's static scratch array in
+    place of a workspace (the call itself allocates nothing; ``lam`` may be
+    passed to keep the binding from allocating the output)."""
+    lam, args = _marshal(A, b, lambda_K, lam, None, stream, LBI_ALGO_CHAIN)
+    Aptr, bptr, lkptr, lamptr, B_, K, r, dt, _ws, _wsb, sptr = args
+    warr, wptr = _widths_arg(widths, int(A.shape[1]))
+    _check(load().lbi_scan_backward_noalloc(Aptr, bptr, lkptr, lamptr, B_, K, r, dt, sptr, wptr,
+                                            int(math), int(algo)))
     return lam
 
 

@@ -18,11 +18,52 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "lbi_internal.h"
+
+// ---- the static scratch array (lbi_scan_backward_noalloc) --------------------
+//
+// The two-level scan's workspace, for callers that cannot allocate: one array
+// per GPU the library runs on, held until the process ends.  Host code never
+// passes the array's name to a kernel (on the host it names a stand-in, not
+// device memory): it takes the array's device address from
+// hipGetSymbolAddress once per device, with that device current, and passes
+// that address on.  Nothing in it needs to start at zero (the two-level scan
+// writes each part before reading it), so no call clears it.
+namespace lbi {
+__device__ __align__(256) char scratch[LBI_NOALLOC_SCRATCH_BYTES];
+}  // namespace lbi
 
 namespace {
 
 using namespace lbi;
+
+constexpr size_t kScratchBytes = (size_t)LBI_NOALLOC_SCRATCH_BYTES;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void *g_scratch_ptr[kMaxDevices];
+
+// The scratch array's address on the current device, or NULL (with *err set)
+// when the runtime does not give it.
+void *scratch_address(lbi_status *err)
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+        *err = LBI_ERR_HIP;
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(lbi::scratch)) != hipSuccess || !ptr) {
+            *err = LBI_ERR_HIP;
+            return nullptr;
+        }
+        g_scratch_ptr[dev] = ptr;
+    }
+    return g_scratch_ptr[dev];
+}
 
 bool supported_r(int32_t r) { return r == 16 || r == 32 || r == 64 || r == 128; }
 int waves_for_r(int32_t r) { return r == 16 ? 1 : (r == 32 ? 2 : 4); }
@@ -60,7 +101,8 @@ struct TwoLevelPlan {
     size_t offP, offc, offcarry, bytes;
 };
 
-TwoLevelPlan two_level_plan(int64_t B, int64_t K, int32_t r)
+// (force_rescan: the aggregates-only form whatever the composites' size)
+TwoLevelPlan two_level_plan(int64_t B, int64_t K, int32_t r, bool force_rescan = false)
 {
     TwoLevelPlan p;
     int64_t S = (int64_t)ceil(sqrt(2.0 * (double)K));
@@ -70,7 +112,7 @@ TwoLevelPlan two_level_plan(int64_t B, int64_t K, int32_t r)
         S = 1;
     p.L = (K + S - 1) / S;
     p.S = (int32_t)((K + p.L - 1) / p.L);
-    p.rescan = 4.0 * (double)B * K * r * r > kRescanBytes;
+    p.rescan = force_rescan || 4.0 * (double)B * K * r * r > kRescanBytes;
     const int64_t nslots = p.rescan ? (int64_t)p.S : K;  // composites kept per chain
     const size_t nP = (size_t)B * nslots * r * r * sizeof(float);
     const size_t nc = (size_t)B * nslots * r * sizeof(float);
@@ -186,9 +228,13 @@ hipError_t launch_chain_mode(const ChainLaunch &c, lbi_dtype dt, lbi_math math)
     return launch_chain_f32x(c);
 }
 
+// With scratch = true, ws / ws_bytes are the library's static scratch array:
+// a two-level scan whose composites do not fit it takes the aggregates-only
+// form, and one that does not fit even so is LBI_ERR_SCRATCH.
 lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam, int64_t B,
                      int64_t K, int32_t r, lbi_dtype dt, void *ws, size_t ws_bytes,
-                     lbi_stream_t stream, const int32_t *widths, lbi_math math, lbi_algo algo)
+                     lbi_stream_t stream, const int32_t *widths, lbi_math math, lbi_algo algo,
+                     bool scratch = false)
 {
     lbi_status st = check_common(dt, math, r, B, K);
     if (st != LBI_OK)
@@ -218,13 +264,28 @@ lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam,
     if (overlaps(lam, nout, A, nA) || overlaps(lam, nout, b, nb) || overlaps(lam, nout, lamK, nl))
         return LBI_ERR_ALIAS;
     const lbi_algo use = resolve_algo(algo, B, K, r, dt, math);
-    const TwoLevelPlan p = two_level_plan(B, K, r);
-    const size_t need = lbi_scan_backward_workspace_bytes_ex(B, K, r, dt, use);
-    if (need > 0 && (!ws || ws_bytes < need))
-        return LBI_ERR_WORKSPACE;
-    if (need > 0 && (overlaps(ws, need, A, nA) || overlaps(ws, need, b, nb) ||
-                     overlaps(ws, need, lamK, nl) || overlaps(ws, need, lam, nout)))
-        return LBI_ERR_ALIAS;
+    TwoLevelPlan p = two_level_plan(B, K, r);
+    size_t need = lbi_scan_backward_workspace_bytes_ex(B, K, r, dt, use);
+    if (scratch && need > kScratchBytes) {
+        p = two_level_plan(B, K, r, true);
+        need = p.bytes;
+        if (need > kScratchBytes)
+            return LBI_ERR_SCRATCH;
+    }
+    if (scratch && need > 0) {
+        // the library's own array: distinct from every caller buffer
+        lbi_status err = LBI_OK;
+        ws = scratch_address(&err);
+        if (!ws)
+            return err;
+        ws_bytes = kScratchBytes;
+    } else {
+        if (need > 0 && (!ws || ws_bytes < need))
+            return LBI_ERR_WORKSPACE;
+        if (need > 0 && (overlaps(ws, need, A, nA) || overlaps(ws, need, b, nb) ||
+                         overlaps(ws, need, lamK, nl) || overlaps(ws, need, lam, nout)))
+            return LBI_ERR_ALIAS;
+    }
 
     ChainLaunch c;
     memset(&c, 0, sizeof c);
@@ -658,6 +719,15 @@ lbi_status lbi_wait_progress(const uint32_t *progress, int64_t B, uint32_t targe
                : LBI_ERR_HIP;
 }
 
+lbi_status lbi_scan_backward_noalloc(const void *A, const void *b, const void *lambda_K,
+                                     float *lambda, int64_t B, int64_t K, int32_t r,
+                                     lbi_dtype dt, lbi_stream_t stream,
+                                     const int32_t *widths_host, lbi_math math, lbi_algo algo)
+{
+    return scan_impl(A, b, lambda_K, lambda, B, K, r, dt, nullptr, 0, stream, widths_host, math,
+                     algo, true);
+}
+
 const char *lbi_status_string(lbi_status s)
 {
     switch (s) {
@@ -670,6 +740,9 @@ const char *lbi_status_string(lbi_status s)
     case LBI_ERR_HIP: return "LBI_ERR_HIP: the HIP runtime refused the launch";
     case LBI_ERR_ALIGN: return "LBI_ERR_ALIGN: a pointer is not 16-byte aligned";
     case LBI_ERR_ALIAS: return "LBI_ERR_ALIAS: an output overlaps an input";
+    case LBI_ERR_SCRATCH:
+        return "LBI_ERR_SCRATCH: the call needs more than the library's static scratch array "
+               "(LBI_NOALLOC_SCRATCH_BYTES)";
     }
     return "unknown lbi_status";
 }

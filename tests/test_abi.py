@@ -34,7 +34,8 @@ def test_header_declares_entry_points():
                             "lbi_scan_suffix_products", "lbi_scan_backward_streaming",
                             "lbi_matrix_norms", "lbi_scan_backward_ragged",
                             "lbi_region_jacobians_workspace_bytes", "lbi_region_jacobians",
-                            "lbi_wait_progress", "lbi_status_string", "lbi_abi_version"])
+                            "lbi_wait_progress", "lbi_scan_backward_noalloc",
+                            "lbi_status_string", "lbi_abi_version"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -58,7 +59,7 @@ def test_header_compiles_as_c():
 def test_version_and_status_strings():
     assert binding.lbi_abi_version() == 10
     assert binding.lbi_status_string(0) == "LBI_OK"
-    for code in range(1, 9):
+    for code in range(1, 10):
         assert binding.lbi_status_string(code).startswith("LBI_ERR_")
     assert "unknown" in binding.lbi_status_string(99)
 
@@ -223,6 +224,23 @@ def test_wait_progress_argument_errors():
     assert f(PP, 2, 1, 10, PR, PC + 4, None) == 7
     assert f(PP, 2, 1, 10, PP + 4, PC, None) == 8           # released on progress
     assert f(PP, 2, 1, 10, PR, PR, None) == 8               # outputs overlap
+
+
+def test_noalloc_argument_errors():
+    f = binding.load().lbi_scan_backward_noalloc
+    # the argument checks of lbi_scan_backward_ex
+    assert f(PA, PB, PL, POUT, 2, 3, 64, 7, None, None, 0, 0) == 3
+    assert f(PA, PB, PL, POUT, 2, 3, 48, 0, None, None, 0, 0) == 4
+    assert f(None, PB, PL, POUT, 2, 3, 64, 0, None, None, 0, 0) == 1
+    assert f(PA, PB, PL, POUT + 4, 2, 3, 64, 0, None, None, 0, 0) == 7
+    assert f(PA, PB, PL, PA + 64, 2, 3, 64, 0, None, None, 0, 0) == 8
+    assert f(None, None, None, None, 0, 3, 64, 0, None, None, 0, 0) == 0
+    # 2048 chains of 2048 slots at r = 128, two-level: even the segment
+    # aggregates (64 segments of 64 KB per chain, 8.6 GB) pass the 64 MiB
+    # array; refused before anything is enqueued (far-apart fake addresses)
+    QA, QL, QO = 1 << 44, 1 << 45, 1 << 46
+    assert f(QA, None, QL, QO, 2048, 2048, 128, 0, None, None, 0, 2) == 9
+    assert "LBI_NOALLOC_SCRATCH_BYTES" in binding.lbi_status_string(9)
 
 
 def test_matrix_norms_argument_errors():
