@@ -451,6 +451,11 @@ def chain_mapping(wl, op, layout, math_name, algo_name, need) -> str:
     wavefront per chain; fp32 split arithmetic at r = 64 with B <= 256
     sixteen waves per chain; else one workgroup per chain)."""
     auto_adj = algo_name == "auto" and op == "adjoints" and layout == "padded"
+    chunk = 8 if wl.r == 64 else 16
+    if algo_name == "tree" or (auto_adj and wl.r <= 32 and wl.B <= 256 and wl.K <= chunk
+                               and math_name == "split"
+                               and wl.K >= (5 if wl.dtype == "f32" else 9)):
+        return "log-depth tree scan (a workgroup per chunk of slots, levels of aggregates)"
     if need:
         return "two-level scan (segments in parallel)"
     if algo_name == "chain_wave" or (auto_adj and wl.dtype == "bf16" and wl.r <= 32
@@ -501,7 +506,8 @@ def main(argv=None) -> int:
                          "cores (the library default) or the fp32 matrix cores; for bf16 "
                          "storage, bf16single feeds the running composite back rounded "
                          "once to bf16 (opt-in, lower accuracy)")
-    ap.add_argument("--algo", choices=["auto", "chain", "two_level", "chain_wave", "chain_splitk"],
+    ap.add_argument("--algo", choices=["auto", "chain", "two_level", "chain_wave", "chain_splitk",
+                                       "tree"],
                     default="auto",
                     help="scan algorithm (auto: the library's choice)")
     ap.add_argument("--op", choices=["adjoints", "suffix_products", "streaming", "norms",
@@ -654,7 +660,8 @@ def measure(wl, op, layout, math_name, algo_name, steps, warmup, chunk, torch, b
     algo = {"auto": binding.LBI_ALGO_AUTO, "chain": binding.LBI_ALGO_CHAIN,
             "two_level": binding.LBI_ALGO_TWO_LEVEL,
             "chain_wave": binding.LBI_ALGO_CHAIN_WAVE,
-            "chain_splitk": binding.LBI_ALGO_CHAIN_SPLITK}[algo_name]
+            "chain_splitk": binding.LBI_ALGO_CHAIN_SPLITK,
+            "tree": binding.LBI_ALGO_TREE}[algo_name]
     need = binding.lbi_scan_backward_workspace_bytes_ex(wl.B, wl.K, wl.r,
                                                          0 if wl.dtype == "f32" else 1, algo)
     ws = torch.empty((need,), dtype=torch.uint8, device=dev) if need else None

@@ -112,7 +112,11 @@ typedef enum {
                              * Otherwise bf16 with r <= 32 and B <= 8192 goes
                              * to LBI_ALGO_CHAIN_WAVE, and fp32 with r = 64 in
                              * the split arithmetic and B <= 256 to
-                             * LBI_ALGO_CHAIN_SPLITK                             */
+                             * LBI_ALGO_CHAIN_SPLITK.  Before all of these,
+                             * chains that fit one tree chunk at r <= 32
+                             * (K <= 16; K >= 5 for fp32, K >= 9 for bf16;
+                             * B <= 256; the default arithmetic) go to one
+                             * launch of LBI_ALGO_TREE                         */
     LBI_ALGO_CHAIN = 1,     /* one workgroup folds each whole chain right to
                              * left (K-1 combines, span K) and applies every
                              * composite to lambda_K as it forms; no workspace */
@@ -154,7 +158,25 @@ typedef enum {
                              * hint is accepted and not needed; no workspace.
                              * AUTO picks it for fp32 r = 64 in the split
                              * arithmetic with B <= 256 when it does not pick
-                             * LBI_ALGO_TWO_LEVEL                              */
+                             * LBI_ALGO_TWO_LEVEL                              */,
+    LBI_ALGO_TREE = 5       /* the log-depth scan of Proposition "Scan
+                             * Formulation of Backpropagation" (span
+                             * logarithmic in K, Proposition "Work-Span
+                             * Decomposition"): a workgroup takes a chunk of
+                             * C slots (C = 8 at r = 64, 16 at r <= 32), forms
+                             * its Blelloch up-sweep of matrix products (C - 1
+                             * products, log2 C deep, spread over the
+                             * chunk's waves) and a vector down-sweep
+                             * lambda_i = P lambda_{i+s} + c (log2 C deep);
+                             * longer chains go over levels of chunk
+                             * aggregates, 2L + 1 launches for K <= C^(L+1).
+                             * fp32 products by the exact three-part split for
+                             * both storage dtypes (LBI_MATH_DEFAULT, or
+                             * LBI_MATH_F32_SPLIT; others: LBI_ERR_DTYPE);
+                             * r <= 64 (else LBI_ERR_UNSUPPORTED_R); a widths
+                             * hint is accepted and not needed; workspace for
+                             * K > C (the aggregates and carries of each
+                             * level).  For chains too few to fill the GPU    */
 } lbi_algo;
 
 typedef enum {
@@ -187,7 +209,9 @@ size_t lbi_scan_backward_workspace_bytes(int64_t B, int64_t K, int32_t r, lbi_dt
  * As lbi_scan_backward_workspace_bytes, for a given algorithm: 0 for
  * LBI_ALGO_CHAIN, LBI_ALGO_CHAIN_WAVE and LBI_ALGO_CHAIN_SPLITK; for
  * LBI_ALGO_TWO_LEVEL about 4 B S r (r + 2) bytes with S ~ sqrt(2K) (the
- * segment aggregates in float32, plus the carries).
+ * segment aggregates in float32, plus the carries), or 4 B K r (r + 2) while
+ * every composite fits 256 MiB; for LBI_ALGO_TREE about 4 B (K / C) r (r + 2)
+ * bytes summed over its levels (0 for K <= C).
  */
 size_t lbi_scan_backward_workspace_bytes_ex(int64_t B, int64_t K, int32_t r, lbi_dtype dt,
                                             lbi_algo algo);

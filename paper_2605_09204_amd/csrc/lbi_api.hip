@@ -127,6 +127,94 @@ TwoLevelPlan two_level_plan(int64_t B, int64_t K, int32_t r, bool force_rescan =
 // The apply pass launches up to B*K workgroups.
 bool two_level_possible(int64_t B, int64_t K) { return B * K < ((int64_t)1 << 31) - 1; }
 
+// The tree scan over levels: level 0 is the chain of K slots, level l + 1
+// the chain of the chunk aggregates of level l (len[l + 1] = ceil(len[l] /
+// chunk)), up to the first level that fits one chunk.  Workspace per level
+// l >= 1: the aggregates P [B][len][r][r] and c [B][len][r] (with b), and the
+// lambda at each element's start [B][len][r], each 256-byte aligned.
+constexpr int kMaxTreeLevels = 24;
+struct TreePlan {
+    int nlev;  // levels above the slots
+    int64_t len[kMaxTreeLevels + 1];
+    size_t offP[kMaxTreeLevels + 1], offc[kMaxTreeLevels + 1], offl[kMaxTreeLevels + 1];
+    size_t bytes;
+};
+
+TreePlan tree_plan(int64_t B, int64_t K, int32_t r, bool aff)
+{
+    TreePlan t;
+    const int64_t C = tree_chunk(r);
+    t.nlev = 0;
+    t.len[0] = K;
+    while (t.len[t.nlev] > C && t.nlev < kMaxTreeLevels) {
+        t.len[t.nlev + 1] = (t.len[t.nlev] + C - 1) / C;
+        ++t.nlev;
+    }
+    size_t o = 0;
+    for (int l = 1; l <= t.nlev; ++l) {
+        t.offP[l] = o;
+        o += align256((size_t)B * t.len[l] * r * r * sizeof(float));
+        t.offc[l] = o;
+        if (aff)
+            o += align256((size_t)B * t.len[l] * r * sizeof(float));
+        t.offl[l] = o;
+        o += align256((size_t)B * t.len[l] * r * sizeof(float));
+    }
+    t.bytes = o;
+    return t;
+}
+
+// The tree scan launches up to B * ceil(K / chunk) workgroups.
+bool tree_possible(int64_t B, int64_t K, int32_t r)
+{
+    const int64_t C = tree_chunk(r);
+    return B * ((K + C - 1) / C) < ((int64_t)1 << 31) - 1;
+}
+
+// Every launch of the tree scan (see the level plan above).
+hipError_t run_tree(const void *A, const void *b, const void *lamK, float *lam, int64_t B,
+                    int64_t K, int32_t r, lbi_dtype dt, void *ws, hipStream_t st)
+{
+    const bool aff = b != nullptr, bf = dt == LBI_BF16;
+    const TreePlan t = tree_plan(B, K, r, aff);
+    char *w = (char *)ws;
+    auto Pl = [&](int l) { return (float *)(w + t.offP[l]); };
+    auto cl = [&](int l) { return aff ? (float *)(w + t.offc[l]) : nullptr; };
+    auto ll = [&](int l) { return (float *)(w + t.offl[l]); };
+    auto level_in = [&](int l, TreeArgs &a) {
+        a.A = l == 0 ? A : (const void *)Pl(l);
+        a.b = l == 0 ? b : (const void *)cl(l);
+        a.K = t.len[l];
+    };
+    TreeArgs a;
+    // up: each level's chunk aggregates
+    for (int l = 0; l < t.nlev; ++l) {
+        memset(&a, 0, sizeof a);
+        level_in(l, a);
+        a.S = (int32_t)t.len[l + 1];
+        a.Pagg = Pl(l + 1);
+        a.cagg = cl(l + 1);
+        const hipError_t e = launch_tree(a, B, r, l == 0 && bf, aff, true, st);
+        if (e != hipSuccess)
+            return e;
+    }
+    // down: the top level from lambda_K, then each level from the carries of
+    // the level above
+    for (int l = t.nlev; l >= 0; --l) {
+        memset(&a, 0, sizeof a);
+        level_in(l, a);
+        a.S = l == t.nlev ? 1 : (int32_t)t.len[l + 1];
+        a.lamNext = l == t.nlev ? nullptr : ll(l + 1);
+        a.lamK = lamK;
+        a.lamK_bf16 = bf ? 1 : 0;
+        a.lam = l == 0 ? lam : ll(l);
+        const hipError_t e = launch_tree(a, B, r, l == 0 && bf, aff, false, st);
+        if (e != hipSuccess)
+            return e;
+    }
+    return hipSuccess;
+}
+
 // Microseconds per slot of one chain-kernel workgroup on an otherwise idle
 // MI355X (r = 16, 32, 64, 128; fp32 storage in the default arithmetic).
 double slot_us(lbi_dtype dt, int32_t r)
@@ -138,6 +226,9 @@ double slot_us(lbi_dtype dt, int32_t r)
 
 // Chains per launch up to which AUTO takes LBI_ALGO_CHAIN_SPLITK: one per CU.
 constexpr int64_t kSplitKMaxB = 256;
+// Chains per launch up to which AUTO takes a single launch of LBI_ALGO_TREE
+// (the batches it was measured on).
+constexpr int64_t kTreeMaxB = 256;
 
 // LBI_ALGO_AUTO: the cheaper of the two by a cost model fitted to MI355X
 // timings (B = 1..512, K = 32..512, every r; within 13% of the faster choice
@@ -159,6 +250,15 @@ lbi_algo resolve_algo(lbi_algo algo, int64_t B, int64_t K, int32_t r, lbi_dtype 
 {
     if (algo != LBI_ALGO_AUTO)
         return algo;
+    // one launch of the tree scan (K within a chunk) at r <= 32: kernel
+    // times on MI355X (rocprofv3, B = 1..256) put it ahead of the chain
+    // kernels there, about twice as fast for fp32 at K = 16 (6.4 against
+    // 12.7 us at r = 32), for bf16 only past K = 8 (at smaller K the
+    // wavefront-per-chain kernel is as fast or faster); at r = 64 the chain
+    // kernels win
+    if (r <= 32 && B <= kTreeMaxB && K <= tree_chunk(r) && math != LBI_MATH_F32_MFMA &&
+        math != LBI_MATH_BF16_SINGLE && K >= (dt == LBI_F32 ? 5 : 9))
+        return LBI_ALGO_TREE;
     const lbi_algo chain =
         dt == LBI_BF16 && math != LBI_MATH_BF16_SINGLE && r <= 32 && B <= 8192 ? LBI_ALGO_CHAIN_WAVE
         : dt == LBI_F32 && math != LBI_MATH_F32_MFMA && r == 64 && B <= kSplitKMaxB
@@ -169,9 +269,18 @@ lbi_algo resolve_algo(lbi_algo algo, int64_t B, int64_t K, int32_t r, lbi_dtype 
     const double ts = slot_us(dt, r), w = waves_for_r(r), cap = 1280.0;
     const double t_chain = 6.0 + (double)K * ts * fmax(1.0, (double)B * w / cap);
     const TwoLevelPlan p = two_level_plan(B, K, r);
-    const double two = 12.0 + (double)p.L * ts * fmax(1.0, (double)B * p.S * w / cap) +
+    // (three launches: 18 us of fixed cost, measured with HIP events at
+    // B = 1..16, K = 16..64, where the chain scan's one launch costs 6 us
+    // plus its slots)
+    const double two = 18.0 + (double)p.L * ts * fmax(1.0, (double)B * p.S * w / cap) +
                        0.22 * p.S * sqrt(r / 64.0) + 8.0 * (double)B * K * r * r / 5.8e6;
     return two < t_chain ? LBI_ALGO_TWO_LEVEL : chain;
+}
+
+bool valid_algo(lbi_algo algo)
+{
+    return algo == LBI_ALGO_AUTO || algo == LBI_ALGO_CHAIN || algo == LBI_ALGO_TWO_LEVEL ||
+           algo == LBI_ALGO_CHAIN_WAVE || algo == LBI_ALGO_CHAIN_SPLITK || algo == LBI_ALGO_TREE;
 }
 
 lbi_status check_common(lbi_dtype dt, lbi_math math, int32_t r, int64_t B, int64_t K)
@@ -239,10 +348,16 @@ lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam,
     lbi_status st = check_common(dt, math, r, B, K);
     if (st != LBI_OK)
         return st;
-    if (algo != LBI_ALGO_AUTO && algo != LBI_ALGO_CHAIN && algo != LBI_ALGO_TWO_LEVEL &&
-        algo != LBI_ALGO_CHAIN_WAVE && algo != LBI_ALGO_CHAIN_SPLITK)
+    if (!valid_algo(algo))
         return LBI_ERR_DTYPE;
     if (algo == LBI_ALGO_TWO_LEVEL && !two_level_possible(B, K))
+        return LBI_ERR_SHAPE;
+    // the tree scan: the split arithmetic for fp32 (the default), r <= 64
+    if (algo == LBI_ALGO_TREE && (math == LBI_MATH_F32_MFMA || math == LBI_MATH_BF16_SINGLE))
+        return LBI_ERR_DTYPE;
+    if (algo == LBI_ALGO_TREE && r > 64)
+        return LBI_ERR_UNSUPPORTED_R;
+    if (algo == LBI_ALGO_TREE && !tree_possible(B, K, r))
         return LBI_ERR_SHAPE;
     if (algo == LBI_ALGO_CHAIN_WAVE && (dt != LBI_BF16 || math == LBI_MATH_BF16_SINGLE))
         return LBI_ERR_DTYPE;
@@ -267,8 +382,10 @@ lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam,
     TwoLevelPlan p = two_level_plan(B, K, r);
     size_t need = lbi_scan_backward_workspace_bytes_ex(B, K, r, dt, use);
     if (scratch && need > kScratchBytes) {
-        p = two_level_plan(B, K, r, true);
-        need = p.bytes;
+        if (use == LBI_ALGO_TWO_LEVEL) {
+            p = two_level_plan(B, K, r, true);
+            need = p.bytes;
+        }
         if (need > kScratchBytes)
             return LBI_ERR_SCRATCH;
     }
@@ -300,6 +417,9 @@ lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam,
     if (!encode_widths(widths, K, r, c))
         return LBI_ERR_SHAPE;
 
+    if (use == LBI_ALGO_TREE)
+        return run_tree(A, b, lamK, lam, B, K, r, dt, ws, c.stream) == hipSuccess ? LBI_OK
+                                                                                  : LBI_ERR_HIP;
     if (use == LBI_ALGO_CHAIN || use == LBI_ALGO_CHAIN_WAVE || use == LBI_ALGO_CHAIN_SPLITK) {
         c.args.lam = lam;
         c.args.L = K;
@@ -402,11 +522,13 @@ size_t lbi_scan_backward_workspace_bytes_ex(int64_t B, int64_t K, int32_t r, lbi
 {
     if (check_common(dt, LBI_MATH_DEFAULT, r, B, K) != LBI_OK || B == 0)
         return 0;
-    if (algo != LBI_ALGO_AUTO && algo != LBI_ALGO_CHAIN && algo != LBI_ALGO_TWO_LEVEL &&
-        algo != LBI_ALGO_CHAIN_WAVE && algo != LBI_ALGO_CHAIN_SPLITK)
+    if (!valid_algo(algo))
         return 0;
-    if (resolve_algo(algo, B, K, r, dt, LBI_MATH_DEFAULT) != LBI_ALGO_TWO_LEVEL ||
-        !two_level_possible(B, K))
+    const lbi_algo use = resolve_algo(algo, B, K, r, dt, LBI_MATH_DEFAULT);
+    if (use == LBI_ALGO_TREE)
+        // (sized for an affine term: enough with or without b)
+        return r <= 64 && tree_possible(B, K, r) ? tree_plan(B, K, r, true).bytes : 0;
+    if (use != LBI_ALGO_TWO_LEVEL || !two_level_possible(B, K))
         return 0;
     return two_level_plan(B, K, r).bytes;
 }

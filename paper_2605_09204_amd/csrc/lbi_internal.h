@@ -88,6 +88,28 @@ hipError_t launch_chain_wave_bf16(const ChainLaunch &c);
 bool chain_ksplit_supported(const ChainLaunch &c);
 hipError_t launch_chain_ksplit_f32x(const ChainLaunch &c);
 
+// The log-depth (tree) scan: one launch over chunks of tree_chunk(r) slots
+// of a chain level of K slots (S = ceil(K / chunk) chunks per chain, B * S
+// workgroups).  AGG: each chunk's aggregate (P [B][S][r][r], c [B][S][r]);
+// otherwise every lambda of the level, each chunk from its carry (lambda at
+// the start of the next chunk, lamNext [B][S][r], or lambda_K for the last).
+struct TreeArgs {
+    const void *A;        // [B][K][r][r], bf16 or fp32 (a_bf16 of launch_tree)
+    const void *b;        // [B][K][r] in A's dtype, or NULL
+    const void *lamK;     // [B][r], bf16 if lamK_bf16 else fp32
+    const float *lamNext; // [B][S][r]: lambda at each chunk's start, from the
+                          // level above (NULL when S = 1)
+    float *lam;           // [B][K][r] out (lambda mode)
+    float *Pagg;          // [B][S][r][r] out (AGG)
+    float *cagg;          // [B][S][r] out (AGG), or NULL
+    int64_t K;
+    int32_t S;
+    int32_t lamK_bf16;
+};
+int tree_chunk(int32_t r);
+hipError_t launch_tree(const TreeArgs &a, int64_t B, int32_t r, bool a_bf16, bool aff, bool agg,
+                       hipStream_t stream);
+
 // One wave polls progress[0..B-1] (acquire, device scope) until every entry
 // is at least target or max_polls polls have passed; then writes released[0]
 // (1: satisfied, 0: gave up) and release_clock[0] (the real-time counter),

@@ -148,9 +148,28 @@ def test_chain_splitk_argument_errors():
     assert call(r=32, algo=4) == 4              # LBI_ERR_UNSUPPORTED_R
     assert call(r=128, algo=4) == 4
     assert call(algo=4, A=None) == 1
-    assert call(algo=5) == 3                    # not an lbi_algo
+    assert call(algo=6) == 3                    # not an lbi_algo
     assert binding.lbi_scan_backward_workspace_bytes_ex(256, 32, 64, 0, 4) == 0
     assert binding.lbi_scan_backward_workspace_bytes_ex(2, 512, 64, 0, 4) == 0
+
+
+def test_tree_argument_errors():
+    # the log-depth scan: split arithmetic (the default) only, r <= 64
+    assert call(algo=5, r=128) == 4             # LBI_ERR_UNSUPPORTED_R
+    assert call(algo=5, math=1) == 3            # fp32 matrix cores: LBI_ERR_DTYPE
+    assert call(dt=1, algo=5, math=3) == 3      # single rounding: LBI_ERR_DTYPE
+    assert call(algo=5, A=None) == 1
+    assert call(algo=5, math=2, A=None) == 1
+    assert call(dt=1, algo=5, A=None) == 1
+    assert call(algo=6) == 3                    # not an lbi_algo
+    ws = binding.lbi_scan_backward_workspace_bytes_ex
+    assert ws(2, 8, 64, 0, 5) == 0              # one chunk: no workspace
+    assert ws(2, 16, 32, 1, 5) == 0
+    # K = 100 at r = 64: levels of 13 and 2 aggregates (P, c, carries)
+    lev = [13, 2]
+    want = sum(-(-(2 * n * x) // 256) * 256 for n in lev for x in (64 * 64 * 4, 64 * 4, 64 * 4))
+    assert ws(2, 100, 64, 0, 5) == want
+    assert ws(2, 100, 128, 0, 5) == 0           # unsupported r
 
 
 def test_bf16_single_argument_errors():
