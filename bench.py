@@ -173,8 +173,8 @@ def scan_payload_bytes(K: int, r: int, elem: int) -> int:
 
 # The sources the chain-scan kernel is compiled from (its traffic counters
 # stay valid while these are unchanged).
-CHAIN_SOURCES = ("lbi_chain.cuh", "lbi_chain_f32.hip", "lbi_chain_f32x.hip", "lbi_chain_bf16.hip",
-                 "lbi_device.cuh", "lbi_internal.h")
+CHAIN_SOURCES = ("lbi_chain.hpp", "lbi_chain_f32.hip", "lbi_chain_f32x.hip", "lbi_chain_bf16.hip",
+                 "lbi_device.hpp", "lbi_internal.h")
 
 
 def source_hash() -> str:

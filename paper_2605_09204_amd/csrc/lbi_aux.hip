@@ -18,7 +18,7 @@
 // with the loads of the next two issued ahead; the apply pass gives each
 // workgroup one or more whole slots, 16 KB of composites or more.
 
-#include "lbi_device.cuh"
+#include "lbi_device.hpp"
 #include "lbi_internal.h"
 
 namespace lbi {

@@ -61,12 +61,12 @@
 //     a slot early, where the slot barrier's wait covers it.
 //
 // All HIP code here is built with packed fp32 math disabled.
-#ifndef LBI_CHAIN_CUH
-#define LBI_CHAIN_CUH
+#ifndef LBI_CHAIN_HPP
+#define LBI_CHAIN_HPP
 
 #include <type_traits>
 
-#include "lbi_device.cuh"
+#include "lbi_device.hpp"
 #include "lbi_internal.h"
 
 namespace lbi {
@@ -281,7 +281,7 @@ __device__ __forceinline__ void combine(f4 (&Pn)[R / 16][NCA / waves_for(R)],
                     u4 hh, mm, ll;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        const Split2 s = split_pair(x[t][2 * e], x[t][2 * e + 1]);
+                        const Split2 s = split_pair_keep(x[t][2 * e], x[t][2 * e + 1]);
                         hh[e] = s.h;
                         mm[e] = s.m;
                         ll[e] = s.l;
@@ -1014,4 +1014,4 @@ hipError_t launch_chain(const ChainLaunch &c)
 }  // namespace
 }  // namespace lbi
 
-#endif  // LBI_CHAIN_CUH
+#endif  // LBI_CHAIN_HPP

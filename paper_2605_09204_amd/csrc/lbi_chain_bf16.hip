@@ -1,6 +1,6 @@
 // Chain-kernel instantiations for one arithmetic mode (one translation unit
 // per mode, so the library builds in parallel).
-#include "lbi_chain.cuh"
+#include "lbi_chain.hpp"
 
 namespace lbi {
 

@@ -38,7 +38,7 @@
 //
 // All HIP code here is built with packed fp32 math disabled.
 
-#include "lbi_chain.cuh"
+#include "lbi_chain.hpp"
 
 namespace lbi {
 namespace {
@@ -260,7 +260,7 @@ __global__ __launch_bounds__(1024) void scan_ksplit_kernel(const ScanArgs args)
                     u4 hh, mm, ll;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        const Split2 sp = split_pair(Po[e >> 1][2 * (e & 1)], Po[e >> 1][2 * (e & 1) + 1]);
+                        const Split2 sp = split_pair_keep(Po[e >> 1][2 * (e & 1)], Po[e >> 1][2 * (e & 1) + 1]);
                         hh[e] = sp.h;
                         mm[e] = sp.m;
                         ll[e] = sp.l;

@@ -1,8 +1,8 @@
 // Device helpers shared by the kernels of the LBI scan library: vector
 // types, lane exchanges within a wavefront, group reductions and the exact
 // three-part bf16 split of fp32 values.
-#ifndef LBI_DEVICE_CUH
-#define LBI_DEVICE_CUH
+#ifndef LBI_DEVICE_HPP
+#define LBI_DEVICE_HPP
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -186,7 +186,22 @@ __device__ __forceinline__ Split2 split_pair(float x0, float x1)
             __builtin_bit_cast(uint32_t, l)};
 }
 
+// The same three parts, with each remainder formed as x - part by an fp32
+// subtraction (exact for the same reason), which leaves x in its register:
+// for values that are still needed after the split.  (The dot-product form
+// above accumulates into its third operand, so the compiler copies x first
+// when x stays live.)
+__device__ __forceinline__ Split2 split_pair_keep(float x0, float x1)
+{
+    const uint32_t h = __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{x0, x1}, bf16x2));
+    const float r0 = x0 - bitsf(h << 16), r1 = x1 - bitsf(h & kHighHalf);
+    const uint32_t m = __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{r0, r1}, bf16x2));
+    const float l0 = r0 - bitsf(m << 16), l1 = r1 - bitsf(m & kHighHalf);
+    const uint32_t l = __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{l0, l1}, bf16x2));
+    return {h, m, l};
+}
+
 }  // namespace
 }  // namespace lbi
 
-#endif  // LBI_DEVICE_CUH
+#endif  // LBI_DEVICE_HPP

@@ -26,7 +26,7 @@
 // permuted (lane group q takes k = q r/4 + t at step t) so that each lane's
 // operands for four steps are one 16-byte LDS read.
 
-#include "lbi_device.cuh"
+#include "lbi_device.hpp"
 #include "lbi_internal.h"
 
 namespace lbi {

@@ -43,7 +43,7 @@
 //   gemm_nt x5  per k: Jdec^T, U'^T = (W1 Jdec)^T scaled by gbar, dp^T, T'^T, Jenc^T
 //   ln_jac      per (b, k): J, stored transposed as A[b][k]
 
-#include "lbi_device.cuh"
+#include "lbi_device.hpp"
 #include "lbi_internal.h"
 
 namespace lbi {

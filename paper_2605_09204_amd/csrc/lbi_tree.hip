@@ -42,7 +42,7 @@
 //
 // All HIP code here is built with packed fp32 math disabled.
 
-#include "lbi_device.cuh"
+#include "lbi_device.hpp"
 #include "lbi_internal.h"
 
 namespace lbi {
