@@ -458,6 +458,8 @@ def chain_mapping(wl, op, layout, math_name, algo_name, need) -> str:
         return "log-depth tree scan (a workgroup per chunk of slots, levels of aggregates)"
     if need:
         return "two-level scan (segments in parallel)"
+    if algo_name == "chain_ring":
+        return "one workgroup per chain, A tiles loaded into an LDS ring"
     if algo_name == "chain_wave" or (auto_adj and wl.dtype == "bf16" and wl.r <= 32
                                      and wl.B <= 8192 and math_name != "bf16single"):
         return "one wavefront per chain"
@@ -507,7 +509,7 @@ def main(argv=None) -> int:
                          "storage, bf16single feeds the running composite back rounded "
                          "once to bf16 (opt-in, lower accuracy)")
     ap.add_argument("--algo", choices=["auto", "chain", "two_level", "chain_wave", "chain_splitk",
-                                       "tree"],
+                                       "tree", "chain_ring"],
                     default="auto",
                     help="scan algorithm (auto: the library's choice)")
     ap.add_argument("--op", choices=["adjoints", "suffix_products", "streaming", "norms",
@@ -579,8 +581,8 @@ def main(argv=None) -> int:
         return 2
     wl = synth.WORKLOADS[args.workload]
     if args.B or args.K or args.r:
-        if wl.widths is not None:
-            print("--B/--K/--r apply to uniform-width workloads only", file=sys.stderr)
+        if wl.widths is not None and (args.K or args.r):
+            print("--K/--r apply to uniform-width workloads only", file=sys.stderr)
             return 2
         wl = wl.with_(B=args.B or wl.B, K=args.K or wl.K, r=args.r or wl.r,
                       name=f"{wl.name}_B{args.B or wl.B}_K{args.K or wl.K}_r{args.r or wl.r}")
@@ -661,7 +663,8 @@ def measure(wl, op, layout, math_name, algo_name, steps, warmup, chunk, torch, b
             "two_level": binding.LBI_ALGO_TWO_LEVEL,
             "chain_wave": binding.LBI_ALGO_CHAIN_WAVE,
             "chain_splitk": binding.LBI_ALGO_CHAIN_SPLITK,
-            "tree": binding.LBI_ALGO_TREE}[algo_name]
+            "tree": binding.LBI_ALGO_TREE,
+            "chain_ring": binding.LBI_ALGO_CHAIN_RING}[algo_name]
     need = binding.lbi_scan_backward_workspace_bytes_ex(wl.B, wl.K, wl.r,
                                                          0 if wl.dtype == "f32" else 1, algo)
     ws = torch.empty((need,), dtype=torch.uint8, device=dev) if need else None

@@ -50,7 +50,7 @@ extern "C" {
 /* HIP stream handle (the same type as hipStream_t). */
 typedef struct ihipStream_t *lbi_stream_t;
 
-#define LBI_ABI_VERSION 10
+#define LBI_ABI_VERSION 11
 
 /* Largest K for which a widths hint is used (longer chains run unhinted,
  * which gives identical results). */
@@ -176,7 +176,21 @@ typedef enum {
                              * r <= 64 (else LBI_ERR_UNSUPPORTED_R); a widths
                              * hint is accepted and not needed; workspace for
                              * K > C (the aggregates and carries of each
-                             * level).  For chains too few to fill the GPU    */
+                             * level).  For chains too few to fill the GPU    */,
+    LBI_ALGO_CHAIN_RING = 6 /* the chain scan (the combines and apply of
+                             * LBI_ALGO_CHAIN) with each A_j tile loaded
+                             * straight from HBM into a ring of LDS blocks by
+                             * buffer-to-LDS loads two slots ahead, only its
+                             * live r_j x r_{j+1} part, and c_j formed on the
+                             * matrix cores beside P_j: no staging registers,
+                             * four chains per CU.  bf16 storage with
+                             * LBI_MATH_DEFAULT or a float32 choice (else
+                             * LBI_ERR_DTYPE); r in {64, 128} with every
+                             * width r_k in {32, 64, 128}, r_K = 64,
+                             * K <= LBI_MAX_HINT_K, and the tiles of any
+                             * three consecutive slots within 36 KB of LDS
+                             * (else LBI_ERR_SHAPE; no widths: every r_k = r);
+                             * no workspace                                   */
 } lbi_algo;
 
 typedef enum {
@@ -184,7 +198,8 @@ typedef enum {
     LBI_ERR_NULL = 1,          /* a required pointer is NULL                */
     LBI_ERR_SHAPE = 2,         /* B < 0, K < 1, size overflow, bad widths,  *
                                 * K past LBI_BF16_SINGLE_MAX_K for         *
-                                * LBI_MATH_BF16_SINGLE                     */
+                                * LBI_MATH_BF16_SINGLE, widths that       *
+                                * LBI_ALGO_CHAIN_RING does not take        */
     LBI_ERR_DTYPE = 3,         /* dtype not an lbi_dtype, math not an       *
                                 * lbi_math, or algo not an lbi_algo         */
     LBI_ERR_UNSUPPORTED_R = 4, /* r not in {16, 32, 64, 128}                */
@@ -207,7 +222,8 @@ size_t lbi_scan_backward_workspace_bytes(int64_t B, int64_t K, int32_t r, lbi_dt
 
 /*
  * As lbi_scan_backward_workspace_bytes, for a given algorithm: 0 for
- * LBI_ALGO_CHAIN, LBI_ALGO_CHAIN_WAVE and LBI_ALGO_CHAIN_SPLITK; for
+ * LBI_ALGO_CHAIN, LBI_ALGO_CHAIN_WAVE, LBI_ALGO_CHAIN_SPLITK and
+ * LBI_ALGO_CHAIN_RING; for
  * LBI_ALGO_TWO_LEVEL about 4 B S r (r + 2) bytes with S ~ sqrt(2K) (the
  * segment aggregates in float32, plus the carries), or 4 B K r (r + 2) while
  * every composite fits 256 MiB; for LBI_ALGO_TREE about 4 B (K / C) r (r + 2)

@@ -29,6 +29,7 @@ LBI_ALGO_TWO_LEVEL = 2
 LBI_ALGO_CHAIN_WAVE = 3
 LBI_ALGO_CHAIN_SPLITK = 4
 LBI_ALGO_TREE = 5
+LBI_ALGO_CHAIN_RING = 6
 LBI_ERR_SCRATCH = 9
 LBI_BF16_SINGLE_MAX_K = 64
 LBI_NOALLOC_SCRATCH_BYTES = 64 << 20

@@ -19,7 +19,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 SOURCES = ["lbi_chain_f32.hip", "lbi_chain_f32x.hip", "lbi_chain_bf16.hip", "lbi_chain_bf16r1.hip",
            "lbi_chain_wave.hip",
-           "lbi_chain_ksplit.hip", "lbi_tree.hip", "lbi_aux.hip", "lbi_norms.hip", "lbi_region.hip",
+           "lbi_chain_ksplit.hip", "lbi_tree.hip", "lbi_chain_ring.hip", "lbi_aux.hip", "lbi_norms.hip", "lbi_region.hip",
            "lbi_api.hip"]
 INCLUDE = os.path.join(ROOT, "include")
 LIBDIR = os.path.join(PKG, "_lib")

@@ -280,7 +280,73 @@ lbi_algo resolve_algo(lbi_algo algo, int64_t B, int64_t K, int32_t r, lbi_dtype 
 bool valid_algo(lbi_algo algo)
 {
     return algo == LBI_ALGO_AUTO || algo == LBI_ALGO_CHAIN || algo == LBI_ALGO_TWO_LEVEL ||
-           algo == LBI_ALGO_CHAIN_WAVE || algo == LBI_ALGO_CHAIN_SPLITK || algo == LBI_ALGO_TREE;
+           algo == LBI_ALGO_CHAIN_WAVE || algo == LBI_ALGO_CHAIN_SPLITK || algo == LBI_ALGO_TREE ||
+           algo == LBI_ALGO_CHAIN_RING;
+}
+
+// The LDS-ring chain kernel (lbi_chain_ring.hip).  Shapes it takes: storage
+// width r of 64 or 128, every interface width 32, 64 or 128 (at most r),
+// r_K = 64, K within the widths hint.  A tile of slot j is
+// (r_j / 16) x (r_{j+1} / 32) blocks of 1 KB; the kernel keeps the tiles of
+// three consecutive slots in a ring of blocks, each placed right after the
+// previous one, or at block 0 when it would pass the ring's end.  The ring
+// size is the smallest, from the largest three-slot sum up, for which that
+// rule never overlaps three consecutive tiles (the rule is run here, the same
+// way); at most kRingMaxBlocks, so that four chains share a CU.
+constexpr int kRingMaxBlocks = 36;
+struct RingPlan {
+    bool ok;
+    int ring, dpw;
+};
+RingPlan ring_plan(const int32_t *widths, int64_t K, int32_t r)
+{
+    RingPlan p{false, 0, 0};
+    if ((r != 64 && r != 128) || K < 1 || K > LBI_MAX_HINT_K)
+        return p;
+    auto wd = [&](int64_t k) { return widths ? widths[k] : r; };
+    for (int64_t k = 0; k <= K; ++k) {
+        const int32_t x = wd(k);
+        if ((x != 32 && x != 64 && x != 128) || x > r)
+            return p;
+    }
+    if (wd(K) != 64)
+        return p;
+    auto blocks = [&](int64_t j) { return j >= 0 ? (wd(j) / 16) * (wd(j + 1) / 32) : 0; };
+    int win = 0;
+    for (int64_t j = 0; j < K; ++j) {
+        if (blocks(j) > (r == 64 ? 8 : 16))
+            return p;
+        const int s3 = blocks(j) + blocks(j - 1) + blocks(j - 2);
+        win = s3 > win ? s3 : win;
+    }
+    for (int ring = win; ring <= kRingMaxBlocks; ++ring) {
+        // bases of tiles K-1, K-2, ... by the kernel's rule; tiles j, j-1,
+        // j-2 must not overlap (each sits inside the ring by construction)
+        int b0 = 0, b1 = -1, b2 = -1;  // bases of tiles j, j+1, j+2
+        bool good = true;
+        for (int64_t j = K - 1; j >= 0 && good; --j) {
+            if (j < K - 1) {
+                const int nxt = b1 + blocks(j + 1);
+                b0 = nxt + blocks(j) <= ring ? nxt : 0;
+            }
+            auto disjoint = [&](int ba, int64_t ja, int bb, int64_t jb) {
+                return ba + blocks(ja) <= bb || bb + blocks(jb) <= ba;
+            };
+            if (j + 1 <= K - 1 && !disjoint(b0, j, b1, j + 1))
+                good = false;
+            if (j + 2 <= K - 1 && !disjoint(b0, j, b2, j + 2))
+                good = false;
+            b2 = b1;
+            b1 = b0;
+        }
+        if (good) {
+            p.ok = true;
+            p.ring = ring;
+            p.dpw = r == 64 ? 2 : 4;
+            return p;
+        }
+    }
+    return p;
 }
 
 lbi_status check_common(lbi_dtype dt, lbi_math math, int32_t r, int64_t B, int64_t K)
@@ -367,6 +433,10 @@ lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam,
         return LBI_ERR_DTYPE;
     if (algo == LBI_ALGO_CHAIN_SPLITK && r != 64)
         return LBI_ERR_UNSUPPORTED_R;
+    if (algo == LBI_ALGO_CHAIN_RING && (dt != LBI_BF16 || math == LBI_MATH_BF16_SINGLE))
+        return LBI_ERR_DTYPE;
+    if (algo == LBI_ALGO_CHAIN_RING && !ring_plan(widths, K, r).ok)
+        return LBI_ERR_SHAPE;
     if (B == 0)
         return LBI_OK;
     if (!A || !lamK || !lam)
@@ -420,6 +490,22 @@ lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam,
     if (use == LBI_ALGO_TREE)
         return run_tree(A, b, lamK, lam, B, K, r, dt, ws, c.stream) == hipSuccess ? LBI_OK
                                                                                   : LBI_ERR_HIP;
+    if (use == LBI_ALGO_CHAIN_RING) {
+        const RingPlan rp = ring_plan(widths, K, r);
+        c.args.lam = lam;
+        c.args.L = K;
+        c.args.S = 1;
+        c.args.ring = rp.ring;
+        c.args.pitch = r;
+        c.out = kOutLambda;
+        if (!c.hint) {
+            // uniform widths: the kernel reads them from the width codes
+            const int32_t code = r / 16;
+            for (int64_t k = 0; k <= K; ++k)
+                c.args.wcode[k >> 3] |= (uint32_t)code << ((k & 7) * 4);
+        }
+        return launch_chain_ring_bf16(c, rp.dpw) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
+    }
     if (use == LBI_ALGO_CHAIN || use == LBI_ALGO_CHAIN_WAVE || use == LBI_ALGO_CHAIN_SPLITK) {
         c.args.lam = lam;
         c.args.L = K;
@@ -662,6 +748,16 @@ lbi_status lbi_scan_backward_ragged(const void *A, const void *b, const void *la
     c.stream = (hipStream_t)stream;
     if (!encode_widths(widths_host, K, R, c) || !c.hint)
         return LBI_ERR_SHAPE;
+    // bf16 in the default arithmetic, widths the LDS-ring kernel takes: that
+    // kernel (it reads the compact tiles block by block)
+    if (dt == LBI_BF16 && math != LBI_MATH_BF16_SINGLE) {
+        const RingPlan rp = ring_plan(widths_host, K, R);
+        if (rp.ok) {
+            c.args.ring = rp.ring;
+            c.args.pitch = R;
+            return launch_chain_ring_bf16(c, rp.dpw) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
+        }
+    }
     return launch_chain_mode(c, dt, math) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
 }
 

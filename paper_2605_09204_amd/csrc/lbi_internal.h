@@ -56,6 +56,10 @@ struct ScanArgs {
     int32_t compact;
     int32_t totalA;
     int32_t totalR;
+    // The LDS-ring chain kernel: ring size in 1 KB blocks, and the row pitch
+    // (elements) of zero-padded storage.
+    int32_t ring;
+    int32_t pitch;
     // ceil(r_k / 16) for k = 0..K as 4-bit fields, 8 per word (hinted launches)
     uint32_t wcode[(LBI_MAX_HINT_K + 1 + 7) / 8];
 };
@@ -81,6 +85,16 @@ hipError_t launch_chain_bf16r1(const ChainLaunch &c);
 // chains, kOutLambda without progress counters; a widths hint is ignored).
 bool chain_wave_supported(const ChainLaunch &c);
 hipError_t launch_chain_wave_bf16(const ChainLaunch &c);
+
+// The chain scan with the A tiles streamed into an LDS ring by direct-to-LDS
+// loads (bf16 storage, hi + lo arithmetic, interface widths 32/64/128 with
+// r_K = 64, whole chains, kOutLambda without progress counters; c.args.ring
+// and c.args.pitch set, c.args.wcode holding the widths).  dpw: block loads
+// per wave and slot (2 with storage width 64: tiles up to 8 blocks of 16 x
+// 32; 4 with width 128: up to 16 blocks).  ring_lds_bytes: the launch's
+// dynamic LDS.
+hipError_t launch_chain_ring_bf16(const ChainLaunch &c, int dpw);
+int ring_lds_bytes(int ring, bool aff);
 
 // The chain scan with sixteen waves per chain for small batches (fp32 storage,
 // split arithmetic, r = 64, whole chains, kOutLambda without progress counters

@@ -57,7 +57,7 @@ def test_header_compiles_as_c():
 
 
 def test_version_and_status_strings():
-    assert binding.lbi_abi_version() == 10
+    assert binding.lbi_abi_version() == 11
     assert binding.lbi_status_string(0) == "LBI_OK"
     for code in range(1, 10):
         assert binding.lbi_status_string(code).startswith("LBI_ERR_")
@@ -148,7 +148,7 @@ def test_chain_splitk_argument_errors():
     assert call(r=32, algo=4) == 4              # LBI_ERR_UNSUPPORTED_R
     assert call(r=128, algo=4) == 4
     assert call(algo=4, A=None) == 1
-    assert call(algo=6) == 3                    # not an lbi_algo
+    assert call(algo=7) == 3                    # not an lbi_algo
     assert binding.lbi_scan_backward_workspace_bytes_ex(256, 32, 64, 0, 4) == 0
     assert binding.lbi_scan_backward_workspace_bytes_ex(2, 512, 64, 0, 4) == 0
 
@@ -161,7 +161,7 @@ def test_tree_argument_errors():
     assert call(algo=5, A=None) == 1
     assert call(algo=5, math=2, A=None) == 1
     assert call(dt=1, algo=5, A=None) == 1
-    assert call(algo=6) == 3                    # not an lbi_algo
+    assert call(algo=7) == 3                    # not an lbi_algo
     ws = binding.lbi_scan_backward_workspace_bytes_ex
     assert ws(2, 8, 64, 0, 5) == 0              # one chunk: no workspace
     assert ws(2, 16, 32, 1, 5) == 0
@@ -170,6 +170,36 @@ def test_tree_argument_errors():
     want = sum(-(-(2 * n * x) // 256) * 256 for n in lev for x in (64 * 64 * 4, 64 * 4, 64 * 4))
     assert ws(2, 100, 64, 0, 5) == want
     assert ws(2, 100, 128, 0, 5) == 0           # unsupported r
+
+
+def call_ex(widths, A=PA, B=2, r=128, dt=1, math=0, algo=6):
+    K = len(widths) - 1
+    arr = (ctypes.c_int32 * len(widths))(*widths)
+    return binding.load().lbi_scan_backward_ex(
+        A, PB, PL, POUT, B, K, r, dt, None, 0, None,
+        ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32)), math, algo)
+
+
+def test_chain_ring_argument_errors():
+    # the LDS-ring chain kernel: bf16 storage, default arithmetic, r in {64,
+    # 128}, widths 32/64/128 with r_K = 64, three tiles within the ring;
+    # rejected before any pointer is touched (A=None reaches LBI_ERR_NULL
+    # only for shapes it takes)
+    assert call(algo=6) == 3                    # fp32 storage: LBI_ERR_DTYPE
+    assert call(dt=1, math=3, algo=6) == 3      # single rounding: LBI_ERR_DTYPE
+    assert call(dt=1, r=64, algo=6, A=None) == 1
+    assert call(dt=1, r=32, algo=6) == 2        # storage width 32: LBI_ERR_SHAPE
+    assert call(dt=1, r=128, algo=6) == 2       # uniform 128: r_K != 64
+    assert call_ex([32, 64, 128, 32, 64], A=None) == 1
+    assert call_ex([32, 64, 128, 32, 64], r=64) == 2     # a width past r
+    assert call_ex([48, 64, 128, 32, 64]) == 2           # 48 not taken
+    assert call_ex([32, 64, 128, 32, 128]) == 2          # r_K = 128
+    assert call_ex([128, 128, 64, 64]) == 2              # a 128 x 128 tile
+    assert call_ex([64] * 2049, r=64) == 2               # K past the hint
+    assert call_ex([64] * 2048, r=64, A=None) == 1
+    assert call_ex([32, 64, 128, 32, 64], math=1, A=None) == 1  # fp32 choice acts as default
+    assert binding.lbi_scan_backward_workspace_bytes_ex(1024, 64, 128, 1, 6) == 0
+    assert binding.lbi_scan_backward_workspace_bytes_ex(4096, 32, 64, 1, 6) == 0
 
 
 def test_bf16_single_argument_errors():

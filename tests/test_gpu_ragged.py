@@ -2,8 +2,9 @@
 the C-ABI (needs a GPU).
 
 The ragged call runs the hinted chain scan on the same tiles, only addressed
-compactly, so it must equal the padded call with the widths hint and
-LBI_ALGO_CHAIN bit for bit; it is also held to the oracle at the tolerances of
+compactly, so it must equal the padded call with the widths hint and the same
+kernel bit for bit (LBI_ALGO_CHAIN_RING for the bf16 widths that the LDS-ring
+kernel takes, LBI_ALGO_CHAIN otherwise); it is also held to the oracle at the tolerances of
 the scan (fp32 1e-5, bf16 2e-2 relative Frobenius over the true-width values).
 """
 import sys
@@ -29,16 +30,33 @@ def _say(msg):
     sys.stdout.flush()
 
 
+def ring_takes(dtype, arith, widths, R):
+    """Whether the ragged call runs the LDS-ring kernel: bf16 in the default
+    arithmetic, widths 32/64/128 with r_K = 64, tiles of at most 16 blocks
+    (8 at R = 64); the ring sizes of these tests all fit."""
+    if dtype != "bf16" or arith is not None or R not in (64, 128) or widths[-1] != 64:
+        return False
+    if any(w not in (32, 64, 128) for w in widths):
+        return False
+    return all((widths[j] // 16) * (widths[j + 1] // 32) <= (8 if R == 64 else 16)
+               for j in range(len(widths) - 1))
+
+
 def _run_both(x, arith):
-    """(ragged result unpacked to [B, K, R], padded hinted chain-scan result)."""
+    """(ragged result unpacked to [B, K, R], the padded hinted call with the
+    same kernel: the LDS-ring chain scan where the ragged call takes it, else
+    the chain scan)."""
     R = x.A.shape[-1]
     p = synth.pack_ragged(x)
     lam_c = binding.lbi_scan_backward_ragged(
         p.A.to(DEV), None if p.b is None else p.b.to(DEV), p.lamK.to(DEV), p.widths,
         MATH[arith])
+    dtype = "bf16" if x.A.dtype == torch.bfloat16 else "f32"
+    algo = (binding.LBI_ALGO_CHAIN_RING if ring_takes(dtype, arith, x.widths, R)
+            else binding.LBI_ALGO_CHAIN)
     lam_p = binding.lbi_scan_backward_ex(
         x.A.to(DEV), None if x.b is None else x.b.to(DEV), x.lamK.to(DEV), list(x.widths),
-        MATH[arith], binding.LBI_ALGO_CHAIN)
+        MATH[arith], algo)
     torch.cuda.synchronize()
     return synth.unpack_ragged(lam_c, p.widths, R).cpu(), lam_p.cpu()
 
@@ -100,8 +118,10 @@ def test_ragged_mixed_widths_full_size():
     x = synth.generate(wl, device=DEV)
     p = synth.pack_ragged(x)
     lam_c = binding.lbi_scan_backward_ragged(p.A, p.b, p.lamK, p.widths)
+    # (the ragged call takes the LDS-ring kernel for these widths)
+    assert ring_takes("bf16", None, p.widths, wl.r)
     lam_p = binding.lbi_scan_backward_ex(x.A, x.b, x.lamK, list(x.widths), 0,
-                                         binding.LBI_ALGO_CHAIN)
+                                         binding.LBI_ALGO_CHAIN_RING)
     torch.cuda.synchronize()
     assert p.A.numel() * 3.3 < x.A.numel()
     assert torch.equal(synth.unpack_ragged(lam_c, p.widths, wl.r), lam_p)

@@ -74,3 +74,16 @@ def test_noalloc_without_scratch_use_matches_bit_for_bit():
         _say(f"[noalloc] B={B} K={K} r={r} {dt} chain")
         got, want = _both(x, binding.LBI_ALGO_CHAIN)
         assert torch.equal(got, want)
+
+
+def test_noalloc_tree_scan_levels_in_the_array():
+    """The tree scan over levels of chunk aggregates keeps each level's
+    aggregates and carries in the array: equal bit for bit to the workspace
+    call (the same plan), and at the parity bar against the oracle."""
+    for B, K, r, dt in ((3, 100, 64, "f32"), (2, 300, 32, "bf16")):
+        x = synth.random_chain(B, K, r, dtype=dt, seed=65 + K)
+        _say(f"[noalloc] B={B} K={K} r={r} {dt} tree")
+        got, want = _both(x, binding.LBI_ALGO_TREE)
+        _check(got, want, x, TOL[dt], f"tree B={B} K={K} {dt}")
+        assert torch.equal(got, want)
+
