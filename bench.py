@@ -63,11 +63,15 @@ def warm_up(step, args, torch) -> int:
             step(i)
         torch.cuda.synchronize()
         return args.warmup
+    # (launches back to back, as in the timed region: the GPU reaches its
+    # sustained clocks under continuous load, which short bursts between
+    # synchronizations do not give it; a synchronization every 256 launches
+    # bounds the queue)
     n, t0 = 0, time.perf_counter()
     while n < 5 or (time.perf_counter() - t0 < WARMUP_MIN_S and n < 20000):
         step(n)
         n += 1
-        if n % 8 == 0:
+        if n % 256 == 0:
             torch.cuda.synchronize()
     torch.cuda.synchronize()
     args.warmup = n

@@ -296,7 +296,7 @@ bool valid_algo(lbi_algo algo)
 constexpr int kRingMaxBlocks = 36;
 struct RingPlan {
     bool ok;
-    int ring, dpw;
+    int ring, maxb;
 };
 RingPlan ring_plan(const int32_t *widths, int64_t K, int32_t r)
 {
@@ -342,7 +342,7 @@ RingPlan ring_plan(const int32_t *widths, int64_t K, int32_t r)
         if (good) {
             p.ok = true;
             p.ring = ring;
-            p.dpw = r == 64 ? 2 : 4;
+            p.maxb = r == 64 ? 8 : 16;
             return p;
         }
     }
@@ -504,7 +504,7 @@ lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam,
             for (int64_t k = 0; k <= K; ++k)
                 c.args.wcode[k >> 3] |= (uint32_t)code << ((k & 7) * 4);
         }
-        return launch_chain_ring_bf16(c, rp.dpw) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
+        return launch_chain_ring_bf16(c, rp.maxb) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
     }
     if (use == LBI_ALGO_CHAIN || use == LBI_ALGO_CHAIN_WAVE || use == LBI_ALGO_CHAIN_SPLITK) {
         c.args.lam = lam;
@@ -755,7 +755,7 @@ lbi_status lbi_scan_backward_ragged(const void *A, const void *b, const void *la
         if (rp.ok) {
             c.args.ring = rp.ring;
             c.args.pitch = R;
-            return launch_chain_ring_bf16(c, rp.dpw) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
+            return launch_chain_ring_bf16(c, rp.maxb) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
         }
     }
     return launch_chain_mode(c, dt, math) == hipSuccess ? LBI_OK : LBI_ERR_HIP;

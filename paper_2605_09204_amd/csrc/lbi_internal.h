@@ -89,11 +89,10 @@ hipError_t launch_chain_wave_bf16(const ChainLaunch &c);
 // The chain scan with the A tiles streamed into an LDS ring by direct-to-LDS
 // loads (bf16 storage, hi + lo arithmetic, interface widths 32/64/128 with
 // r_K = 64, whole chains, kOutLambda without progress counters; c.args.ring
-// and c.args.pitch set, c.args.wcode holding the widths).  dpw: block loads
-// per wave and slot (2 with storage width 64: tiles up to 8 blocks of 16 x
-// 32; 4 with width 128: up to 16 blocks).  ring_lds_bytes: the launch's
-// dynamic LDS.
-hipError_t launch_chain_ring_bf16(const ChainLaunch &c, int dpw);
+// and c.args.pitch set, c.args.wcode holding the widths).  maxb: blocks of
+// 16 x 32 in the largest tile, 8 with storage width 64, 16 with 128.
+// ring_lds_bytes: the launch's dynamic LDS.
+hipError_t launch_chain_ring_bf16(const ChainLaunch &c, int maxb);
 int ring_lds_bytes(int ring, bool aff);
 
 // The chain scan with sixteen waves per chain for small batches (fp32 storage,
