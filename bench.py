@@ -178,7 +178,7 @@ def scan_payload_bytes(K: int, r: int, elem: int) -> int:
 # The sources the chain-scan kernel is compiled from (its traffic counters
 # stay valid while these are unchanged).
 CHAIN_SOURCES = ("lbi_chain.hpp", "lbi_chain_f32.hip", "lbi_chain_f32x.hip", "lbi_chain_bf16.hip",
-                 "lbi_device.hpp", "lbi_internal.h")
+                 "lbi_chain_ring.hip", "lbi_device.hpp", "lbi_internal.h")
 
 
 def source_hash() -> str:
@@ -214,7 +214,7 @@ def record_traffic(workload: str, fetch_csv: str, write_csv: str, copy_mib: int)
     for tag, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"),
                                ("write", write_csv, "WRITE_SIZE")):
         rows = [r for r in _counter_rows(path) if r[1] == counter]
-        scan = [v for n, _, v in rows if "scan_chain_kernel" in n]
+        scan = [v for n, _, v in rows if "scan_chain_kernel" in n or "scan_ring_kernel" in n]
         copy = [v for n, _, v in rows if "neg_kernel" in n]
         if not scan or not copy:
             raise SystemExit(f"{path}: no {counter} rows for the scan or the copy kernel")
@@ -462,7 +462,13 @@ def chain_mapping(wl, op, layout, math_name, algo_name, need) -> str:
         return "log-depth tree scan (a workgroup per chunk of slots, levels of aggregates)"
     if need:
         return "two-level scan (segments in parallel)"
-    if algo_name == "chain_ring":
+    ring_widths = wl.widths is not None and wl.widths[-1] == 64 and all(
+        w in (32, 64, 128) for w in wl.widths) and all(
+        (wl.widths[j] // 16) * (wl.widths[j + 1] // 32) <= 16 for j in range(wl.K))
+    if algo_name == "chain_ring" or (layout == "compact" and wl.dtype == "bf16" and ring_widths
+                                     and math_name != "bf16single") or (
+            algo_name == "auto" and op == "adjoints" and wl.dtype == "bf16" and wl.r == 128
+            and ring_widths and math_name != "bf16single"):
         return "one workgroup per chain, A tiles loaded into an LDS ring"
     if algo_name == "chain_wave" or (auto_adj and wl.dtype == "bf16" and wl.r <= 32
                                      and wl.B <= 8192 and math_name != "bf16single"):
@@ -637,6 +643,20 @@ def main(argv=None) -> int:
             others[name] = rec
             del x2
             torch.cuda.empty_cache()
+            if name == "mixed_widths":
+                # the same workload in compact storage (tiles at their true
+                # shapes back to back): no over-read of the zero padding
+                o3, x3 = measure(w2, "adjoints", "compact", "split", "auto", steps2, None,
+                                 args.chunk, torch, binding, synth, dev)
+                others["mixed_widths_compact"] = {
+                    "ms_per_step": o3["ms_per_step"],
+                    "avg_launch_ms": o3["extra"]["avg_launch_ms"],
+                    "value": o3["value"], "unit": o3["unit"], "steps": steps2,
+                    "warmup": o3["warmup"], "dtype": o3["dtype"], "config": o3["config"],
+                    "roofline": o3["roofline"], "alg_tflops": o3["extra"]["alg_tflops"],
+                    "alg_hbm_gbs": o3["extra"]["alg_hbm_gbs"]}
+                del x3
+                torch.cuda.empty_cache()
         out["extra"]["configs"] = others
     print(json.dumps(out), flush=True)
     return 0

@@ -116,7 +116,10 @@ typedef enum {
                              * chains that fit one tree chunk at r <= 32
                              * (K <= 16; K >= 5 for fp32, K >= 9 for bf16;
                              * B <= 256; the default arithmetic) go to one
-                             * launch of LBI_ALGO_TREE                         */
+                             * launch of LBI_ALGO_TREE.  Where AUTO would take
+                             * LBI_ALGO_CHAIN for bf16 stored at r = 128 (the
+                             * default arithmetic) and the widths hint is one
+                             * LBI_ALGO_CHAIN_RING takes, it takes that      */
     LBI_ALGO_CHAIN = 1,     /* one workgroup folds each whole chain right to
                              * left (K-1 combines, span K) and applies every
                              * composite to lambda_K as it forms; no workspace */

@@ -448,7 +448,14 @@ lbi_status scan_impl(const void *A, const void *b, const void *lamK, float *lam,
     const size_t nl = (size_t)B * r * esz, nout = (size_t)B * K * r * sizeof(float);
     if (overlaps(lam, nout, A, nA) || overlaps(lam, nout, b, nb) || overlaps(lam, nout, lamK, nl))
         return LBI_ERR_ALIAS;
-    const lbi_algo use = resolve_algo(algo, B, K, r, dt, math);
+    lbi_algo use = resolve_algo(algo, B, K, r, dt, math);
+    // bf16 chains stored at width 128 whose widths the LDS-ring kernel takes
+    // (the mixed-width case): that kernel, measured 1.45x faster there than
+    // the workgroup kernel (188 against 275 us on 1024 chains of 64 slots of
+    // widths 32/64/128); at width 64 the two tie
+    if (algo == LBI_ALGO_AUTO && use == LBI_ALGO_CHAIN && dt == LBI_BF16 &&
+        math != LBI_MATH_BF16_SINGLE && r == 128 && ring_plan(widths, K, r).ok)
+        use = LBI_ALGO_CHAIN_RING;
     TwoLevelPlan p = two_level_plan(B, K, r);
     size_t need = lbi_scan_backward_workspace_bytes_ex(B, K, r, dt, use);
     if (scratch && need > kScratchBytes) {

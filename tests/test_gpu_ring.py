@@ -153,3 +153,15 @@ def test_ring_empty_batch():
                                        torch.empty((0, 64), dtype=torch.bfloat16, device=DEV),
                                        None, 0, RING)
     assert lam.shape == (0, 4, 64)
+
+
+def test_auto_takes_the_ring_kernel_at_width_128():
+    """AUTO runs the LDS-ring kernel for bf16 stored at width 128 with widths
+    it takes (bit for bit the explicit call), and the workgroup kernel for
+    uniform width 64 (bit for bit LBI_ALGO_CHAIN).  (300 chains: enough that
+    AUTO's cost model keeps the chain scan rather than the two-level one.)"""
+    widths = cycle_ending_64(64, (32, 64, 128))
+    x = synth.random_chain(300, 64, 128, dtype="bf16", seed=95, widths=widths)
+    assert torch.equal(run(x, widths, binding.LBI_ALGO_AUTO), run(x, widths, RING))
+    y = synth.random_chain(300, 32, 64, dtype="bf16", seed=96)
+    assert torch.equal(run(y, None, binding.LBI_ALGO_AUTO), run(y, None, binding.LBI_ALGO_CHAIN))
