@@ -27,6 +27,12 @@ Bounded Interfaces"):
   tokens, LayerNorm over the r interface features with eps 1e-5): the forward
   written out in fp64 torch ops and J_k = dR_k(m_k) from torch autograd
   (Eq. "jacobian-identity-construction": the differential applied to I_r).
+  With ``phi="ssm"`` Phi_k mixes the tokens (the SSM-style region block of the
+  architecture section, "e.g. attention, SSM, MLP"): a causal diagonal linear
+  recurrence s_l = a_k * s_{l-1} + (1 - a_k) * x_l from s_0 = 0, then
+  Phi_k(x)_l = x_l + (W2 silu(W1 s_l)) * silu(s_l).  ``ssm_states`` is that
+  recurrence on its own; ``region_jacobian_columns`` gives chosen columns of
+  J_k by forward-mode AD (Eq. "basis-JVP": dR_k(m_k) e_j), for large regions.
 
 Every function here is pinned by the CPU tests against closed forms, exact
 rational brute force, invariants and torch autograd (see tests/test_oracle_*).
@@ -220,8 +226,23 @@ def _silu(t):
     return t * (1.0 / (1.0 + (-t).exp()))
 
 
-def region_forward(params: dict, k: int, x_embed_b, m_bk):
-    """R_k(m) for one sequence in float64: x_embed_b [L, D], m_bk [r] (torch)."""
+def ssm_states(x, a):
+    """The causal diagonal linear recurrence over the tokens of one sequence:
+    s_l = a * s_{l-1} + (1 - a) * x_l for l = 1..L, s_0 = 0; x [L, D], a [D]
+    (torch, any float dtype).  Returns s [L, D]."""
+    import torch
+    out = []
+    prev = torch.zeros_like(x[0])
+    for t in range(x.shape[0]):
+        prev = a * prev + (1.0 - a) * x[t]
+        out.append(prev)
+    return torch.stack(out)
+
+
+def region_forward(params: dict, k: int, x_embed_b, m_bk, phi: str = "mlp"):
+    """R_k(m) for one sequence in float64: x_embed_b [L, D], m_bk [r] (torch).
+    phi: "mlp" (token-wise residual MLP) or "ssm" (causal recurrence over the
+    tokens, then the MLP gated by silu of the state; needs params["decay"])."""
     import torch
     f = {n: v[k].to(torch.float64) for n, v in params.items()}
     x_embed_b = x_embed_b.to(torch.float64)
@@ -229,8 +250,17 @@ def region_forward(params: dict, k: int, x_embed_b, m_bk):
     # Dec_k: injects the interface state into the region (Eq. "concrete-region-injection")
     d = f["W_d2"] @ _silu(f["W_d1"] @ m + f["b_d1"]) + f["b_d2"]
     x_in = x_embed_b + d                               # [L, D]
-    # Phi_k: token-wise residual MLP
-    phi = x_in + _silu(x_in @ f["W1"].T) @ f["W2"].T   # [L, D]
+    if phi == "mlp":
+        # Phi_k: token-wise residual MLP
+        phi_out = x_in + _silu(x_in @ f["W1"].T) @ f["W2"].T   # [L, D]
+    elif phi == "ssm":
+        # Phi_k: the state s_l of the causal recurrence, the MLP on s_l gated
+        # by silu(s_l), plus the token's input
+        s = ssm_states(x_in, f["decay"])
+        phi_out = x_in + (_silu(s @ f["W1"].T) @ f["W2"].T) * _silu(s)
+    else:
+        raise ValueError(f"phi must be 'mlp' or 'ssm', got {phi!r}")
+    phi = phi_out
     # pool: mean over the L tokens
     p = phi.mean(dim=0)
     # Enc_k projects into the interface space
@@ -241,11 +271,12 @@ def region_forward(params: dict, k: int, x_embed_b, m_bk):
     return f["gamma"] * (z - mu) / torch.sqrt(var + LN_EPS) + f["beta"]
 
 
-def region_jacobians(params: dict, x_embed, m, pairs=None) -> Tuple[np.ndarray, np.ndarray]:
+def region_jacobians(params: dict, x_embed, m, pairs=None,
+                     phi: str = "mlp") -> Tuple[np.ndarray, np.ndarray]:
     """(J [B, K, r, r], m_next [B, K, r]) in float64: J[b, k] = d m_{k+1} / d m_k
     of region k at m[b, k] (rows: outputs), and m_next[b, k] = R_k(m[b, k]).
     With ``pairs`` (a list of (b, k)), only those entries are computed (the
-    rest are NaN)."""
+    rest are NaN).  ``phi`` selects the region block (``region_forward``)."""
     import torch
     B, K, r = m.shape
     J = np.full((B, K, r, r), np.nan)
@@ -254,7 +285,27 @@ def region_jacobians(params: dict, x_embed, m, pairs=None) -> Tuple[np.ndarray, 
     for b, k in todo:
         m0 = m[b, k].detach().to("cpu", torch.float64)
         xb = x_embed[b].detach().to("cpu")
-        fn = lambda mm: region_forward(params, k, xb, mm)  # noqa: E731
+        fn = lambda mm: region_forward(params, k, xb, mm, phi)  # noqa: E731
         J[b, k] = torch.autograd.functional.jacobian(fn, m0, vectorize=True).numpy()
         mn[b, k] = fn(m0).detach().numpy()
     return J, mn
+
+
+def region_jacobian_columns(params: dict, x_embed, m, b: int, k: int, cols,
+                            phi: str = "mlp") -> Tuple[np.ndarray, np.ndarray]:
+    """(columns [len(cols), r], m_next [r]) in float64: row i is column
+    cols[i] of J_k at m[b, k], dR_k(m_k) e_j by forward-mode AD (one
+    Jacobian-vector product per column, Eq. "basis-JVP")."""
+    import torch
+    m0 = m[b, k].detach().to("cpu", torch.float64)
+    xb = x_embed[b].detach().to("cpu")
+    fn = lambda mm: region_forward(params, k, xb, mm, phi)  # noqa: E731
+    out = []
+    val = None
+    for j in cols:
+        e = torch.zeros_like(m0)
+        e[j] = 1.0
+        val, tan = torch.func.jvp(fn, (m0,), (e,))
+        out.append(tan.detach().numpy())
+    mn = (val if val is not None else fn(m0)).detach().numpy()
+    return np.stack(out) if out else np.zeros((0, m0.shape[0])), mn

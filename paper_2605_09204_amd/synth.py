@@ -312,7 +312,10 @@ def unpack_ragged(lam: torch.Tensor, widths: Sequence[int], R: int) -> torch.Ten
 #   Dec_k = 2-layer MLP r -> D -> D:  W_d1 [D, r], b_d1 [D], W_d2 [D, D], b_d2 [D]
 #   Phi_k = token-wise residual MLP D -> X -> D:  W1 [X, D], W2 [D, X]
 #   Enc_k = 2-layer MLP D -> D -> r:  W_e1 [D, D], b_e1 [D], W_e2 [r, D], b_e2 [r]
-#   alpha_k (scalar), LN gain gamma [r] and shift beta [r].
+#   alpha_k (scalar), LN gain gamma [r] and shift beta [r];
+#   decay a_k [D] for the token-mixing block (Phi_k with a causal recurrence
+#   s_l = a_k s_{l-1} + (1 - a_k) x_l over the tokens, then
+#   Phi_k(x)_l = x_l + (W2 silu(W1 s_l)) silu(s_l)), unused by the token-wise one.
 # Matrices ~ N(0, 1/fan_in), rounded to bf16; biases ~ N(0, 0.01) and the
 # rest in fp32.  x_embed [B, L, D] ~ N(0, 1) in bf16; m [B, K, r] ~ N(0, 1) in
 # fp32 (each region's Jacobian depends only on its own m_k and x_embed).
@@ -379,4 +382,9 @@ def generate_region(wl: RegionWorkload, device="cpu") -> RegionInputs:
     p["beta"] = vec(r)
     x = torch.randn((wl.B, wl.L, D), generator=gen, device=device, dtype=torch.float64)
     m = torch.randn((wl.B, K, r), generator=gen, device=device, dtype=torch.float64)
+    # the token-mixing block's per-channel state decay a_k in [0.9, 0.999]
+    # (1 - a log-uniform over [1e-3, 1e-1]: memories of about 10 to 1000
+    # tokens), drawn last so that the other parameters do not depend on it
+    u = torch.rand((K, D), generator=gen, device=device, dtype=torch.float64)
+    p["decay"] = (1.0 - 10.0 ** (-3.0 + 2.0 * u)).to(torch.float32)
     return RegionInputs(p, x.to(torch.float32).to(torch.bfloat16), m.to(torch.float32), wl)
