@@ -50,7 +50,7 @@ extern "C" {
 /* HIP stream handle (the same type as hipStream_t). */
 typedef struct ihipStream_t *lbi_stream_t;
 
-#define LBI_ABI_VERSION 11
+#define LBI_ABI_VERSION 12
 
 /* Largest K for which a widths hint is used (longer chains run unhinted,
  * which gives identical results). */
@@ -513,6 +513,35 @@ lbi_status lbi_region_jacobians(const lbi_region_params *params, const void *x_e
                                 const float *m, float *A, float *m_next, int64_t B, int64_t K,
                                 int64_t L, int32_t D, int32_t X, int32_t r, void *workspace,
                                 size_t workspace_bytes, lbi_stream_t stream);
+
+/*
+ * Phase 1 for the same region map with a token-mixing region block, of the
+ * SSM kind that the architecture section lists among the region
+ * transformations: over the L tokens of a sequence,
+ *
+ *   s_l = a_k * s_{l-1} + (1 - a_k) * x_l   (l = 1 .. L, s_0 = 0, elementwise),
+ *   Phi_k(x)_l = x_l + (W2 silu(W1 s_l)) * silu(s_l),
+ *
+ * with x_l = x_embed_l + Dec_k(m_k), the mean pool, Enc_k and LN as above.  The
+ * tangent of all r directions is propagated through every token, as the
+ * batched construction of Eq. "jacobian-identity-construction" over
+ * B x L x D x r tensors does: per sequence and region, the products
+ * W1 (c_l Jdec) and W2 (.) over the L r columns of the directions, whose work
+ * is r times that of the token products of the forward (Eq. "jacobian-work").
+ *   decay    [K][D] float32 DEVICE pointer: a_k, each in [0, 1].
+ *   Other arguments, sizes, layouts and errors as lbi_region_jacobians, and
+ *   additionally L r / 128 <= 65535 (else LBI_ERR_SHAPE).  The workspace
+ *   (lbi_region_jacobians_ssm_workspace_bytes) holds the per-token tangent
+ *   products of a group of (sequence, region) pairs at a time, up to about
+ *   6 GiB plus the token-wise block's parts.
+ */
+size_t lbi_region_jacobians_ssm_workspace_bytes(int64_t B, int64_t K, int64_t L, int32_t D,
+                                                int32_t X, int32_t r);
+lbi_status lbi_region_jacobians_ssm(const lbi_region_params *params, const float *decay,
+                                    const void *x_embed, const float *m, float *A, float *m_next,
+                                    int64_t B, int64_t K, int64_t L, int32_t D, int32_t X,
+                                    int32_t r, void *workspace, size_t workspace_bytes,
+                                    lbi_stream_t stream);
 
 /* A static, human-readable name for a status code. */
 const char *lbi_status_string(lbi_status s);

@@ -120,6 +120,11 @@ def load() -> ctypes.CDLL:
     lib.lbi_region_jacobians.argtypes = [ctypes.POINTER(RegionParams), vp, vp, vp, vp, i64, i64,
                                          i64, i32, i32, i32, vp, sz, vp]
     lib.lbi_region_jacobians.restype = ctypes.c_int
+    lib.lbi_region_jacobians_ssm_workspace_bytes.argtypes = [i64, i64, i64, i32, i32, i32]
+    lib.lbi_region_jacobians_ssm_workspace_bytes.restype = sz
+    lib.lbi_region_jacobians_ssm.argtypes = [ctypes.POINTER(RegionParams), vp, vp, vp, vp, vp,
+                                             i64, i64, i64, i32, i32, i32, vp, sz, vp]
+    lib.lbi_region_jacobians_ssm.restype = ctypes.c_int
     lib.lbi_matrix_norms.argtypes = [vp, i64, i32, ctypes.c_int, vp, vp, vp]
     lib.lbi_matrix_norms.restype = ctypes.c_int
     lib.lbi_status_string.argtypes = [ctypes.c_int]
@@ -400,10 +405,26 @@ def lbi_region_jacobians_workspace_bytes(B: int, K: int, L: int, D: int, X: int,
                                                             int(X), int(r)))
 
 
+def lbi_region_jacobians_ssm_workspace_bytes(B: int, K: int, L: int, D: int, X: int,
+                                             r: int) -> int:
+    return int(load().lbi_region_jacobians_ssm_workspace_bytes(int(B), int(K), int(L), int(D),
+                                                                int(X), int(r)))
+
+
+def lbi_region_jacobians_ssm(params: dict, x_embed: torch.Tensor, m: torch.Tensor,
+                             A: Optional[torch.Tensor] = None,
+                             m_next: Optional[torch.Tensor] = None, want_m_next: bool = True,
+                             workspace: Optional[torch.Tensor] = None, stream=None):
+    """As ``lbi_region_jacobians`` for the token-mixing region block, whose
+    per-channel decay is params["decay"] ([K, D] float32)."""
+    return lbi_region_jacobians(params, x_embed, m, A, m_next, want_m_next, workspace, stream,
+                                _ssm=True)
+
+
 def lbi_region_jacobians(params: dict, x_embed: torch.Tensor, m: torch.Tensor,
                          A: Optional[torch.Tensor] = None, m_next: Optional[torch.Tensor] = None,
                          want_m_next: bool = True, workspace: Optional[torch.Tensor] = None,
-                         stream=None):
+                         stream=None, _ssm: bool = False):
     """(A [B, K, r, r] = J_k^T, m_next [B, K, r] or None), float32: Phase 1 for the
     synthetic region map (include/lbi.h), from the parameter dict of
     ``REGION_PARAM_FIELDS``, x_embed [B, L, D] bf16 and m [B, K, r] float32."""
@@ -428,13 +449,25 @@ def lbi_region_jacobians(params: dict, x_embed: torch.Tensor, m: torch.Tensor,
         A = torch.empty((B, K, r, r), dtype=torch.float32, device=x_embed.device)
     if want_m_next and m_next is None:
         m_next = torch.empty((B, K, r), dtype=torch.float32, device=x_embed.device)
-    need = lbi_region_jacobians_workspace_bytes(B, K, L, D, X, r)
+    rp = RegionParams(*ptrs)
+    tail = (m.data_ptr(), A.data_ptr(), m_next.data_ptr() if m_next is not None else None,
+            B, K, L, D, X, r)
+    if _ssm:
+        dec = params["decay"]
+        if (tuple(dec.shape) != (K, D) or dec.dtype != torch.float32 or not dec.is_contiguous()
+                or dec.device != x_embed.device):
+            raise ValueError(f"decay must be a contiguous float32 {(K, D)} tensor on x_embed's "
+                             "device")
+        need = lbi_region_jacobians_ssm_workspace_bytes(B, K, L, D, X, r)
+    else:
+        need = lbi_region_jacobians_workspace_bytes(B, K, L, D, X, r)
     if workspace is None and need > 0:
         workspace = torch.empty((need,), dtype=torch.uint8, device=x_embed.device)
-    rp = RegionParams(*ptrs)
-    _check(load().lbi_region_jacobians(
-        ctypes.byref(rp), x_embed.data_ptr(), m.data_ptr(), A.data_ptr(),
-        m_next.data_ptr() if m_next is not None else None, B, K, L, D, X, r,
-        workspace.data_ptr() if workspace is not None else None,
-        workspace.numel() if workspace is not None else 0, _stream_ptr(stream, x_embed.device)))
+    ws = (workspace.data_ptr() if workspace is not None else None,
+          workspace.numel() if workspace is not None else 0, _stream_ptr(stream, x_embed.device))
+    if _ssm:
+        _check(load().lbi_region_jacobians_ssm(ctypes.byref(rp), dec.data_ptr(),
+                                               x_embed.data_ptr(), *tail, *ws))
+    else:
+        _check(load().lbi_region_jacobians(ctypes.byref(rp), x_embed.data_ptr(), *tail, *ws))
     return A, m_next

@@ -593,6 +593,59 @@ RegionPlan region_plan(int64_t B, int64_t K, int64_t L, int32_t D, int32_t X, in
     return p;
 }
 
+// The token-mixing block adds, for G (sequence, region) pairs at a time: s16,
+// h16, S16, Vt (bf16), s32, c32, g32, y32, wv, Tpart (fp32), after the parts
+// above.  G is what fits kSsmGroupBytes (at least 1); the second tangent
+// product splits each pair's token tiles into nchunk chunks, enough for about
+// 1024 workgroups per group.
+constexpr int kSsmParts = 10;
+constexpr size_t kSsmGroupBytes = (size_t)6 << 30;
+
+struct SsmPlan {
+    RegionPlan base;
+    int64_t G;
+    int32_t nchunk;
+    size_t off[kSsmParts];
+    size_t bytes;
+};
+
+SsmPlan ssm_plan(int64_t B, int64_t K, int64_t L, int32_t D, int32_t X, int32_t r)
+{
+    SsmPlan p;
+    p.base = region_plan(B, K, L, D, X, r);
+    const size_t LD = (size_t)L * D, LX = (size_t)L * X, Lr = (size_t)L * r;
+    const size_t mtiles = (Lr + 127) / 128, nct = (size_t)(D + 127) / 128;
+    const size_t pair = align256(LD * 2) + align256(LX * 2) + align256(Lr * D * 2) +
+                        align256(Lr * X * 2) + 3 * align256(LD * 4) + align256(LX * 4) +
+                        align256((size_t)D * 4) + align256(mtiles * r * D * 4);
+    int64_t G = (int64_t)(kSsmGroupBytes / pair);
+    const int64_t BK = B * K;
+    if (G > BK)
+        G = BK;
+    if (G > 65535)
+        G = 65535;
+    if (G < 1)
+        G = 1;
+    size_t nch = (1024 + (size_t)G * nct - 1) / ((size_t)G * nct);
+    if (nch > mtiles)
+        nch = mtiles;
+    if (nch < 1)
+        nch = 1;
+    p.G = G;
+    p.nchunk = (int32_t)nch;
+    const size_t g = (size_t)G;
+    const size_t n[kSsmParts] = {g * LD * 2, g * LX * 2, g * Lr * D * 2, g * Lr * X * 2,
+                                 g * LD * 4, g * LD * 4, g * LX * 4, g * LD * 4,
+                                 g * D * 4, g * nch * r * D * 4};
+    size_t o = p.base.bytes;
+    for (int i = 0; i < kSsmParts; ++i) {
+        p.off[i] = o;
+        o += align256(n[i]);
+    }
+    p.bytes = o;
+    return p;
+}
+
 bool region_sizes_ok(int64_t B, int64_t K, int64_t L, int32_t D, int32_t X, int32_t r)
 {
     if (B < 0 || K < 1 || L < 1 || !supported_r(r))
@@ -606,6 +659,96 @@ bool region_sizes_ok(int64_t B, int64_t K, int64_t L, int32_t D, int32_t X, int3
     return B * K * (X / 128) < ((int64_t)1 << 31) - 1;
 }
 
+// the token-mixing block's first tangent product has L r rows: L r / 128 row
+// tiles in a launch's y
+bool ssm_sizes_ok(int64_t L, int32_t r) { return (L * r + 127) / 128 <= 65535; }
+
+}  // namespace
+
+namespace {
+// Argument checks shared by both region blocks; ws_need is the workspace the
+// block needs, decay its extra input (NULL for the token-wise block).
+lbi_status region_check(const lbi_region_params *params, const float *decay, bool ssm,
+                        const void *x_embed, const float *m, float *A, float *m_next, int64_t B,
+                        int64_t K, int64_t L, int32_t D, int32_t r, void *workspace,
+                        size_t workspace_bytes, size_t ws_need)
+{
+    if (!params)
+        return LBI_ERR_NULL;
+    if (B == 0)
+        return LBI_OK;
+    const lbi_region_params &p = *params;
+    const void *ptrs[] = {p.W_d1, p.b_d1, p.W_d2, p.b_d2, p.W1, p.W2, p.W_e1, p.b_e1, p.W_e2,
+                          p.b_e2, p.alpha, p.gamma, p.beta, x_embed, m, A};
+    for (const void *q : ptrs)
+        if (!q)
+            return LBI_ERR_NULL;
+    if (ssm && !decay)
+        return LBI_ERR_NULL;
+    for (const void *q : ptrs)
+        if (misaligned(q))
+            return LBI_ERR_ALIGN;
+    if (misaligned(m_next) || misaligned(workspace) || misaligned(decay))
+        return LBI_ERR_ALIGN;
+    if (!workspace || workspace_bytes < ws_need)
+        return LBI_ERR_WORKSPACE;
+    const size_t nA = (size_t)B * K * r * r * 4, nm = (size_t)B * K * r * 4;
+    const size_t nx = (size_t)B * L * D * 2;
+    if (overlaps(A, nA, x_embed, nx) || overlaps(A, nA, m, nm) ||
+        overlaps(A, nA, workspace, ws_need) || overlaps(m_next, nm, x_embed, nx) ||
+        overlaps(m_next, nm, m, nm) || overlaps(m_next, nm, A, nA) ||
+        overlaps(m_next, nm, workspace, ws_need) || overlaps(workspace, ws_need, m, nm) ||
+        overlaps(workspace, ws_need, x_embed, nx))
+        return LBI_ERR_ALIAS;
+    if (ssm) {
+        const size_t nd = (size_t)K * D * 4;
+        if (overlaps(A, nA, decay, nd) || overlaps(m_next, nm, decay, nd) ||
+            overlaps(workspace, ws_need, decay, nd))
+            return LBI_ERR_ALIAS;
+    }
+    return LBI_OK;
+}
+
+// The launch arguments of both blocks (the token-wise block's workspace parts).
+RegionArgs region_args(const lbi_region_params &p, const void *x_embed, const float *m, float *A,
+                       float *m_next, int64_t B, int64_t K, int64_t L, int32_t D, int32_t X,
+                       int32_t r, void *workspace, const RegionPlan &plan)
+{
+    RegionArgs q;
+    memset(&q, 0, sizeof q);
+    q.W_d1 = p.W_d1;
+    q.W_d2 = p.W_d2;
+    q.W1 = p.W1;
+    q.W2 = p.W2;
+    q.W_e1 = p.W_e1;
+    q.W_e2 = p.W_e2;
+    q.b_d1 = p.b_d1;
+    q.b_d2 = p.b_d2;
+    q.b_e1 = p.b_e1;
+    q.b_e2 = p.b_e2;
+    q.alpha = p.alpha;
+    q.gamma = p.gamma;
+    q.beta = p.beta;
+    q.x_embed = x_embed;
+    q.m = m;
+    q.A = A;
+    q.m_next = m_next;
+    q.B = B;
+    q.K = K;
+    q.L = L;
+    q.D = D;
+    q.X = X;
+    q.r = r;
+    char *w = (char *)workspace;
+    float **f32[15] = {&q.su,  &q.sa, &q.d,   &q.cvec, &q.xpart, &q.xbar, &q.sbar, &q.gbar,
+                       &q.p,   &q.sue, &q.se, &q.encv, &q.zhat,  &q.isig, &q.JencT};
+    for (int i = 0; i < 15; ++i)
+        *f32[i] = (float *)(w + plan.off[i]);
+    __bf16 **h16[5] = {&q.P1, &q.JdT, &q.UT, &q.dpT, &q.TT};
+    for (int i = 0; i < 5; ++i)
+        *h16[i] = (__bf16 *)(w + plan.off[15 + i]);
+    return q;
+}
 }  // namespace
 
 extern "C" {
@@ -776,6 +919,7 @@ size_t lbi_region_jacobians_workspace_bytes(int64_t B, int64_t K, int64_t L, int
     return region_plan(B, K, L, D, X, r).bytes;
 }
 
+
 lbi_status lbi_region_jacobians(const lbi_region_params *params, const void *x_embed,
                                 const float *m, float *A, float *m_next, int64_t B, int64_t K,
                                 int64_t L, int32_t D, int32_t X, int32_t r, void *workspace,
@@ -783,66 +927,55 @@ lbi_status lbi_region_jacobians(const lbi_region_params *params, const void *x_e
 {
     if (!region_sizes_ok(B, K, L, D, X, r))
         return r > 0 && !supported_r(r) ? LBI_ERR_UNSUPPORTED_R : LBI_ERR_SHAPE;
-    if (!params)
-        return LBI_ERR_NULL;
-    if (B == 0)
-        return LBI_OK;
-    const lbi_region_params &p = *params;
-    const void *ptrs[] = {p.W_d1, p.b_d1, p.W_d2, p.b_d2, p.W1, p.W2, p.W_e1, p.b_e1, p.W_e2,
-                          p.b_e2, p.alpha, p.gamma, p.beta, x_embed, m, A};
-    for (const void *q : ptrs)
-        if (!q)
-            return LBI_ERR_NULL;
-    for (const void *q : ptrs)
-        if (misaligned(q))
-            return LBI_ERR_ALIGN;
-    if (misaligned(m_next) || misaligned(workspace))
-        return LBI_ERR_ALIGN;
     const RegionPlan plan = region_plan(B, K, L, D, X, r);
-    if (!workspace || workspace_bytes < plan.bytes)
-        return LBI_ERR_WORKSPACE;
-    const size_t nA = (size_t)B * K * r * r * 4, nm = (size_t)B * K * r * 4;
-    const size_t nx = (size_t)B * L * D * 2;
-    if (overlaps(A, nA, x_embed, nx) || overlaps(A, nA, m, nm) ||
-        overlaps(A, nA, workspace, plan.bytes) || overlaps(m_next, nm, x_embed, nx) ||
-        overlaps(m_next, nm, m, nm) || overlaps(m_next, nm, A, nA) ||
-        overlaps(m_next, nm, workspace, plan.bytes) || overlaps(workspace, plan.bytes, m, nm) ||
-        overlaps(workspace, plan.bytes, x_embed, nx))
-        return LBI_ERR_ALIAS;
-    RegionArgs q;
-    memset(&q, 0, sizeof q);
-    q.W_d1 = p.W_d1;
-    q.W_d2 = p.W_d2;
-    q.W1 = p.W1;
-    q.W2 = p.W2;
-    q.W_e1 = p.W_e1;
-    q.W_e2 = p.W_e2;
-    q.b_d1 = p.b_d1;
-    q.b_d2 = p.b_d2;
-    q.b_e1 = p.b_e1;
-    q.b_e2 = p.b_e2;
-    q.alpha = p.alpha;
-    q.gamma = p.gamma;
-    q.beta = p.beta;
-    q.x_embed = x_embed;
-    q.m = m;
-    q.A = A;
-    q.m_next = m_next;
-    q.B = B;
-    q.K = K;
-    q.L = L;
-    q.D = D;
-    q.X = X;
-    q.r = r;
-    char *w = (char *)workspace;
-    float **f32[15] = {&q.su,  &q.sa, &q.d,   &q.cvec, &q.xpart, &q.xbar, &q.sbar, &q.gbar,
-                       &q.p,   &q.sue, &q.se, &q.encv, &q.zhat,  &q.isig, &q.JencT};
-    for (int i = 0; i < 15; ++i)
-        *f32[i] = (float *)(w + plan.off[i]);
-    __bf16 **h16[5] = {&q.P1, &q.JdT, &q.UT, &q.dpT, &q.TT};
-    for (int i = 0; i < 5; ++i)
-        *h16[i] = (__bf16 *)(w + plan.off[15 + i]);
+    const lbi_status st = region_check(params, nullptr, false, x_embed, m, A, m_next, B, K, L, D,
+                                       r, workspace, workspace_bytes, plan.bytes);
+    if (st != LBI_OK || B == 0)
+        return st;
+    const RegionArgs q = region_args(*params, x_embed, m, A, m_next, B, K, L, D, X, r, workspace,
+                                     plan);
     return launch_region_jacobians(q, (hipStream_t)stream) == hipSuccess ? LBI_OK : LBI_ERR_HIP;
+}
+
+size_t lbi_region_jacobians_ssm_workspace_bytes(int64_t B, int64_t K, int64_t L, int32_t D,
+                                                int32_t X, int32_t r)
+{
+    if (!region_sizes_ok(B, K, L, D, X, r) || !ssm_sizes_ok(L, r))
+        return 0;
+    return ssm_plan(B, K, L, D, X, r).bytes;
+}
+
+lbi_status lbi_region_jacobians_ssm(const lbi_region_params *params, const float *decay,
+                                    const void *x_embed, const float *m, float *A, float *m_next,
+                                    int64_t B, int64_t K, int64_t L, int32_t D, int32_t X,
+                                    int32_t r, void *workspace, size_t workspace_bytes,
+                                    lbi_stream_t stream)
+{
+    if (!region_sizes_ok(B, K, L, D, X, r) || !ssm_sizes_ok(L, r))
+        return r > 0 && !supported_r(r) ? LBI_ERR_UNSUPPORTED_R : LBI_ERR_SHAPE;
+    const SsmPlan plan = ssm_plan(B, K, L, D, X, r);
+    const lbi_status st = region_check(params, decay, true, x_embed, m, A, m_next, B, K, L, D, r,
+                                       workspace, workspace_bytes, plan.bytes);
+    if (st != LBI_OK || B == 0)
+        return st;
+    RegionArgs q = region_args(*params, x_embed, m, A, m_next, B, K, L, D, X, r, workspace,
+                               plan.base);
+    char *w = (char *)workspace;
+    q.decay = decay;
+    q.G = plan.G;
+    q.nchunk = plan.nchunk;
+    q.s16 = (__bf16 *)(w + plan.off[0]);
+    q.h16 = (__bf16 *)(w + plan.off[1]);
+    q.S16 = (__bf16 *)(w + plan.off[2]);
+    q.Vt = (__bf16 *)(w + plan.off[3]);
+    q.s32 = (float *)(w + plan.off[4]);
+    q.c32 = (float *)(w + plan.off[5]);
+    q.g32 = (float *)(w + plan.off[6]);
+    q.y32 = (float *)(w + plan.off[7]);
+    q.wv = (float *)(w + plan.off[8]);
+    q.Tpart = (float *)(w + plan.off[9]);
+    return launch_region_jacobians_ssm(q, (hipStream_t)stream) == hipSuccess ? LBI_OK
+                                                                             : LBI_ERR_HIP;
 }
 
 lbi_status lbi_matrix_norms(const void *M, int64_t n, int32_t r, lbi_dtype dt, float *spec,

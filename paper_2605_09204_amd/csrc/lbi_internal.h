@@ -164,9 +164,22 @@ struct RegionArgs {
     float *su, *sa, *d, *cvec, *xpart, *xbar, *sbar, *gbar, *p, *sue, *se, *encv, *zhat, *isig,
         *JencT;
     __bf16 *P1, *JdT, *UT, *dpT, *TT;
+    // the token-mixing block: per-channel decay [K][D]; (sequence, region)
+    // pairs p = k B + b taken G at a time, each with its states s (bf16 and
+    // fp32) and the constant-input states c [L][D], silu / silu' of W1 s
+    // [L][X], y = W2 silu(W1 s) [L][D], the tangent operand S [L r][D], the
+    // scaled first tangent product Vt [L r][X], the partial sums of the
+    // second over nchunk token chunks [nchunk][r][D], and w [D]
+    const float *decay;
+    int64_t G;
+    int32_t nchunk;
+    __bf16 *s16, *h16, *S16, *Vt;
+    float *s32, *c32, *g32, *y32, *Tpart, *wv;
 };
 
 hipError_t launch_region_jacobians(const RegionArgs &q, hipStream_t stream);
+// The same construction for the token-mixing block (q.decay set).
+hipError_t launch_region_jacobians_ssm(const RegionArgs &q, hipStream_t stream);
 
 // Spectral norm and Frobenius norm / sqrt(r) of n r x r matrices (either
 // output may be NULL).

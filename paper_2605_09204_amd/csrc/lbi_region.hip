@@ -510,6 +510,12 @@ struct GemmOp {
     int grp_shift;  // rows per scale row: 2^grp_shift (1, or the interface width)
     const __bf16 *add;  // NULL: 0 (ld ldc, batch stride sC)
     bool out_bf16;
+    // B's batch index is (bz0 + z) / bdiv (bdiv 0: z), so that a batch of
+    // (sequence, region) pairs ordered region-major takes its region's weights
+    int64_t bz0 = 0, bdiv = 0;
+    // act: C = silu(v) (bf16) and C2 = silu'(v) (fp32, same index) in place of v
+    bool act = false;
+    float *C2 = nullptr;
 };
 
 __global__ __launch_bounds__(kT) void gemm_nt_kernel(GemmOp g)
@@ -519,7 +525,7 @@ __global__ __launch_bounds__(kT) void gemm_nt_kernel(GemmOp g)
     const int64_t z = blockIdx.z;
     const int64_t m0 = (int64_t)blockIdx.y * BM, n0 = (int64_t)blockIdx.x * BN;
     const __bf16 *A = g.A + z * g.sA;
-    const __bf16 *B = g.B + z * g.sB;
+    const __bf16 *B = g.B + (g.bdiv ? (g.bz0 + z) / g.bdiv : z) * g.sB;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wm = w >> 1, wn = w & 1;
     f4 acc[4][4];
 #pragma unroll
@@ -582,10 +588,14 @@ __global__ __launch_bounds__(kT) void gemm_nt_kernel(GemmOp g)
                 const int64_t o = z * g.sC + row * g.ldc + col;
                 if (g.add)
                     val += (float)g.add[o];
-                if (g.out_bf16)
+                if (g.act) {
+                    ((__bf16 *)g.C)[o] = (__bf16)silu(val);
+                    g.C2[o] = dsilu(val);
+                } else if (g.out_bf16) {
                     ((__bf16 *)g.C)[o] = (__bf16)val;
-                else
+                } else {
                     ((float *)g.C)[o] = val;
+                }
             }
         }
 }
@@ -624,6 +634,270 @@ __global__ __launch_bounds__(kT) void ln_jac_kernel(RegionArgs q)
         const float v = (i == j ? 1.0f : 0.0f) + alpha * JT[idx];
         A[idx] = q.gamma[k * r + i] * is * (v - cm[j] - zh[i] * cd[j]);
     }
+}
+
+
+// ==== the token-mixing block ======================================================
+// Phi_k(x)_l = x_l + (W2 silu(W1 s_l)) silu(s_l) with the causal recurrence
+// s_l = a_k s_{l-1} + (1 - a_k) x_l over the tokens (s_0 = 0).  The tangent of
+// all r directions goes through every token: with Jdec (D x r) the same for
+// each token, the state's tangent is c_l Jdec, c_l = 1 - a^l (the state of a
+// constant input), and
+//   dp = Jdec (1 + w) + (1/L) sum_l diag(silu(s_l)) W2 diag(silu'(W1 s_l)) W1 (c_l Jdec),
+//   w  = mean_l y_l silu'(s_l) c_l,   y_l = W2 silu(W1 s_l),
+// two products of r times the size of the forward's token products per
+// sequence and region (Eq. "jacobian-work"), which nothing here shortcuts.
+
+constexpr int kSsmChunks = 8;  // token chunks per channel in the recurrence kernels
+
+// ---- ssm_fwd: s (bf16, fp32) and c for 64 channels of one pair -------------------
+// Thread (channel cc, chunk ch) runs its chunk of tokens from a zero state,
+// then again from the state the chunks before it leave (a chunk of n tokens
+// maps a state S to a^n S + its zero-start end state).
+__global__ __launch_bounds__(64 * kSsmChunks) void ssm_fwd_kernel(RegionArgs q, int64_t p0)
+{
+    __shared__ float endS[kSsmChunks][64], endP[kSsmChunks][64];
+    const int64_t z = blockIdx.y, pr = p0 + z, k = pr / q.B, b = pr % q.B;
+    const int cc = threadIdx.x & 63, ch = threadIdx.x >> 6;
+    const int dch = blockIdx.x * 64 + cc;  // D is a multiple of 64
+    const int D = q.D;
+    const int64_t L = q.L;
+    const float a = q.decay[k * D + dch];
+    const float ia = 1.0f - a;
+    const float dv = q.d[(b * q.K + k) * D + dch];
+    const int64_t per = (L + kSsmChunks - 1) / kSsmChunks;
+    const int64_t l0 = ch * per < L ? ch * per : L;
+    const int64_t l1 = l0 + per < L ? l0 + per : L;
+    const __bf16 *x = (const __bf16 *)q.x_embed + b * L * D + dch;
+    float st = 0.0f, pw = 1.0f;
+#pragma unroll 8
+    for (int64_t l = l0; l < l1; ++l) {
+        st = a * st + ia * ((float)x[l * D] + dv);
+        pw *= a;
+    }
+    endS[ch][cc] = st;
+    endP[ch][cc] = pw;
+    __syncthreads();
+    float cs = 0.0f, cc1 = 0.0f;  // states entering the chunk: of x, of the constant 1
+    for (int u = 0; u < ch; ++u) {
+        cs = cs * endP[u][cc] + endS[u][cc];
+        cc1 = cc1 * endP[u][cc] + (1.0f - endP[u][cc]);
+    }
+    const int64_t o = z * L * D + dch;
+#pragma unroll 8
+    for (int64_t l = l0; l < l1; ++l) {
+        cs = a * cs + ia * ((float)x[l * D] + dv);
+        cc1 = a * cc1 + ia;
+        q.s16[o + l * D] = (__bf16)cs;
+        q.s32[o + l * D] = cs;
+        q.c32[o + l * D] = cc1;
+    }
+}
+
+// ---- ssm_red: p = mean x_embed + d + mean_l y_l silu(s_l), w = mean_l y_l silu'(s_l) c_l
+__global__ __launch_bounds__(64 * kSsmChunks) void ssm_red_kernel(RegionArgs q, int64_t p0)
+{
+    __shared__ float r1[kSsmChunks][64], r2[kSsmChunks][64];
+    const int64_t z = blockIdx.y, pr = p0 + z, k = pr / q.B, b = pr % q.B;
+    const int cc = threadIdx.x & 63, ch = threadIdx.x >> 6;
+    const int dch = blockIdx.x * 64 + cc;
+    const int D = q.D;
+    const int64_t L = q.L;
+    const int64_t per = (L + kSsmChunks - 1) / kSsmChunks;
+    const int64_t l0 = ch * per < L ? ch * per : L;
+    const int64_t l1 = l0 + per < L ? l0 + per : L;
+    const int64_t o = z * L * D + dch;
+    float u1 = 0.0f, u2 = 0.0f;
+#pragma unroll 8
+    for (int64_t l = l0; l < l1; ++l) {
+        const float y = q.y32[o + l * D], sv = q.s32[o + l * D];
+        u1 = fmaf(y, silu(sv), u1);
+        u2 = fmaf(y * dsilu(sv), q.c32[o + l * D], u2);
+    }
+    r1[ch][cc] = u1;
+    r2[ch][cc] = u2;
+    __syncthreads();
+    if (ch == 0) {
+        float t1 = 0.0f, t2 = 0.0f;
+        for (int u = 0; u < kSsmChunks; ++u) {
+            t1 += r1[u][cc];
+            t2 += r2[u][cc];
+        }
+        const float inv = 1.0f / (float)L;
+        const int64_t bk = b * q.K + k;
+        q.p[bk * D + dch] = q.xbar[b * D + dch] + q.d[bk * D + dch] + t1 * inv;
+        q.wv[z * D + dch] = t2 * inv;
+    }
+}
+
+// ---- sgen: S[z][l r + j][d] = c_l[d] Jdec^T[pair][j][d] (bf16), 8 d per thread ----
+__global__ __launch_bounds__(kT) void sgen_kernel(RegionArgs q, int64_t p0)
+{
+    const int64_t z = blockIdx.y, pr = p0 + z;
+    const int D = q.D, r = q.r;
+    const int64_t n8 = q.L * r * (D / 8);
+    const int64_t i = (int64_t)blockIdx.x * kT + threadIdx.x;
+    if (i >= n8)
+        return;
+    const int64_t row = i / (D / 8);
+    const int d0 = (int)(i % (D / 8)) * 8;
+    const int64_t l = row / r;
+    const int j = (int)(row % r);
+    const bf16x8 jv = *(const bf16x8 *)(q.JdT + (pr * r + j) * D + d0);
+    const float *cp = q.c32 + (z * q.L + l) * D + d0;
+    const f4 c0 = *(const f4 *)cp, c1 = *(const f4 *)(cp + 4);
+    bf16x8 o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        o[e] = (__bf16)(c0[e] * (float)jv[e]);
+        o[4 + e] = (__bf16)(c1[e] * (float)jv[4 + e]);
+    }
+    *(bf16x8 *)(q.S16 + (z * q.L * r + row) * D + d0) = o;
+}
+
+// ---- tok_gemm: Tpart[z][c][j][d] = sum over the tokens l of chunk c of
+//      silu(s_l)[d] (Vt[z] W2[k]^T)[l r + j][d] ------------------------------------
+// One workgroup: 128 columns d and the 128-row tiles of token chunk c (a tile
+// holds 128 / r tokens, so a tile row's j is its row mod r), in the tile
+// pipeline of gemm_nt over consecutive row tiles; each tile's products are weighted by silu(s_l) and
+// summed over the tiles in registers, then over the tile's tokens through LDS.
+struct TokArgs {
+    const __bf16 *Vt;   // [G][L r][X]
+    const __bf16 *W2;   // [K][D][X]
+    const float *s32;   // [G][L][D]
+    float *Tpart;       // [G][nchunk][r][D]
+    int64_t L, p0, Bn;  // pair z is p0 + z, of region (p0 + z) / Bn
+    int X, D, r, rs, nchunk;
+};
+
+__global__ __launch_bounds__(kT) void tok_gemm_kernel(TokArgs a)
+{
+    __shared__ __attribute__((aligned(16))) __bf16 smem[4][TILE];  // sA[2], sB[2]; then [128][128] fp32
+    const int64_t z = blockIdx.z;
+    const int c = blockIdx.y;
+    const int64_t n0 = (int64_t)blockIdx.x * BN;
+    const int64_t k = (a.p0 + z) / a.Bn;
+    const int64_t M = a.L * a.r;
+    const int64_t mtiles = (M + BM - 1) / BM;
+    const int64_t per = (mtiles + a.nchunk - 1) / a.nchunk;
+    const int64_t t0 = (int64_t)c * per < mtiles ? (int64_t)c * per : mtiles;
+    const int64_t t1 = t0 + per < mtiles ? t0 + per : mtiles;
+    const __bf16 *Av = a.Vt + z * M * a.X;
+    const __bf16 *W = a.W2 + k * (int64_t)a.D * a.X;
+    const float *sz = a.s32 + z * a.L * a.D;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wm = w >> 1, wn = w & 1;
+    f4 acc[4][4], run[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+            run[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+        }
+    if (t0 < t1) {
+        __bf16 *sA0 = smem[0], *sA1 = smem[1], *sB0 = smem[2], *sB1 = smem[3];
+        const int nk = a.X / BK;
+        int64_t lt = t0;
+        int lkb = 0;
+        uint32_t voff[4];
+        tile_offsets(voff, a.X);
+        auto load = [&](u4 (&va)[4], u4 (&vb)[4]) {
+            if (lt < t1) {
+                tile_load(va, voff, Av, a.X, lt * BM, M, lkb * BK);
+                tile_load(vb, voff, W, a.X, n0, a.D, lkb * BK);
+            }
+            if (++lkb == nk) {
+                lkb = 0;
+                ++lt;
+            }
+        };
+        // (two stages ahead, as gemm_nt: a third register set would cost the
+        // second workgroup per CU)
+        u4 ra0[4], rb0[4], ra1[4], rb1[4];
+        load(ra0, rb0);
+        tile_store(ra0, sA0);
+        tile_store(rb0, sB0);
+        load(ra0, rb0);
+        load(ra1, rb1);
+        __syncthreads();
+        int64_t t = t0;
+        int kb = 0, cur = 0;
+        auto body = [&](u4 (&va)[4], u4 (&vb)[4]) -> bool {
+            mma_bk(acc, cur ? sA1 : sA0, cur ? sB1 : sB0, wm, wn, lane);
+            if (kb == nk - 1) {
+                // rows of a 16-row block share one token (r >= 16)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int64_t l = (t * BM + wm * 64 + i * 16) >> a.rs;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int64_t col = n0 + wn * 64 + j * 16 + (lane & 15);
+                        const float wt = l < a.L && col < a.D ? silu(sz[l * a.D + col]) : 0.0f;
+#pragma unroll
+                        for (int v = 0; v < 4; ++v)
+                            run[i][j][v] = fmaf(wt, acc[i][j][v], run[i][j][v]);
+                        acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+                    }
+                }
+            }
+            if (++kb == nk) {
+                kb = 0;
+                ++t;
+            }
+            if (t >= t1)
+                return false;
+            tile_store(va, cur ? sA0 : sA1);
+            tile_store(vb, cur ? sB0 : sB1);
+            __syncthreads();
+            cur ^= 1;
+            load(va, vb);
+            return true;
+        };
+        for (;;) {
+            if (!body(ra0, rb0))
+                break;
+            if (!body(ra1, rb1))
+                break;
+        }
+    }
+    // the 128 / r tokens of a tile: rows q r + j of the running sums
+    __syncthreads();
+    float *red = (float *)&smem[0][0];  // [128][128]
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                red[(wm * 64 + i * 16 + 4 * (lane >> 4) + v) * 128 + wn * 64 + j * 16 + (lane & 15)] =
+                    run[i][j][v];
+    __syncthreads();
+    const int nq = 128 >> a.rs;
+    for (int idx = tid; idx < a.r * 128; idx += kT) {
+        const int jr = idx >> 7, cl = idx & 127;
+        float sum = 0.0f;
+        for (int u = 0; u < nq; ++u)
+            sum += red[((u << a.rs) + jr) * 128 + cl];
+        const int64_t col = n0 + cl;
+        if (col < a.D)
+            a.Tpart[((z * a.nchunk + c) * a.r + jr) * (int64_t)a.D + col] = sum;
+    }
+}
+
+// ---- tfin: dp^T[pair][j][d] = Jdec^T (1 + w[d]) + (1/L) sum_c Tpart[z][c][j][d] ----
+__global__ __launch_bounds__(kT) void tfin_kernel(RegionArgs q, int64_t p0)
+{
+    const int64_t z = blockIdx.y, pr = p0 + z;
+    const int D = q.D, r = q.r;
+    const int idx = blockIdx.x * kT + threadIdx.x;
+    if (idx >= r * D)
+        return;
+    const int j = idx / D, dch = idx % D;
+    float t = 0.0f;
+    for (int c = 0; c < q.nchunk; ++c)
+        t += q.Tpart[((z * q.nchunk + c) * r + j) * (int64_t)D + dch];
+    const int64_t o = (pr * r + j) * D + dch;
+    q.dpT[o] = (__bf16)((float)q.JdT[o] * (1.0f + q.wv[z * D + dch]) + t / (float)q.L);
 }
 
 hipError_t gemm(const GemmOp &g, int64_t batch, hipStream_t st)
@@ -727,6 +1001,118 @@ hipError_t launch_region_jacobians(const RegionArgs &q, hipStream_t st)
     if ((e = gemm(g, q.K, st)) != hipSuccess)
         return e;
     // Jenc^T[k] = T'^T W_e2[k]^T                        (B r x r, K = D), fp32
+    g = GemmOp{q.TT, D, Br * D, We2, D, (int64_t)r * D, q.JencT, r, Br * r, Br, r, D,
+               nullptr, 0, 0, 0, nullptr, false};
+    if ((e = gemm(g, q.K, st)) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(ln_jac_kernel, dim3((unsigned)BKn), dim3(kT), (size_t)3 * r * sizeof(float),
+                       st, q);
+    return hipGetLastError();
+}
+
+}  // namespace lbi
+
+namespace lbi {
+
+hipError_t launch_region_jacobians_ssm(const RegionArgs &q, hipStream_t st)
+{
+    const int64_t BKn = q.B * q.K;
+    const int64_t Br = q.B * (int64_t)q.r;
+    const int D = q.D, X = q.X, r = q.r;
+    const int64_t K = q.K, L = q.L;
+    const int rs = r == 16 ? 4 : (r == 32 ? 5 : (r == 64 ? 6 : 7));
+    const __bf16 *Wd2 = (const __bf16 *)q.W_d2, *W1 = (const __bf16 *)q.W1;
+    const __bf16 *W2 = (const __bf16 *)q.W2, *We1 = (const __bf16 *)q.W_e1;
+    const __bf16 *We2 = (const __bf16 *)q.W_e2;
+    hipError_t e;
+    // Dec_k: a = W_d1 m + b_d1 -> silu(a), silu'(a); d = W_d2 silu(a) + b_d2
+    BmvArgs v{};
+    v = BmvArgs{(const __bf16 *)q.W_d1, (int64_t)D * r, q.m, K * r, r, q.b_d1, D, nullptr, 0, 0,
+                nullptr, 0, 0, nullptr, q.su, q.sa, K * D, D, q.B, D, r};
+    if ((e = bmv(v, K, st)) != hipSuccess)
+        return e;
+    v = BmvArgs{(const __bf16 *)q.W_d2, (int64_t)D * D, q.su, K * D, D, q.b_d2, D, nullptr, 0, 0,
+                nullptr, 0, 0, q.d, nullptr, nullptr, K * D, D, q.B, D, D};
+    if ((e = bmv(v, K, st)) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(p1_kernel, dim3((unsigned)BKn, (unsigned)(D / 64)), dim3(kT), 0, st, q);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(xpart_kernel, dim3((unsigned)((L + 63) / 64), (unsigned)q.B), dim3(kT), 0,
+                       st, q);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(xfin_kernel, dim3((unsigned)((D + kT - 1) / kT), (unsigned)q.B), dim3(kT),
+                       0, st, q);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    GemmOp g;
+    // Jdec^T[k] = P1[k] W_d2[k]^T                      (B r x D, K = D)
+    g = GemmOp{q.P1, D, Br * D, Wd2, D, (int64_t)D * D, q.JdT, D, Br * D, Br, D, D,
+               nullptr, 0, 0, 0, nullptr, true};
+    if ((e = gemm(g, q.K, st)) != hipSuccess)
+        return e;
+
+    // the token-mixing block, G (sequence, region) pairs at a time
+    const int64_t Lr = L * r;
+    const int nct = (D + BN - 1) / BN;
+    for (int64_t p0 = 0; p0 < BKn; p0 += q.G) {
+        const int64_t gz = q.G < BKn - p0 ? q.G : BKn - p0;
+        hipLaunchKernelGGL(ssm_fwd_kernel, dim3((unsigned)(D / 64), (unsigned)gz),
+                           dim3(64 * kSsmChunks), 0, st, q, p0);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+        // silu(u), silu'(u) for u = s W1[k]^T              (L x X, K = D)
+        g = GemmOp{q.s16, D, L * D, W1, D, (int64_t)X * D, q.h16, X, L * X, L, X, D,
+                   nullptr, 0, 0, 0, nullptr, true, p0, q.B, true, q.g32};
+        if ((e = gemm(g, gz, st)) != hipSuccess)
+            return e;
+        // y = silu(u) W2[k]^T                               (L x D, K = X), fp32
+        g = GemmOp{q.h16, X, L * X, W2, X, (int64_t)D * X, q.y32, D, L * D, L, D, X,
+                   nullptr, 0, 0, 0, nullptr, false, p0, q.B, false, nullptr};
+        if ((e = gemm(g, gz, st)) != hipSuccess)
+            return e;
+        hipLaunchKernelGGL(ssm_red_kernel, dim3((unsigned)(D / 64), (unsigned)gz),
+                           dim3(64 * kSsmChunks), 0, st, q, p0);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+        const int64_t n8 = Lr * (D / 8);
+        hipLaunchKernelGGL(sgen_kernel, dim3((unsigned)((n8 + kT - 1) / kT), (unsigned)gz),
+                           dim3(kT), 0, st, q, p0);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+        // Vt = (S W1[k]^T) * silu'(u)[l][x]                (L r x X, K = D), bf16
+        g = GemmOp{q.S16, D, Lr * D, W1, D, (int64_t)X * D, q.Vt, X, Lr * X, Lr, X, D,
+                   q.g32, L * X, X, rs, nullptr, true, p0, q.B, false, nullptr};
+        if ((e = gemm(g, gz, st)) != hipSuccess)
+            return e;
+        TokArgs ta{q.Vt, W2, q.s32, q.Tpart, L, p0, q.B, X, D, r, rs, q.nchunk};
+        hipLaunchKernelGGL(tok_gemm_kernel, dim3((unsigned)nct, (unsigned)q.nchunk, (unsigned)gz),
+                           dim3(kT), 0, st, ta);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+        hipLaunchKernelGGL(tfin_kernel, dim3((unsigned)((r * D + kT - 1) / kT), (unsigned)gz),
+                           dim3(kT), 0, st, q, p0);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+    }
+
+    // Enc_k and the LayerNorm, as for the token-wise block
+    v = BmvArgs{(const __bf16 *)q.W_e1, (int64_t)D * D, q.p, K * D, D, q.b_e1, D, nullptr, 0, 0,
+                nullptr, 0, 0, nullptr, q.sue, q.se, K * D, D, q.B, D, D};
+    if ((e = bmv(v, K, st)) != hipSuccess)
+        return e;
+    v = BmvArgs{(const __bf16 *)q.W_e2, (int64_t)r * D, q.sue, K * D, D, q.b_e2, r, nullptr, 0, 0,
+                nullptr, 0, 0, q.encv, nullptr, nullptr, K * r, r, q.B, r, D};
+    if ((e = bmv(v, K, st)) != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(ln_fwd_kernel, dim3((unsigned)BKn), dim3(64), 0, st, q);
+    if ((e = hipGetLastError()) != hipSuccess)
+        return e;
+    g = GemmOp{q.dpT, D, Br * D, We1, D, (int64_t)D * D, q.TT, D, Br * D, Br, D, D,
+               q.se, D, q.K * (int64_t)D, rs, nullptr, true};
+    if ((e = gemm(g, q.K, st)) != hipSuccess)
+        return e;
     g = GemmOp{q.TT, D, Br * D, We2, D, (int64_t)r * D, q.JencT, r, Br * r, Br, r, D,
                nullptr, 0, 0, 0, nullptr, false};
     if ((e = gemm(g, q.K, st)) != hipSuccess)

@@ -34,7 +34,8 @@ def test_header_declares_entry_points():
                             "lbi_scan_suffix_products", "lbi_scan_backward_streaming",
                             "lbi_matrix_norms", "lbi_scan_backward_ragged",
                             "lbi_region_jacobians_workspace_bytes", "lbi_region_jacobians",
-                            "lbi_wait_progress", "lbi_scan_backward_noalloc",
+                            "lbi_region_jacobians_ssm_workspace_bytes",
+                            "lbi_region_jacobians_ssm", "lbi_wait_progress", "lbi_scan_backward_noalloc",
                             "lbi_status_string", "lbi_abi_version"])
 
 
@@ -57,7 +58,7 @@ def test_header_compiles_as_c():
 
 
 def test_version_and_status_strings():
-    assert binding.lbi_abi_version() == 11
+    assert binding.lbi_abi_version() == 12
     assert binding.lbi_status_string(0) == "LBI_OK"
     for code in range(1, 10):
         assert binding.lbi_status_string(code).startswith("LBI_ERR_")
@@ -362,3 +363,36 @@ def test_region_argument_errors():
     assert call(a=XE + 256) == 8                     # A inside x_embed
     assert call(mn=WS + 1024) == 8                   # m_next inside the workspace
     assert call(B=0, xe=None, m=None, a=None) == 0   # B = 0: no-op
+
+
+def test_region_ssm_argument_errors():
+    # the token-mixing block: the token-wise block's checks, a decay pointer,
+    # and L r / 128 row tiles within a launch's y
+    f = binding.load().lbi_region_jacobians_ssm
+    wsb = binding.lbi_region_jacobians_ssm_workspace_bytes
+    paper = wsb(8, 16, 2048, 768, 3072, 64)
+    # past the token-wise block's workspace: a group of pairs' tangent products
+    assert paper > binding.lbi_region_jacobians_workspace_bytes(8, 16, 2048, 768, 3072, 64)
+    assert paper < (8 << 30)
+    assert wsb(8, 16, 2048, 760, 3072, 64) == 0
+    assert wsb(1, 1, 65535 * 128 // 64 + 1, 64, 128, 64) == 0   # L r / 128 past 65535
+    assert wsb(1, 1, 65535 * 128 // 64, 64, 128, 64) > 0
+    base = 0x10000000
+    good = binding.RegionParams(*[base + 0x01000000 * i for i in range(13)])
+    DEC, XE, M, A, MN, WS = 0x2f000000, 0x30000000, 0x31000000, 0x32000000, 0x33000000, 0x40000000
+    need = wsb(2, 3, 256, 128, 256, 32)
+    assert need > 0
+
+    def call(params=good, dec=DEC, xe=XE, m=M, a=A, mn=MN, B=2, K=3, L=256, D=128, X=256, r=32,
+             ws=WS, nws=None):
+        return f(ctypes.byref(params) if params is not None else None, dec, xe, m, a, mn, B, K,
+                 L, D, X, r, ws, need if nws is None else nws, None)
+
+    assert call(r=48) == 4
+    assert call(D=100) == 2 and call(L=0) == 2
+    assert call(L=65535 * 128 // 32 + 1) == 2
+    assert call(params=None) == 1 and call(dec=None) == 1
+    assert call(dec=DEC + 4) == 7                    # misaligned decay
+    assert call(ws=None) == 5 and call(nws=need - 1) == 5
+    assert call(a=DEC) == 8                          # A over the decay vectors
+    assert call(B=0, dec=None, xe=None, m=None, a=None) == 0
