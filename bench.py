@@ -309,6 +309,18 @@ def region_flops(wl) -> float:
     return tok + tan
 
 
+def region_ssm_flops(wl) -> float:
+    """Matrix-core flops of one Phase 1 call with the token-mixing block: per
+    sequence and region the forward's two token products (L x D x X each) and
+    the tangent's two per-token products over the r directions (L r x D x X
+    each), plus the products with N = B r per region (Jdec: D x D, W_e1:
+    D x D, W_e2: r x D)."""
+    tok = 4.0 * wl.B * wl.K * wl.L * wl.D * wl.X
+    tan = 4.0 * wl.B * wl.K * wl.L * wl.r * wl.D * wl.X
+    small = 2.0 * wl.K * wl.B * wl.r * (2 * wl.D * wl.D + wl.r * wl.D)
+    return tok + tan + small
+
+
 def bench_phase1(args) -> int:
     import torch
     from paper_2605_09204_amd import binding, synth
@@ -319,13 +331,16 @@ def bench_phase1(args) -> int:
     dev = torch.device("cuda:0")
     print(f"[bench] generating {wl.name}", file=sys.stderr, flush=True)
     x = synth.generate_region(wl, device=dev)
-    need = binding.lbi_region_jacobians_workspace_bytes(wl.B, wl.K, wl.L, wl.D, wl.X, wl.r)
+    ssm = args.phi == "ssm"
+    need = (binding.lbi_region_jacobians_ssm_workspace_bytes if ssm else
+            binding.lbi_region_jacobians_workspace_bytes)(wl.B, wl.K, wl.L, wl.D, wl.X, wl.r)
     ws = torch.empty((need,), dtype=torch.uint8, device=dev)
     A = torch.empty((wl.B, wl.K, wl.r, wl.r), dtype=torch.float32, device=dev)
     mn = torch.empty((wl.B, wl.K, wl.r), dtype=torch.float32, device=dev)
+    call = binding.lbi_region_jacobians_ssm if ssm else binding.lbi_region_jacobians
 
     def step(i):
-        binding.lbi_region_jacobians(x.params, x.x_embed, x.m, A=A, m_next=mn, workspace=ws)
+        call(x.params, x.x_embed, x.m, A=A, m_next=mn, workspace=ws)
 
     warm_up(step, args, torch)
     stream = torch.cuda.current_stream(dev)
@@ -339,10 +354,11 @@ def bench_phase1(args) -> int:
     per = [a.elapsed_time(b) for a, b in zip(starts, ends)]
     total_ms = starts[0].elapsed_time(ends[-1])
     avg_s = sum(per) / len(per) / 1e3
-    f = region_flops(wl)
+    f = region_ssm_flops(wl) if ssm else region_flops(wl)
     ach = f / avg_s / 1e12
     out = {
-        "metric": "interface Jacobians/sec (Phase 1, synthetic region map)",
+        "metric": "interface Jacobians/sec (Phase 1, synthetic region map"
+                  + (", token-mixing block)" if ssm else ")"),
         "value": wl.B * wl.K * args.steps / (total_ms / 1e3),
         "unit": "jacobians/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -351,7 +367,7 @@ def bench_phase1(args) -> int:
         "data": "synthetic (seeded random region weights, x_embed and interface states; "
                 "no dataset or checkpoint)",
         "config": {"workload": wl.name, "B": wl.B, "K": wl.K, "L": wl.L, "D": wl.D, "X": wl.X,
-                   "r": wl.r, "op": "phase1", "parallelism": "1 GPU"},
+                   "r": wl.r, "op": "phase1", "phi": args.phi, "parallelism": "1 GPU"},
         "roofline": {"bound": "mfma", "achieved": ach, "peak": PEAK["mfma_bf16_tflops"],
                      "unit": "TFLOP/s", "frac": ach / PEAK["mfma_bf16_tflops"],
                      "traffic": None},
@@ -532,6 +548,9 @@ def main(argv=None) -> int:
                          "reported in matrices/s), or Phase 1, the interface Jacobians of "
                          "every region (lbi_region_jacobians; --workload region_paper or "
                          "region_small)")
+    ap.add_argument("--phi", choices=["mlp", "ssm"], default="mlp",
+                    help="phase1: the region block, token-wise MLP (lbi_region_jacobians) or "
+                         "token-mixing recurrence with a gated MLP (lbi_region_jacobians_ssm)")
     ap.add_argument("--chunk", type=int, default=16, help="streaming: slots per publication")
     ap.add_argument("--layout", choices=["padded", "compact"], default="padded",
                     help="adjoints: R x R tiles with the widths hint (lbi_scan_backward_ex), or "

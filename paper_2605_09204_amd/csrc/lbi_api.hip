@@ -594,11 +594,12 @@ RegionPlan region_plan(int64_t B, int64_t K, int64_t L, int32_t D, int32_t X, in
 }
 
 // The token-mixing block adds, for G (sequence, region) pairs at a time: s16,
-// h16, S16, Vt (bf16), s32, c32, g32, y32, wv, Tpart (fp32), after the parts
-// above.  G is what fits kSsmGroupBytes (at least 1); the second tangent
-// product splits each pair's token tiles into nchunk chunks, enough for about
-// 1024 workgroups per group.
-constexpr int kSsmParts = 10;
+// h16, Vt (bf16), s32, c32, g32, y32, wv, Tpart (fp32), after the parts above.
+// G is what fits kSsmGroupBytes (at least 1, and few enough for a 1-D grid of
+// the first tangent product's tiles); the second tangent product splits each
+// pair's token tiles into nchunk chunks, enough for about 1024 workgroups per
+// group.
+constexpr int kSsmParts = 9;
 constexpr size_t kSsmGroupBytes = (size_t)6 << 30;
 
 struct SsmPlan {
@@ -615,15 +616,18 @@ SsmPlan ssm_plan(int64_t B, int64_t K, int64_t L, int32_t D, int32_t X, int32_t 
     p.base = region_plan(B, K, L, D, X, r);
     const size_t LD = (size_t)L * D, LX = (size_t)L * X, Lr = (size_t)L * r;
     const size_t mtiles = (Lr + 127) / 128, nct = (size_t)(D + 127) / 128;
-    const size_t pair = align256(LD * 2) + align256(LX * 2) + align256(Lr * D * 2) +
-                        align256(Lr * X * 2) + 3 * align256(LD * 4) + align256(LX * 4) +
-                        align256((size_t)D * 4) + align256(mtiles * r * D * 4);
+    const size_t pair = align256(LD * 2) + align256(LX * 2) + align256(Lr * X * 2) +
+                        3 * align256(LD * 4) + align256(LX * 4) + align256((size_t)D * 4) +
+                        align256(mtiles * r * D * 4);
     int64_t G = (int64_t)(kSsmGroupBytes / pair);
     const int64_t BK = B * K;
+    const int64_t tiles = (int64_t)(mtiles * ((size_t)(X + 127) / 128));
     if (G > BK)
         G = BK;
     if (G > 65535)
         G = 65535;
+    if (G > (((int64_t)1 << 31) - 1) / tiles)
+        G = (((int64_t)1 << 31) - 1) / tiles;
     if (G < 1)
         G = 1;
     size_t nch = (1024 + (size_t)G * nct - 1) / ((size_t)G * nct);
@@ -634,9 +638,9 @@ SsmPlan ssm_plan(int64_t B, int64_t K, int64_t L, int32_t D, int32_t X, int32_t 
     p.G = G;
     p.nchunk = (int32_t)nch;
     const size_t g = (size_t)G;
-    const size_t n[kSsmParts] = {g * LD * 2, g * LX * 2, g * Lr * D * 2, g * Lr * X * 2,
-                                 g * LD * 4, g * LD * 4, g * LX * 4, g * LD * 4,
-                                 g * D * 4, g * nch * r * D * 4};
+    const size_t n[kSsmParts] = {g * LD * 2, g * LX * 2, g * Lr * X * 2, g * LD * 4,
+                                 g * LD * 4, g * LX * 4, g * LD * 4, g * D * 4,
+                                 g * nch * r * D * 4};
     size_t o = p.base.bytes;
     for (int i = 0; i < kSsmParts; ++i) {
         p.off[i] = o;
@@ -966,14 +970,13 @@ lbi_status lbi_region_jacobians_ssm(const lbi_region_params *params, const float
     q.nchunk = plan.nchunk;
     q.s16 = (__bf16 *)(w + plan.off[0]);
     q.h16 = (__bf16 *)(w + plan.off[1]);
-    q.S16 = (__bf16 *)(w + plan.off[2]);
-    q.Vt = (__bf16 *)(w + plan.off[3]);
-    q.s32 = (float *)(w + plan.off[4]);
-    q.c32 = (float *)(w + plan.off[5]);
-    q.g32 = (float *)(w + plan.off[6]);
-    q.y32 = (float *)(w + plan.off[7]);
-    q.wv = (float *)(w + plan.off[8]);
-    q.Tpart = (float *)(w + plan.off[9]);
+    q.Vt = (__bf16 *)(w + plan.off[2]);
+    q.s32 = (float *)(w + plan.off[3]);
+    q.c32 = (float *)(w + plan.off[4]);
+    q.g32 = (float *)(w + plan.off[5]);
+    q.y32 = (float *)(w + plan.off[6]);
+    q.wv = (float *)(w + plan.off[7]);
+    q.Tpart = (float *)(w + plan.off[8]);
     return launch_region_jacobians_ssm(q, (hipStream_t)stream) == hipSuccess ? LBI_OK
                                                                              : LBI_ERR_HIP;
 }

@@ -167,13 +167,13 @@ struct RegionArgs {
     // the token-mixing block: per-channel decay [K][D]; (sequence, region)
     // pairs p = k B + b taken G at a time, each with its states s (bf16 and
     // fp32) and the constant-input states c [L][D], silu / silu' of W1 s
-    // [L][X], y = W2 silu(W1 s) [L][D], the tangent operand S [L r][D], the
-    // scaled first tangent product Vt [L r][X], the partial sums of the
-    // second over nchunk token chunks [nchunk][r][D], and w [D]
+    // [L][X], y = W2 silu(W1 s) [L][D], the scaled first tangent product Vt
+    // [L r][X], the partial sums of the second over nchunk token chunks
+    // [nchunk][r][D], and w [D]
     const float *decay;
     int64_t G;
     int32_t nchunk;
-    __bf16 *s16, *h16, *S16, *Vt;
+    __bf16 *s16, *h16, *Vt;
     float *s32, *c32, *g32, *y32, *Tpart, *wv;
 };
 

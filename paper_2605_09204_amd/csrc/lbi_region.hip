@@ -730,29 +730,148 @@ __global__ __launch_bounds__(64 * kSsmChunks) void ssm_red_kernel(RegionArgs q, 
     }
 }
 
-// ---- sgen: S[z][l r + j][d] = c_l[d] Jdec^T[pair][j][d] (bf16), 8 d per thread ----
-__global__ __launch_bounds__(kT) void sgen_kernel(RegionArgs q, int64_t p0)
+// Workgroup order of the two big tangent products: workgroup i runs on XCD
+// i % 8, so logical tile lg = (i % 8) (n / 8) + i / 8 gives each XCD a
+// contiguous range of logical tiles, whose column tiles (fastest) then share
+// their row tile's operand in that XCD's L2.
+__device__ __forceinline__ int64_t xcd_order(int64_t i, int64_t n)
 {
-    const int64_t z = blockIdx.y, pr = p0 + z;
-    const int D = q.D, r = q.r;
-    const int64_t n8 = q.L * r * (D / 8);
-    const int64_t i = (int64_t)blockIdx.x * kT + threadIdx.x;
-    if (i >= n8)
-        return;
-    const int64_t row = i / (D / 8);
-    const int d0 = (int)(i % (D / 8)) * 8;
-    const int64_t l = row / r;
-    const int j = (int)(row % r);
-    const bf16x8 jv = *(const bf16x8 *)(q.JdT + (pr * r + j) * D + d0);
-    const float *cp = q.c32 + (z * q.L + l) * D + d0;
-    const f4 c0 = *(const f4 *)cp, c1 = *(const f4 *)(cp + 4);
-    bf16x8 o;
+    return n % 8 == 0 ? (i % 8) * (n / 8) + i / 8 : i;
+}
+
+// ---- gen_gemm: Vt[z] = (S W1[k]^T) * silu'(u)[l][x], the first tangent product,
+//      with S[l r + j][d] = c_l[d] Jdec^T[pair][j][d] formed as its tiles load
+//      (S is never stored) ---------------------------------------------------------
+struct GenArgs {
+    const __bf16 *JdT;  // [K B r][D]: the pair's rows from (p0 + z) r
+    const float *c32;   // [G][L][D]
+    const __bf16 *W1;   // [K][X][D]
+    const float *g32;   // [G][L][X]
+    __bf16 *Vt;         // [G][L r][X]
+    int64_t L, p0, Bn;
+    int D, X, r, rs;
+    int64_t ntn, ntm;   // column and row tiles
+};
+
+__global__ __launch_bounds__(kT) void gen_gemm_kernel(GenArgs a)
+{
+    __shared__ __attribute__((aligned(16))) __bf16 sA[2][TILE];
+    __shared__ __attribute__((aligned(16))) __bf16 sB[2][TILE];
+    const int64_t lg = xcd_order(blockIdx.x, (int64_t)gridDim.x);
+    const int64_t nt = lg % a.ntn, mt = (lg / a.ntn) % a.ntm, z = lg / (a.ntn * a.ntm);
+    const int64_t m0 = mt * BM, n0 = nt * BN;
+    const int64_t pr = a.p0 + z, k = pr / a.Bn;
+    const int64_t M = a.L * a.r;
+    const int D = a.D;
+    const __bf16 *W = a.W1 + k * (int64_t)a.X * D;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wm = w >> 1, wn = w & 1;
+    // this thread's four 8-column chunks of the A tile (row c / 8, chunk c % 8)
+    // as byte offsets into the pair's Jdec^T rows and into c of the tile's
+    // tokens l0 ..; the resource of c ends with the last token, so rows past
+    // L r read c = 0
+    const int64_t l0 = m0 >> a.rs;
+    const int64_t ltile = (BM >> a.rs) > 0 ? (BM >> a.rs) : 1;
+    const int64_t nl = a.L - l0 < ltile ? a.L - l0 : ltile;
+    const __amdgpu_buffer_rsrc_t rsJ = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(a.JdT + pr * a.r * D), 0, a.r * D * 2, kBufferWord3);
+    const __amdgpu_buffer_rsrc_t rsC = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(a.c32 + (z * a.L + l0) * D), 0, (int)(nl * D * 4), kBufferWord3);
+    uint32_t joff[4], coff[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        o[e] = (__bf16)(c0[e] * (float)jv[e]);
-        o[4 + e] = (__bf16)(c1[e] * (float)jv[4 + e]);
+    for (int i = 0; i < 4; ++i) {
+        // (the tile's first row m0 is a multiple of 128, so of r: the local
+        // row gives j and the token relative to l0)
+        const int c = tid + kT * i;
+        const int row = c >> 3;
+        joff[i] = (uint32_t)(((row & (a.r - 1)) * D + (c & 7) * 8) * 2);
+        coff[i] = (uint32_t)(((row >> a.rs) * D + (c & 7) * 8) * 4);
     }
-    *(bf16x8 *)(q.S16 + (z * q.L * r + row) * D + d0) = o;
+    f4 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    const int nk = D / BK;
+    int lkb = 0;
+    uint32_t vob[4];
+    tile_offsets(vob, D);
+    struct Raw {
+        u4 j[4];
+        f4 c[4][2];
+        u4 b[4];
+    };
+    auto load = [&](Raw &v) {
+        if (lkb < nk) {
+            const int k0 = lkb * BK;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                v.j[i] = __builtin_bit_cast(
+                    u4, __builtin_amdgcn_raw_buffer_load_b128(rsJ, joff[i] + k0 * 2, 0, 0));
+                v.c[i][0] = __builtin_bit_cast(
+                    f4, __builtin_amdgcn_raw_buffer_load_b128(rsC, coff[i] + k0 * 4, 0, 0));
+                v.c[i][1] = __builtin_bit_cast(
+                    f4, __builtin_amdgcn_raw_buffer_load_b128(rsC, coff[i] + k0 * 4 + 16, 0, 0));
+            }
+            tile_load(v.b, vob, W, D, n0, a.X, k0);
+        }
+        ++lkb;
+    };
+    auto store = [&](const Raw &v, __bf16 *la, __bf16 *lb) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const bf16x8 jv = __builtin_bit_cast(bf16x8, v.j[i]);
+            bf16x8 o;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                o[e] = (__bf16)(v.c[i][0][e] * (float)jv[e]);
+                o[4 + e] = (__bf16)(v.c[i][1][e] * (float)jv[4 + e]);
+            }
+            const int c = tid + kT * i;
+            *(bf16x8 *)(la + lds_off(c >> 3, c & 7)) = o;
+        }
+        tile_store(v.b, lb);
+    };
+    Raw r0, r1;
+    load(r0);
+    store(r0, sA[0], sB[0]);
+    load(r0);
+    load(r1);
+    __syncthreads();
+    int kb = 0, cur = 0;
+    auto body = [&](Raw &v) -> bool {
+        mma_bk(acc, sA[cur], sB[cur], wm, wn, lane);
+        if (++kb == nk)
+            return false;
+        store(v, sA[cur ^ 1], sB[cur ^ 1]);
+        __syncthreads();
+        cur ^= 1;
+        load(v);
+        return true;
+    };
+    for (;;) {
+        if (!body(r0))
+            break;
+        if (!body(r1))
+            break;
+    }
+    const float *gz = a.g32 + z * a.L * a.X;
+    __bf16 *out = a.Vt + z * M * a.X;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int64_t row = m0 + wm * 64 + i * 16 + 4 * (lane >> 4) + v;
+            if (row >= M)
+                continue;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int64_t col = n0 + wn * 64 + j * 16 + (lane & 15);
+                if (col < a.X)
+                    out[row * a.X + col] =
+                        (__bf16)(acc[i][j][v] * gz[(row >> a.rs) * a.X + col]);
+            }
+        }
 }
 
 // ---- tok_gemm: Tpart[z][c][j][d] = sum over the tokens l of chunk c of
@@ -773,9 +892,12 @@ struct TokArgs {
 __global__ __launch_bounds__(kT) void tok_gemm_kernel(TokArgs a)
 {
     __shared__ __attribute__((aligned(16))) __bf16 smem[4][TILE];  // sA[2], sB[2]; then [128][128] fp32
-    const int64_t z = blockIdx.z;
-    const int c = blockIdx.y;
-    const int64_t n0 = (int64_t)blockIdx.x * BN;
+    // (column tiles fastest, then token chunks, then pairs; in XCD order)
+    const int64_t nct = (a.D + BN - 1) / BN;
+    const int64_t lg = xcd_order(blockIdx.x, (int64_t)gridDim.x);
+    const int64_t z = lg / (nct * a.nchunk);
+    const int c = (int)((lg / nct) % a.nchunk);
+    const int64_t n0 = (lg % nct) * BN;
     const int64_t k = (a.p0 + z) / a.Bn;
     const int64_t M = a.L * a.r;
     const int64_t mtiles = (M + BM - 1) / BM;
@@ -1076,19 +1198,15 @@ hipError_t launch_region_jacobians_ssm(const RegionArgs &q, hipStream_t st)
                            dim3(64 * kSsmChunks), 0, st, q, p0);
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
-        const int64_t n8 = Lr * (D / 8);
-        hipLaunchKernelGGL(sgen_kernel, dim3((unsigned)((n8 + kT - 1) / kT), (unsigned)gz),
-                           dim3(kT), 0, st, q, p0);
+        // Vt = (S W1[k]^T) * silu'(u)[l][x]                (L r x X, K = D), bf16
+        const int64_t ntn = (X + BN - 1) / BN, ntm = (Lr + BM - 1) / BM;
+        GenArgs ga{q.JdT, q.c32, W1, q.g32, q.Vt, L, p0, q.B, D, X, r, rs, ntn, ntm};
+        hipLaunchKernelGGL(gen_gemm_kernel, dim3((unsigned)(ntn * ntm * gz)), dim3(kT), 0, st, ga);
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
-        // Vt = (S W1[k]^T) * silu'(u)[l][x]                (L r x X, K = D), bf16
-        g = GemmOp{q.S16, D, Lr * D, W1, D, (int64_t)X * D, q.Vt, X, Lr * X, Lr, X, D,
-                   q.g32, L * X, X, rs, nullptr, true, p0, q.B, false, nullptr};
-        if ((e = gemm(g, gz, st)) != hipSuccess)
-            return e;
         TokArgs ta{q.Vt, W2, q.s32, q.Tpart, L, p0, q.B, X, D, r, rs, q.nchunk};
-        hipLaunchKernelGGL(tok_gemm_kernel, dim3((unsigned)nct, (unsigned)q.nchunk, (unsigned)gz),
-                           dim3(kT), 0, st, ta);
+        hipLaunchKernelGGL(tok_gemm_kernel, dim3((unsigned)(nct * q.nchunk * gz)), dim3(kT), 0,
+                           st, ta);
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
         hipLaunchKernelGGL(tfin_kernel, dim3((unsigned)((r * D + kT - 1) / kT), (unsigned)gz),
