@@ -597,8 +597,7 @@ RegionPlan region_plan(int64_t B, int64_t K, int64_t L, int32_t D, int32_t X, in
 // h16, Vt (bf16), s32, c32, g32, y32, wv, Tpart (fp32), after the parts above.
 // G is what fits kSsmGroupBytes (at least 1, and few enough for a 1-D grid of
 // the first tangent product's tiles); the second tangent product splits each
-// pair's token tiles into nchunk chunks, enough for about 1024 workgroups per
-// group.
+// pair's token tiles into nchunk chunks, at most 1024 workgroups per group.
 constexpr int kSsmParts = 9;
 constexpr size_t kSsmGroupBytes = (size_t)6 << 30;
 
@@ -630,7 +629,9 @@ SsmPlan ssm_plan(int64_t B, int64_t K, int64_t L, int32_t D, int32_t X, int32_t 
         G = (((int64_t)1 << 31) - 1) / tiles;
     if (G < 1)
         G = 1;
-    size_t nch = (1024 + (size_t)G * nct - 1) / ((size_t)G * nct);
+    // (at most 1024 workgroups: two full rounds of two per CU, no third
+    // round for a few)
+    size_t nch = 1024 / ((size_t)G * nct);
     if (nch > mtiles)
         nch = mtiles;
     if (nch < 1)

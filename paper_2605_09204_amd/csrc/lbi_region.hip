@@ -732,8 +732,8 @@ __global__ __launch_bounds__(64 * kSsmChunks) void ssm_red_kernel(RegionArgs q, 
 
 // Workgroup order of the two big tangent products: workgroup i runs on XCD
 // i % 8, so logical tile lg = (i % 8) (n / 8) + i / 8 gives each XCD a
-// contiguous range of logical tiles, whose column tiles (fastest) then share
-// their row tile's operand in that XCD's L2.
+// contiguous range of logical tiles, which then share an operand in that
+// XCD's L2.
 __device__ __forceinline__ int64_t xcd_order(int64_t i, int64_t n)
 {
     return n % 8 == 0 ? (i % 8) * (n / 8) + i / 8 : i;
@@ -742,6 +742,9 @@ __device__ __forceinline__ int64_t xcd_order(int64_t i, int64_t n)
 // ---- gen_gemm: Vt[z] = (S W1[k]^T) * silu'(u)[l][x], the first tangent product,
 //      with S[l r + j][d] = c_l[d] Jdec^T[pair][j][d] formed as its tiles load
 //      (S is never stored) ---------------------------------------------------------
+// One workgroup: one 128-column tile of X and a chunk of consecutive 128-row
+// tiles, in one pipeline over (row tile, k block) as tok_gemm; each row tile's
+// epilogue scales and stores it while the next tile's products run.
 struct GenArgs {
     const __bf16 *JdT;  // [K B r][D]: the pair's rows from (p0 + z) r
     const float *c32;   // [G][L][D]
@@ -751,41 +754,55 @@ struct GenArgs {
     int64_t L, p0, Bn;
     int D, X, r, rs;
     int64_t ntn, ntm;   // column and row tiles
+    int mchunk;         // row-tile chunks per (pair, column tile)
 };
 
+// (RS = log2 r: a thread's four A chunks are rows x + 32 i of the tile, x =
+// tid / 8 < 32, so they span 128 >> RS tokens at most and their rows within
+// the interface repeat; each distinct token's c and row's Jdec^T is loaded
+// once)
+template <int RS>
 __global__ __launch_bounds__(kT) void gen_gemm_kernel(GenArgs a)
 {
+    constexpr int NJ = RS == 7 ? 4 : (RS == 6 ? 2 : 1);  // distinct rows j
+    constexpr int NT = RS == 7 ? 1 : (RS == 6 ? 2 : 4);  // distinct tokens
+    // chunk i's row and token among them
+    auto ji = [](int i) { return RS == 7 ? i : (RS == 6 ? (i & 1) : 0); };
+    auto ti = [](int i) { return RS == 7 ? 0 : (RS == 6 ? (i >> 1) : i); };
     __shared__ __attribute__((aligned(16))) __bf16 sA[2][TILE];
     __shared__ __attribute__((aligned(16))) __bf16 sB[2][TILE];
+    // (row-tile chunks fastest, then column tiles, then pairs, in XCD order:
+    // an XCD's workgroups share W1's column tile and the pair's Jdec^T and c)
     const int64_t lg = xcd_order(blockIdx.x, (int64_t)gridDim.x);
-    const int64_t nt = lg % a.ntn, mt = (lg / a.ntn) % a.ntm, z = lg / (a.ntn * a.ntm);
-    const int64_t m0 = mt * BM, n0 = nt * BN;
+    const int mc = (int)(lg % a.mchunk);
+    const int64_t nt = (lg / a.mchunk) % a.ntn, z = lg / (a.mchunk * a.ntn);
+    const int64_t per = (a.ntm + a.mchunk - 1) / a.mchunk;
+    const int64_t t0 = (int64_t)mc * per < a.ntm ? (int64_t)mc * per : a.ntm;
+    const int64_t t1 = t0 + per < a.ntm ? t0 + per : a.ntm;
+    if (t0 >= t1)
+        return;
+    const int64_t n0 = nt * BN;
     const int64_t pr = a.p0 + z, k = pr / a.Bn;
     const int64_t M = a.L * a.r;
     const int D = a.D;
     const __bf16 *W = a.W1 + k * (int64_t)a.X * D;
+    const float *gz = a.g32 + z * a.L * a.X;
+    __bf16 *out = a.Vt + z * M * a.X;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wm = w >> 1, wn = w & 1;
-    // this thread's four 8-column chunks of the A tile (row c / 8, chunk c % 8)
+    // this thread's four 8-column chunks of an A tile (row c / 8, chunk c % 8)
     // as byte offsets into the pair's Jdec^T rows and into c of the tile's
-    // tokens l0 ..; the resource of c ends with the last token, so rows past
-    // L r read c = 0
-    const int64_t l0 = m0 >> a.rs;
-    const int64_t ltile = (BM >> a.rs) > 0 ? (BM >> a.rs) : 1;
-    const int64_t nl = a.L - l0 < ltile ? a.L - l0 : ltile;
+    // first token; a tile's first row is a multiple of 128, so of r
     const __amdgpu_buffer_rsrc_t rsJ = __builtin_amdgcn_make_buffer_rsrc(
         (void *)(a.JdT + pr * a.r * D), 0, a.r * D * 2, kBufferWord3);
-    const __amdgpu_buffer_rsrc_t rsC = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)(a.c32 + (z * a.L + l0) * D), 0, (int)(nl * D * 4), kBufferWord3);
-    uint32_t joff[4], coff[4];
+    const int64_t ltile = (BM >> a.rs) > 0 ? (BM >> a.rs) : 1;
+    const int x = tid >> 3, q = tid & 7;
+    uint32_t joff[NJ], coff[NT];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        // (the tile's first row m0 is a multiple of 128, so of r: the local
-        // row gives j and the token relative to l0)
-        const int c = tid + kT * i;
-        const int row = c >> 3;
-        joff[i] = (uint32_t)(((row & (a.r - 1)) * D + (c & 7) * 8) * 2);
-        coff[i] = (uint32_t)(((row >> a.rs) * D + (c & 7) * 8) * 4);
-    }
+    for (int u = 0; u < NJ; ++u)  // rows (x + 32 u) mod r
+        joff[u] = (uint32_t)((((x + 32 * u) & ((1 << RS) - 1)) * D + q * 8) * 2);
+#pragma unroll
+    for (int u = 0; u < NT; ++u)  // tokens (x + 32 i) >> RS of chunks i with ti(i) = u
+        coff[u] = (uint32_t)((((x + 32 * (RS == 6 ? 2 * u : u)) >> RS) * D + q * 8) * 4);
     f4 acc[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -793,39 +810,52 @@ __global__ __launch_bounds__(kT) void gen_gemm_kernel(GenArgs a)
         for (int j = 0; j < 4; ++j)
             acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
     const int nk = D / BK;
+    int64_t lt = t0;
     int lkb = 0;
     uint32_t vob[4];
     tile_offsets(vob, D);
     struct Raw {
-        u4 j[4];
-        f4 c[4][2];
+        u4 j[NJ];
+        f4 c[NT][2];
         u4 b[4];
     };
     auto load = [&](Raw &v) {
-        if (lkb < nk) {
+        if (lt < t1) {
             const int k0 = lkb * BK;
+            // c of the tile's tokens; the resource ends with the last token,
+            // so rows past L r read c = 0
+            const int64_t l0 = (lt * BM) >> RS;
+            const int64_t nl = a.L - l0 < ltile ? a.L - l0 : ltile;
+            const __amdgpu_buffer_rsrc_t rsC = __builtin_amdgcn_make_buffer_rsrc(
+                (void *)(a.c32 + (z * a.L + l0) * D), 0, (int)(nl * D * 4), kBufferWord3);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                v.j[i] = __builtin_bit_cast(
-                    u4, __builtin_amdgcn_raw_buffer_load_b128(rsJ, joff[i] + k0 * 2, 0, 0));
-                v.c[i][0] = __builtin_bit_cast(
-                    f4, __builtin_amdgcn_raw_buffer_load_b128(rsC, coff[i] + k0 * 4, 0, 0));
-                v.c[i][1] = __builtin_bit_cast(
-                    f4, __builtin_amdgcn_raw_buffer_load_b128(rsC, coff[i] + k0 * 4 + 16, 0, 0));
+            for (int u = 0; u < NJ; ++u)
+                v.j[u] = __builtin_bit_cast(
+                    u4, __builtin_amdgcn_raw_buffer_load_b128(rsJ, joff[u] + k0 * 2, 0, 0));
+#pragma unroll
+            for (int u = 0; u < NT; ++u) {
+                v.c[u][0] = __builtin_bit_cast(
+                    f4, __builtin_amdgcn_raw_buffer_load_b128(rsC, coff[u] + k0 * 4, 0, 0));
+                v.c[u][1] = __builtin_bit_cast(
+                    f4, __builtin_amdgcn_raw_buffer_load_b128(rsC, coff[u] + k0 * 4 + 16, 0, 0));
             }
             tile_load(v.b, vob, W, D, n0, a.X, k0);
         }
-        ++lkb;
+        if (++lkb == nk) {
+            lkb = 0;
+            ++lt;
+        }
     };
     auto store = [&](const Raw &v, __bf16 *la, __bf16 *lb) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const bf16x8 jv = __builtin_bit_cast(bf16x8, v.j[i]);
+            const bf16x8 jv = __builtin_bit_cast(bf16x8, v.j[ji(i)]);
+            const f4 c0 = v.c[ti(i)][0], c1 = v.c[ti(i)][1];
             bf16x8 o;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                o[e] = (__bf16)(v.c[i][0][e] * (float)jv[e]);
-                o[4 + e] = (__bf16)(v.c[i][1][e] * (float)jv[4 + e]);
+                o[e] = (__bf16)(c0[e] * (float)jv[e]);
+                o[4 + e] = (__bf16)(c1[e] * (float)jv[4 + e]);
             }
             const int c = tid + kT * i;
             *(bf16x8 *)(la + lds_off(c >> 3, c & 7)) = o;
@@ -838,10 +868,37 @@ __global__ __launch_bounds__(kT) void gen_gemm_kernel(GenArgs a)
     load(r0);
     load(r1);
     __syncthreads();
+    int64_t t = t0;
     int kb = 0, cur = 0;
     auto body = [&](Raw &v) -> bool {
         mma_bk(acc, sA[cur], sB[cur], wm, wn, lane);
-        if (++kb == nk)
+        if (kb == nk - 1) {
+            // epilogue of row tile t: times silu'(u) of the row's token (one
+            // token per 16-row block), bf16
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int64_t rb = t * BM + wm * 64 + i * 16;
+                const int64_t l = rb >> a.rs;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int64_t col = n0 + wn * 64 + j * 16 + (lane & 15);
+                    const bool ok = l < a.L && col < a.X;
+                    const float gs = ok ? gz[l * a.X + col] : 0.0f;
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const int64_t row = rb + 4 * (lane >> 4) + v;
+                        if (ok && row < M)
+                            out[row * a.X + col] = (__bf16)(acc[i][j][v] * gs);
+                    }
+                    acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+                }
+            }
+        }
+        if (++kb == nk) {
+            kb = 0;
+            ++t;
+        }
+        if (t >= t1)
             return false;
         store(v, sA[cur ^ 1], sB[cur ^ 1]);
         __syncthreads();
@@ -855,23 +912,6 @@ __global__ __launch_bounds__(kT) void gen_gemm_kernel(GenArgs a)
         if (!body(r1))
             break;
     }
-    const float *gz = a.g32 + z * a.L * a.X;
-    __bf16 *out = a.Vt + z * M * a.X;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int64_t row = m0 + wm * 64 + i * 16 + 4 * (lane >> 4) + v;
-            if (row >= M)
-                continue;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int64_t col = n0 + wn * 64 + j * 16 + (lane & 15);
-                if (col < a.X)
-                    out[row * a.X + col] =
-                        (__bf16)(acc[i][j][v] * gz[(row >> a.rs) * a.X + col]);
-            }
-        }
 }
 
 // ---- tok_gemm: Tpart[z][c][j][d] = sum over the tokens l of chunk c of
@@ -1200,8 +1240,19 @@ hipError_t launch_region_jacobians_ssm(const RegionArgs &q, hipStream_t st)
             return e;
         // Vt = (S W1[k]^T) * silu'(u)[l][x]                (L r x X, K = D), bf16
         const int64_t ntn = (X + BN - 1) / BN, ntm = (Lr + BM - 1) / BM;
-        GenArgs ga{q.JdT, q.c32, W1, q.g32, q.Vt, L, p0, q.B, D, X, r, rs, ntn, ntm};
-        hipLaunchKernelGGL(gen_gemm_kernel, dim3((unsigned)(ntn * ntm * gz)), dim3(kT), 0, st, ga);
+        // (at most 1024 workgroups: two rounds of two per CU)
+        int64_t mch = 1024 / (ntn * gz);
+        mch = mch < 1 ? 1 : (mch > ntm ? ntm : mch);
+        GenArgs ga{q.JdT, q.c32, W1, q.g32, q.Vt, L, p0, q.B, D, X, r, rs, ntn, ntm, (int)mch};
+        const dim3 ggrid((unsigned)(ntn * mch * gz));
+        if (rs == 4)
+            hipLaunchKernelGGL(gen_gemm_kernel<4>, ggrid, dim3(kT), 0, st, ga);
+        else if (rs == 5)
+            hipLaunchKernelGGL(gen_gemm_kernel<5>, ggrid, dim3(kT), 0, st, ga);
+        else if (rs == 6)
+            hipLaunchKernelGGL(gen_gemm_kernel<6>, ggrid, dim3(kT), 0, st, ga);
+        else
+            hipLaunchKernelGGL(gen_gemm_kernel<7>, ggrid, dim3(kT), 0, st, ga);
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
         TokArgs ta{q.Vt, W2, q.s32, q.Tpart, L, p0, q.B, X, D, r, rs, q.nchunk};
