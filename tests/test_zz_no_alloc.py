@@ -76,6 +76,25 @@ def test_noalloc_without_scratch_use_matches_bit_for_bit():
         assert torch.equal(got, want)
 
 
+@pytest.mark.parametrize("algo", ["ring", "auto"])
+def test_noalloc_ring_kernel_with_widths(algo):
+    # the LDS-ring chain kernel (explicit, and AUTO's choice at width 128 with
+    # these widths: 300 chains keep AUTO on the chain scan) needs no scratch
+    # either: equal bit for bit, with the hint
+    widths = tuple((32, 64, 128)[k % 3] for k in range(10)) + (64,)
+    x = synth.random_chain(300, 10, 128, dtype="bf16", seed=64, widths=widths)
+    a = binding.LBI_ALGO_CHAIN_RING if algo == "ring" else binding.LBI_ALGO_AUTO
+    dev = torch.device("cuda:0")
+    A, b, lk = x.A.to(dev), x.b.to(dev), x.lamK.to(dev)
+    _say(f"[noalloc] B=300 K=10 widths 32/64/128 bf16 {algo}")
+    want = binding.lbi_scan_backward_ex(A, b, lk, list(widths), 0, a)
+    lam = torch.full_like(want, float("nan"))
+    binding.lbi_scan_backward_noalloc(A, b, lk, list(widths), 0, a, lam=lam)
+    torch.cuda.synchronize()
+    assert torch.equal(lam, want)
+    _check(lam, want, x, TOL["bf16"], "ring widths")
+
+
 def test_noalloc_tree_scan_levels_in_the_array():
     """The tree scan over levels of chunk aggregates keeps each level's
     aggregates and carries in the array: equal bit for bit to the workspace
