@@ -21,6 +21,7 @@
 #include <mutex>
 
 #include "lbi_internal.h"
+#include "lbi_region_args.hpp"
 
 // ---- the static scratch array (lbi_scan_backward_noalloc) --------------------
 //

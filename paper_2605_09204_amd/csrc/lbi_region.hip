@@ -45,6 +45,7 @@
 
 #include "lbi_device.hpp"
 #include "lbi_internal.h"
+#include "lbi_region_args.hpp"
 
 namespace lbi {
 namespace {
