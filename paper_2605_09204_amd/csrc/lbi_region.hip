@@ -740,12 +740,12 @@ __device__ __forceinline__ int64_t xcd_order(int64_t i, int64_t n)
     return n % 8 == 0 ? (i % 8) * (n / 8) + i / 8 : i;
 }
 
-// ---- gen_gemm: Vt[z] = (S W1[k]^T) * silu'(u)[l][x], the first tangent product,
-//      with S[l r + j][d] = c_l[d] Jdec^T[pair][j][d] formed as its tiles load
-//      (S is never stored) ---------------------------------------------------------
-// One workgroup: one 128-column tile of X and a chunk of consecutive 128-row
-// tiles, in one pipeline over (row tile, k block) as tok_gemm; each row tile's
-// epilogue scales and stores it while the next tile's products run.
+// ---- the first tangent product: Vt[z] = (S W1[k]^T) * silu'(u)[l][x], with
+//      S[l r + j][d] = c_l[d] Jdec^T[pair][j][d] formed as its tiles load (S is
+//      never stored).  A workgroup holds one column tile of W1 and loops over a
+//      chunk of consecutive row tiles in one pipeline over (row tile, k block);
+//      each row tile's epilogue scales and stores it while the next tile's
+//      products run.
 struct GenArgs {
     const __bf16 *JdT;  // [K B r][D]: the pair's rows from (p0 + z) r
     const float *c32;   // [G][L][D]
@@ -758,22 +758,79 @@ struct GenArgs {
     int mchunk;         // row-tile chunks per (pair, column tile)
 };
 
-// (RS = log2 r: a thread's four A chunks are rows x + 32 i of the tile, x =
-// tid / 8 < 32, so they span 128 >> RS tokens at most and their rows within
-// the interface repeat; each distinct token's c and row's Jdec^T is loaded
-// once)
-template <int RS>
-__global__ __launch_bounds__(kT) void gen_gemm_kernel(GenArgs a)
+// ---- the second tangent product: Tpart[z][c][j][d] = sum over the tokens l of
+//      chunk c of silu(s_l)[d] (Vt[z] W2[k]^T)[l r + j][d] ----------------------------
+// One workgroup: a column tile of D and the 128-row tiles of token chunk c (a
+// tile holds 128 / r tokens, so a tile row's j is its row mod r), in one
+// pipeline over consecutive row tiles; each tile's products are weighted by
+// silu(s_l) and summed over the tiles in registers, then over the tile's
+// tokens through LDS.
+struct TokArgs {
+    const __bf16 *Vt;   // [G][L r][X]
+    const __bf16 *W2;   // [K][D][X]
+    const float *s32;   // [G][L][D]
+    float *Tpart;       // [G][nchunk][r][D]
+    int64_t L, p0, Bn;  // pair z is p0 + z, of region (p0 + z) / Bn
+    int X, D, r, rs, nchunk;
+};
+
+// ==== the tile pipeline of the two tangent products ===============================
+// 128 x 256 output tiles, eight waves of 64 x 64 (2 x 4): each k step brings
+// 48 KB of operands into LDS for 4.2 MFLOP (a 128 x 128 tile: 32 KB for 2.1).
+// 96 KB of LDS: one workgroup (eight waves) per CU.
+constexpr int kTW = 512;   // threads
+constexpr int BNW = 256;   // columns of a tile
+
+// ROWS x 64 k of a row-major bf16 matrix from row0 (rows >= nrows read zero);
+// thread t takes chunks c = t + 512 i: row c / 8, chunk c % 8.
+template <int ROWS> struct WT {
+    static constexpr int CPT = ROWS * 8 / kTW;
+};
+template <int ROWS>
+__device__ __forceinline__ void wtile_offsets(uint32_t (&voff)[WT<ROWS>::CPT], int ld)
 {
-    constexpr int NJ = RS == 7 ? 4 : (RS == 6 ? 2 : 1);  // distinct rows j
-    constexpr int NT = RS == 7 ? 1 : (RS == 6 ? 2 : 4);  // distinct tokens
-    // chunk i's row and token among them
-    auto ji = [](int i) { return RS == 7 ? i : (RS == 6 ? (i & 1) : 0); };
-    auto ti = [](int i) { return RS == 7 ? 0 : (RS == 6 ? (i >> 1) : i); };
-    __shared__ __attribute__((aligned(16))) __bf16 sA[2][TILE];
-    __shared__ __attribute__((aligned(16))) __bf16 sB[2][TILE];
-    // (row-tile chunks fastest, then column tiles, then pairs, in XCD order:
-    // an XCD's workgroups share W1's column tile and the pair's Jdec^T and c)
+#pragma unroll
+    for (int i = 0; i < WT<ROWS>::CPT; ++i) {
+        const int c = threadIdx.x + kTW * i;
+        voff[i] = (uint32_t)(((c >> 3) * ld + (c & 7) * 8) * 2);
+    }
+}
+template <int ROWS>
+__device__ __forceinline__ void wtile_load(u4 (&v)[WT<ROWS>::CPT],
+                                           const uint32_t (&voff)[WT<ROWS>::CPT],
+                                           const __bf16 *base, int64_t ld, int64_t row0,
+                                           int64_t nrows, int k0)
+{
+    const int64_t left = nrows - row0;
+    const int valid = left < ROWS ? (int)left : ROWS;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(base + row0 * ld + k0), 0, (int)(valid * (int)ld * 2 - k0 * 2), kBufferWord3);
+#pragma unroll
+    for (int i = 0; i < WT<ROWS>::CPT; ++i)
+        v[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, voff[i], 0, 0);
+}
+template <int ROWS>
+__device__ __forceinline__ void wtile_store(const u4 (&v)[WT<ROWS>::CPT], __bf16 *s)
+{
+#pragma unroll
+    for (int i = 0; i < WT<ROWS>::CPT; ++i) {
+        const int c = threadIdx.x + kTW * i;
+        *(u4 *)(s + lds_off(c >> 3, c & 7)) = v[i];
+    }
+}
+
+// ---- gen_gemm_w: the first tangent product (GenArgs above) ------------------------
+// (a thread's two A chunks are rows x + 64 i, x = tid / 8 < 64: at RS = 7 two
+// interface rows of one token, below it one row j = x mod r of two tokens)
+template <int RS>
+__global__ __launch_bounds__(kTW) void gen_gemm_w_kernel(GenArgs a)
+{
+    constexpr int NJ = RS == 7 ? 2 : 1;
+    constexpr int NT = RS == 7 ? 1 : 2;
+    __shared__ __attribute__((aligned(16))) __bf16 smem[6 * TILE];
+    // (buffers i of A, 128 x 64, and of B, 256 x 64)
+    auto sA = [&](int i) { return smem + i * TILE; };
+    auto sB = [&](int i) { return smem + (2 + 2 * i) * TILE; };
     const int64_t lg = xcd_order(blockIdx.x, (int64_t)gridDim.x);
     const int mc = (int)(lg % a.mchunk);
     const int64_t nt = (lg / a.mchunk) % a.ntn, z = lg / (a.mchunk * a.ntn);
@@ -782,28 +839,25 @@ __global__ __launch_bounds__(kT) void gen_gemm_kernel(GenArgs a)
     const int64_t t1 = t0 + per < a.ntm ? t0 + per : a.ntm;
     if (t0 >= t1)
         return;
-    const int64_t n0 = nt * BN;
+    const int64_t n0 = nt * BNW;
     const int64_t pr = a.p0 + z, k = pr / a.Bn;
     const int64_t M = a.L * a.r;
     const int D = a.D;
     const __bf16 *W = a.W1 + k * (int64_t)a.X * D;
     const float *gz = a.g32 + z * a.L * a.X;
     __bf16 *out = a.Vt + z * M * a.X;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wm = w >> 1, wn = w & 1;
-    // this thread's four 8-column chunks of an A tile (row c / 8, chunk c % 8)
-    // as byte offsets into the pair's Jdec^T rows and into c of the tile's
-    // first token; a tile's first row is a multiple of 128, so of r
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wm = w >> 2, wn = w & 3;
     const __amdgpu_buffer_rsrc_t rsJ = __builtin_amdgcn_make_buffer_rsrc(
         (void *)(a.JdT + pr * a.r * D), 0, a.r * D * 2, kBufferWord3);
-    const int64_t ltile = (BM >> a.rs) > 0 ? (BM >> a.rs) : 1;
+    const int64_t ltile = (BM >> RS) > 0 ? (BM >> RS) : 1;
     const int x = tid >> 3, q = tid & 7;
     uint32_t joff[NJ], coff[NT];
 #pragma unroll
-    for (int u = 0; u < NJ; ++u)  // rows (x + 32 u) mod r
-        joff[u] = (uint32_t)((((x + 32 * u) & ((1 << RS) - 1)) * D + q * 8) * 2);
+    for (int u = 0; u < NJ; ++u)
+        joff[u] = (uint32_t)((((x + 64 * u) & ((1 << RS) - 1)) * D + q * 8) * 2);
 #pragma unroll
-    for (int u = 0; u < NT; ++u)  // tokens (x + 32 i) >> RS of chunks i with ti(i) = u
-        coff[u] = (uint32_t)((((x + 32 * (RS == 6 ? 2 * u : u)) >> RS) * D + q * 8) * 4);
+    for (int u = 0; u < NT; ++u)
+        coff[u] = (uint32_t)((((x + 64 * u) >> RS) * D + q * 8) * 4);
     f4 acc[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -813,18 +867,16 @@ __global__ __launch_bounds__(kT) void gen_gemm_kernel(GenArgs a)
     const int nk = D / BK;
     int64_t lt = t0;
     int lkb = 0;
-    uint32_t vob[4];
-    tile_offsets(vob, D);
+    uint32_t vob[WT<256>::CPT];
+    wtile_offsets<256>(vob, D);
     struct Raw {
         u4 j[NJ];
         f4 c[NT][2];
-        u4 b[4];
+        u4 b[WT<256>::CPT];
     };
     auto load = [&](Raw &v) {
         if (lt < t1) {
             const int k0 = lkb * BK;
-            // c of the tile's tokens; the resource ends with the last token,
-            // so rows past L r read c = 0
             const int64_t l0 = (lt * BM) >> RS;
             const int64_t nl = a.L - l0 < ltile ? a.L - l0 : ltile;
             const __amdgpu_buffer_rsrc_t rsC = __builtin_amdgcn_make_buffer_rsrc(
@@ -840,7 +892,7 @@ __global__ __launch_bounds__(kT) void gen_gemm_kernel(GenArgs a)
                 v.c[u][1] = __builtin_bit_cast(
                     f4, __builtin_amdgcn_raw_buffer_load_b128(rsC, coff[u] + k0 * 4 + 16, 0, 0));
             }
-            tile_load(v.b, vob, W, D, n0, a.X, k0);
+            wtile_load<256>(v.b, vob, W, D, n0, a.X, k0);
         }
         if (++lkb == nk) {
             lkb = 0;
@@ -849,37 +901,35 @@ __global__ __launch_bounds__(kT) void gen_gemm_kernel(GenArgs a)
     };
     auto store = [&](const Raw &v, __bf16 *la, __bf16 *lb) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const bf16x8 jv = __builtin_bit_cast(bf16x8, v.j[ji(i)]);
-            const f4 c0 = v.c[ti(i)][0], c1 = v.c[ti(i)][1];
+        for (int i = 0; i < 2; ++i) {
+            const bf16x8 jv = __builtin_bit_cast(bf16x8, v.j[RS == 7 ? i : 0]);
+            const f4 c0 = v.c[RS == 7 ? 0 : i][0], c1 = v.c[RS == 7 ? 0 : i][1];
             bf16x8 o;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 o[e] = (__bf16)(c0[e] * (float)jv[e]);
                 o[4 + e] = (__bf16)(c1[e] * (float)jv[4 + e]);
             }
-            const int c = tid + kT * i;
+            const int c = tid + kTW * i;
             *(bf16x8 *)(la + lds_off(c >> 3, c & 7)) = o;
         }
-        tile_store(v.b, lb);
+        wtile_store<256>(v.b, lb);
     };
     Raw r0, r1;
     load(r0);
-    store(r0, sA[0], sB[0]);
+    store(r0, sA(0), sB(0));
     load(r0);
     load(r1);
     __syncthreads();
     int64_t t = t0;
     int kb = 0, cur = 0;
     auto body = [&](Raw &v) -> bool {
-        mma_bk(acc, sA[cur], sB[cur], wm, wn, lane);
+        mma_bk(acc, sA(cur), sB(cur), wm, wn, lane);
         if (kb == nk - 1) {
-            // epilogue of row tile t: times silu'(u) of the row's token (one
-            // token per 16-row block), bf16
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int64_t rb = t * BM + wm * 64 + i * 16;
-                const int64_t l = rb >> a.rs;
+                const int64_t l = rb >> RS;
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     const int64_t col = n0 + wn * 64 + j * 16 + (lane & 15);
@@ -901,7 +951,7 @@ __global__ __launch_bounds__(kT) void gen_gemm_kernel(GenArgs a)
         }
         if (t >= t1)
             return false;
-        store(v, sA[cur ^ 1], sB[cur ^ 1]);
+        store(v, sA(cur ^ 1), sB(cur ^ 1));
         __syncthreads();
         cur ^= 1;
         load(v);
@@ -915,30 +965,18 @@ __global__ __launch_bounds__(kT) void gen_gemm_kernel(GenArgs a)
     }
 }
 
-// ---- tok_gemm: Tpart[z][c][j][d] = sum over the tokens l of chunk c of
-//      silu(s_l)[d] (Vt[z] W2[k]^T)[l r + j][d] ------------------------------------
-// One workgroup: 128 columns d and the 128-row tiles of token chunk c (a tile
-// holds 128 / r tokens, so a tile row's j is its row mod r), in the tile
-// pipeline of gemm_nt over consecutive row tiles; each tile's products are weighted by silu(s_l) and
-// summed over the tiles in registers, then over the tile's tokens through LDS.
-struct TokArgs {
-    const __bf16 *Vt;   // [G][L r][X]
-    const __bf16 *W2;   // [K][D][X]
-    const float *s32;   // [G][L][D]
-    float *Tpart;       // [G][nchunk][r][D]
-    int64_t L, p0, Bn;  // pair z is p0 + z, of region (p0 + z) / Bn
-    int X, D, r, rs, nchunk;
-};
-
-__global__ __launch_bounds__(kT) void tok_gemm_kernel(TokArgs a)
+// ---- tok_gemm_w: the second tangent product (TokArgs above) -----------------------
+__global__ __launch_bounds__(kTW) void tok_gemm_w_kernel(TokArgs a)
 {
-    __shared__ __attribute__((aligned(16))) __bf16 smem[4][TILE];  // sA[2], sB[2]; then [128][128] fp32
-    // (column tiles fastest, then token chunks, then pairs; in XCD order)
-    const int64_t nct = (a.D + BN - 1) / BN;
+    __shared__ __attribute__((aligned(16))) __bf16 smem[6 * TILE];
+    // (buffers i of A, 128 x 64, and of B, 256 x 64)
+    auto sA = [&](int i) { return smem + i * TILE; };
+    auto sB = [&](int i) { return smem + (2 + 2 * i) * TILE; };
+    const int64_t nct = (a.D + BNW - 1) / BNW;
     const int64_t lg = xcd_order(blockIdx.x, (int64_t)gridDim.x);
     const int64_t z = lg / (nct * a.nchunk);
     const int c = (int)((lg / nct) % a.nchunk);
-    const int64_t n0 = (lg % nct) * BN;
+    const int64_t n0 = (lg % nct) * BNW;
     const int64_t k = (a.p0 + z) / a.Bn;
     const int64_t M = a.L * a.r;
     const int64_t mtiles = (M + BM - 1) / BM;
@@ -948,7 +986,7 @@ __global__ __launch_bounds__(kT) void tok_gemm_kernel(TokArgs a)
     const __bf16 *Av = a.Vt + z * M * a.X;
     const __bf16 *W = a.W2 + k * (int64_t)a.D * a.X;
     const float *sz = a.s32 + z * a.L * a.D;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wm = w >> 1, wn = w & 1;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wm = w >> 2, wn = w & 3;
     f4 acc[4][4], run[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -958,37 +996,38 @@ __global__ __launch_bounds__(kT) void tok_gemm_kernel(TokArgs a)
             run[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
         }
     if (t0 < t1) {
-        __bf16 *sA0 = smem[0], *sA1 = smem[1], *sB0 = smem[2], *sB1 = smem[3];
         const int nk = a.X / BK;
         int64_t lt = t0;
         int lkb = 0;
-        uint32_t voff[4];
-        tile_offsets(voff, a.X);
-        auto load = [&](u4 (&va)[4], u4 (&vb)[4]) {
+        uint32_t voa[WT<128>::CPT], vob[WT<256>::CPT];
+        wtile_offsets<128>(voa, a.X);
+        wtile_offsets<256>(vob, a.X);
+        struct Raw {
+            u4 a[WT<128>::CPT];
+            u4 b[WT<256>::CPT];
+        };
+        auto load = [&](Raw &v) {
             if (lt < t1) {
-                tile_load(va, voff, Av, a.X, lt * BM, M, lkb * BK);
-                tile_load(vb, voff, W, a.X, n0, a.D, lkb * BK);
+                wtile_load<128>(v.a, voa, Av, a.X, lt * BM, M, lkb * BK);
+                wtile_load<256>(v.b, vob, W, a.X, n0, a.D, lkb * BK);
             }
             if (++lkb == nk) {
                 lkb = 0;
                 ++lt;
             }
         };
-        // (two stages ahead, as gemm_nt: a third register set would cost the
-        // second workgroup per CU)
-        u4 ra0[4], rb0[4], ra1[4], rb1[4];
-        load(ra0, rb0);
-        tile_store(ra0, sA0);
-        tile_store(rb0, sB0);
-        load(ra0, rb0);
-        load(ra1, rb1);
+        Raw r0, r1;
+        load(r0);
+        wtile_store<128>(r0.a, sA(0));
+        wtile_store<256>(r0.b, sB(0));
+        load(r0);
+        load(r1);
         __syncthreads();
         int64_t t = t0;
         int kb = 0, cur = 0;
-        auto body = [&](u4 (&va)[4], u4 (&vb)[4]) -> bool {
-            mma_bk(acc, cur ? sA1 : sA0, cur ? sB1 : sB0, wm, wn, lane);
+        auto body = [&](Raw &v) -> bool {
+            mma_bk(acc, sA(cur), sB(cur), wm, wn, lane);
             if (kb == nk - 1) {
-                // rows of a 16-row block share one token (r >= 16)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int64_t l = (t * BM + wm * 64 + i * 16) >> a.rs;
@@ -1009,41 +1048,46 @@ __global__ __launch_bounds__(kT) void tok_gemm_kernel(TokArgs a)
             }
             if (t >= t1)
                 return false;
-            tile_store(va, cur ? sA0 : sA1);
-            tile_store(vb, cur ? sB0 : sB1);
+            wtile_store<128>(v.a, sA(cur ^ 1));
+            wtile_store<256>(v.b, sB(cur ^ 1));
             __syncthreads();
             cur ^= 1;
-            load(va, vb);
+            load(v);
             return true;
         };
         for (;;) {
-            if (!body(ra0, rb0))
+            if (!body(r0))
                 break;
-            if (!body(ra1, rb1))
+            if (!body(r1))
                 break;
         }
     }
-    // the 128 / r tokens of a tile: rows q r + j of the running sums
-    __syncthreads();
-    float *red = (float *)&smem[0][0];  // [128][128]
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int v = 0; v < 4; ++v)
-                red[(wm * 64 + i * 16 + 4 * (lane >> 4) + v) * 128 + wn * 64 + j * 16 + (lane & 15)] =
-                    run[i][j][v];
-    __syncthreads();
+    // the 128 / r tokens of a tile, 128 columns at a time through LDS
+    float *red = (float *)smem;  // [128][128]
     const int nq = 128 >> a.rs;
-    for (int idx = tid; idx < a.r * 128; idx += kT) {
-        const int jr = idx >> 7, cl = idx & 127;
-        float sum = 0.0f;
-        for (int u = 0; u < nq; ++u)
-            sum += red[((u << a.rs) + jr) * 128 + cl];
-        const int64_t col = n0 + cl;
-        if (col < a.D)
-            a.Tpart[((z * a.nchunk + c) * a.r + jr) * (int64_t)a.D + col] = sum;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        __syncthreads();
+        if ((wn >> 1) == h) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        red[(wm * 64 + i * 16 + 4 * (lane >> 4) + v) * 128 + (wn & 1) * 64 +
+                            j * 16 + (lane & 15)] = run[i][j][v];
+        }
+        __syncthreads();
+        for (int idx = tid; idx < a.r * 128; idx += kTW) {
+            const int jr = idx >> 7, cl = idx & 127;
+            float sum = 0.0f;
+            for (int u = 0; u < nq; ++u)
+                sum += red[((u << a.rs) + jr) * 128 + cl];
+            const int64_t col = n0 + h * 128 + cl;
+            if (col < a.D)
+                a.Tpart[((z * a.nchunk + c) * a.r + jr) * (int64_t)a.D + col] = sum;
+        }
     }
 }
 
@@ -1218,7 +1262,7 @@ hipError_t launch_region_jacobians_ssm(const RegionArgs &q, hipStream_t st)
 
     // the token-mixing block, G (sequence, region) pairs at a time
     const int64_t Lr = L * r;
-    const int nct = (D + BN - 1) / BN;
+    const int nctw = (D + BNW - 1) / BNW;
     for (int64_t p0 = 0; p0 < BKn; p0 += q.G) {
         const int64_t gz = q.G < BKn - p0 ? q.G : BKn - p0;
         hipLaunchKernelGGL(ssm_fwd_kernel, dim3((unsigned)(D / 64), (unsigned)gz),
@@ -1240,25 +1284,25 @@ hipError_t launch_region_jacobians_ssm(const RegionArgs &q, hipStream_t st)
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
         // Vt = (S W1[k]^T) * silu'(u)[l][x]                (L r x X, K = D), bf16
-        const int64_t ntn = (X + BN - 1) / BN, ntm = (Lr + BM - 1) / BM;
-        // (at most 1024 workgroups: two rounds of two per CU)
-        int64_t mch = 1024 / (ntn * gz);
+        const int64_t ntn = (X + BNW - 1) / BNW, ntm = (Lr + BM - 1) / BM;
+        // (at most 512 workgroups: two rounds of one per CU)
+        int64_t mch = 512 / (ntn * gz);
         mch = mch < 1 ? 1 : (mch > ntm ? ntm : mch);
         GenArgs ga{q.JdT, q.c32, W1, q.g32, q.Vt, L, p0, q.B, D, X, r, rs, ntn, ntm, (int)mch};
         const dim3 ggrid((unsigned)(ntn * mch * gz));
         if (rs == 4)
-            hipLaunchKernelGGL(gen_gemm_kernel<4>, ggrid, dim3(kT), 0, st, ga);
+            hipLaunchKernelGGL(gen_gemm_w_kernel<4>, ggrid, dim3(kTW), 0, st, ga);
         else if (rs == 5)
-            hipLaunchKernelGGL(gen_gemm_kernel<5>, ggrid, dim3(kT), 0, st, ga);
+            hipLaunchKernelGGL(gen_gemm_w_kernel<5>, ggrid, dim3(kTW), 0, st, ga);
         else if (rs == 6)
-            hipLaunchKernelGGL(gen_gemm_kernel<6>, ggrid, dim3(kT), 0, st, ga);
+            hipLaunchKernelGGL(gen_gemm_w_kernel<6>, ggrid, dim3(kTW), 0, st, ga);
         else
-            hipLaunchKernelGGL(gen_gemm_kernel<7>, ggrid, dim3(kT), 0, st, ga);
+            hipLaunchKernelGGL(gen_gemm_w_kernel<7>, ggrid, dim3(kTW), 0, st, ga);
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
         TokArgs ta{q.Vt, W2, q.s32, q.Tpart, L, p0, q.B, X, D, r, rs, q.nchunk};
-        hipLaunchKernelGGL(tok_gemm_kernel, dim3((unsigned)(nct * q.nchunk * gz)), dim3(kT), 0,
-                           st, ta);
+        hipLaunchKernelGGL(tok_gemm_w_kernel, dim3((unsigned)(nctw * q.nchunk * gz)), dim3(kTW),
+                           0, st, ta);
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
         hipLaunchKernelGGL(tfin_kernel, dim3((unsigned)((r * D + kT - 1) / kT), (unsigned)gz),
