@@ -57,11 +57,13 @@ def test_region_ssm_small_matches_oracle():
 
 
 @pytest.mark.parametrize("r", [16, 32, 64, 128])
-@pytest.mark.parametrize("shape", [(3, 2, 200, 192, 384), (1, 1, 64, 64, 128), (2, 2, 7, 64, 128)],
-                         ids=["ragged", "minimal", "few_tokens"])
+@pytest.mark.parametrize("shape", [(3, 2, 200, 192, 384), (1, 1, 64, 64, 128), (2, 2, 7, 64, 128),
+                                   (1, 2, 1, 128, 256)],
+                         ids=["ragged", "minimal", "few_tokens", "one_token"])
 def test_region_ssm_shapes(r, shape):
-    """Token counts off the 128-row tile (L r a multiple of 128 or not),
-    several column tiles of X and of D, a D that leaves a half column tile."""
+    """Token counts off the 128-row tile (L r a multiple of 128 or not, down
+    to a single token), several column tiles of X and of D, a D that leaves a
+    partial column tile."""
     B, K, L, D, X = shape
     wl = synth.RegionWorkload(f"ssm_B{B}_K{K}_L{L}_D{D}_X{X}_r{r}", B, K, L, D, X, r,
                               seed=31 + r)
