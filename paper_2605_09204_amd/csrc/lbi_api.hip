@@ -595,11 +595,12 @@ RegionPlan region_plan(int64_t B, int64_t K, int64_t L, int32_t D, int32_t X, in
 }
 
 // The token-mixing block adds, for G (sequence, region) pairs at a time: s16,
-// h16, Vt (bf16), s32, c32, g32, y32, wv, Tpart (fp32), after the parts above.
+// h16, Vt (bf16), s32, c32, g32, y32, wv, Tpart (fp32), S16 (bf16), after the
+// parts above.
 // G is what fits kSsmGroupBytes (at least 1, and few enough for a 1-D grid of
 // the first tangent product's tiles); the second tangent product splits each
 // pair's token tiles into nchunk chunks, at most 512 workgroups per group.
-constexpr int kSsmParts = 9;
+constexpr int kSsmParts = 10;
 constexpr size_t kSsmGroupBytes = (size_t)6 << 30;
 
 struct SsmPlan {
@@ -618,7 +619,7 @@ SsmPlan ssm_plan(int64_t B, int64_t K, int64_t L, int32_t D, int32_t X, int32_t 
     const size_t mtiles = (Lr + 127) / 128, nct = (size_t)(D + 255) / 256;
     const size_t pair = align256(LD * 2) + align256(LX * 2) + align256(Lr * X * 2) +
                         3 * align256(LD * 4) + align256(LX * 4) + align256((size_t)D * 4) +
-                        align256(mtiles * r * D * 4);
+                        align256(mtiles * r * D * 4) + align256(Lr * D * 2);
     int64_t G = (int64_t)(kSsmGroupBytes / pair);
     const int64_t BK = B * K;
     const int64_t tiles = (int64_t)(mtiles * ((size_t)(X + 255) / 256));
@@ -642,7 +643,7 @@ SsmPlan ssm_plan(int64_t B, int64_t K, int64_t L, int32_t D, int32_t X, int32_t 
     const size_t g = (size_t)G;
     const size_t n[kSsmParts] = {g * LD * 2, g * LX * 2, g * Lr * X * 2, g * LD * 4,
                                  g * LD * 4, g * LX * 4, g * LD * 4, g * D * 4,
-                                 g * nch * r * D * 4};
+                                 g * nch * r * D * 4, g * Lr * D * 2};
     size_t o = p.base.bytes;
     for (int i = 0; i < kSsmParts; ++i) {
         p.off[i] = o;
@@ -979,6 +980,7 @@ lbi_status lbi_region_jacobians_ssm(const lbi_region_params *params, const float
     q.y32 = (float *)(w + plan.off[6]);
     q.wv = (float *)(w + plan.off[7]);
     q.Tpart = (float *)(w + plan.off[8]);
+    q.S16 = (__bf16 *)(w + plan.off[9]);
     return launch_region_jacobians_ssm(q, (hipStream_t)stream) == hipSuccess ? LBI_OK
                                                                              : LBI_ERR_HIP;
 }

@@ -740,22 +740,17 @@ __device__ __forceinline__ int64_t xcd_order(int64_t i, int64_t n)
     return n % 8 == 0 ? (i % 8) * (n / 8) + i / 8 : i;
 }
 
-// ---- the first tangent product: Vt[z] = (S W1[k]^T) * silu'(u)[l][x], with
-//      S[l r + j][d] = c_l[d] Jdec^T[pair][j][d] formed as its tiles load (S is
-//      never stored).  A workgroup holds one column tile of W1 and loops over a
-//      chunk of consecutive row tiles in one pipeline over (row tile, k block);
-//      each row tile's epilogue scales and stores it while the next tile's
-//      products run.
+// ---- the first tangent product: Vt[z] = (S W1[k]^T) * silu'(u)[l][x] with
+//      S[l r + j][d] = c_l[d] Jdec^T[pair][j][d], stored first (ssm_s) so that
+//      both operands stream straight into LDS (gen_dma below) -----------------------
 struct GenArgs {
-    const __bf16 *JdT;  // [K B r][D]: the pair's rows from (p0 + z) r
-    const float *c32;   // [G][L][D]
+    const __bf16 *S;    // [G][L r][D]
     const __bf16 *W1;   // [K][X][D]
     const float *g32;   // [G][L][X]
     __bf16 *Vt;         // [G][L r][X]
     int64_t L, p0, Bn;
-    int D, X, r, rs;
-    int64_t ntn, ntm;   // column and row tiles
-    int mchunk;         // row-tile chunks per (pair, column tile)
+    int D, X, rs;
+    int ntn, ntm;       // 256-wide column tiles, 256-row tiles of a pair
 };
 
 // ---- the second tangent product: Tpart[z][c][j][d] = sum over the tokens l of
@@ -819,149 +814,196 @@ __device__ __forceinline__ void wtile_store(const u4 (&v)[WT<ROWS>::CPT], __bf16
     }
 }
 
-// ---- gen_gemm_w: the first tangent product (GenArgs above) ------------------------
-// (a thread's two A chunks are rows x + 64 i, x = tid / 8 < 64: at RS = 7 two
-// interface rows of one token, below it one row j = x mod r of two tokens)
-template <int RS>
-__global__ __launch_bounds__(kTW) void gen_gemm_w_kernel(GenArgs a)
+// ---- ssm_s: the first tangent product's left operand S (GenArgs above), rounded
+//      to bf16 as it is formed; thread e writes the 8 values of chunk e % (D / 8)
+//      of row e / (D / 8) --------------------------------------------------------------
+__global__ __launch_bounds__(kT) void ssm_s_kernel(RegionArgs q, int64_t p0)
 {
-    constexpr int NJ = RS == 7 ? 2 : 1;
-    constexpr int NT = RS == 7 ? 1 : 2;
-    __shared__ __attribute__((aligned(16))) __bf16 smem[6 * TILE];
-    // (buffers i of A, 128 x 64, and of B, 256 x 64)
-    auto sA = [&](int i) { return smem + i * TILE; };
-    auto sB = [&](int i) { return smem + (2 + 2 * i) * TILE; };
-    const int64_t lg = xcd_order(blockIdx.x, (int64_t)gridDim.x);
-    const int mc = (int)(lg % a.mchunk);
-    const int64_t nt = (lg / a.mchunk) % a.ntn, z = lg / (a.mchunk * a.ntn);
-    const int64_t per = (a.ntm + a.mchunk - 1) / a.mchunk;
-    const int64_t t0 = (int64_t)mc * per < a.ntm ? (int64_t)mc * per : a.ntm;
-    const int64_t t1 = t0 + per < a.ntm ? t0 + per : a.ntm;
-    if (t0 >= t1)
+    const int64_t z = blockIdx.y;
+    const int D = q.D, r = q.r, dq = D / 8;
+    const int64_t Lr = q.L * r;
+    const int64_t e = (int64_t)blockIdx.x * kT + threadIdx.x;
+    if (e >= Lr * dq)
         return;
-    const int64_t n0 = nt * BNW;
-    const int64_t pr = a.p0 + z, k = pr / a.Bn;
-    const int64_t M = a.L * a.r;
+    const int64_t row = e / dq, l = row / r;
+    const int c = (int)(e % dq), j = (int)(row % r);
+    const float *cp = q.c32 + (z * q.L + l) * D + c * 8;
+    const f4 c0 = *(const f4 *)cp, c1 = *(const f4 *)(cp + 4);
+    const bf16x8 jv = *(const bf16x8 *)(q.JdT + ((p0 + z) * r + j) * D + c * 8);
+    bf16x8 o;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        o[i] = (__bf16)(c0[i] * (float)jv[i]);
+        o[4 + i] = (__bf16)(c1[i] * (float)jv[4 + i]);
+    }
+    *(bf16x8 *)(q.S16 + (z * Lr + row) * D + c * 8) = o;
+}
+
+// ==== 256 x 256 tiles with operands loaded straight into LDS ===========================
+// C (256 x 256, fp32 in registers) = A rows x B rows^T over K, both bf16 with K
+// contiguous.  Eight waves (2 x 4) of 128 x 64.  Two LDS stages of 64 k
+// (32 KB per operand): the next stage's loads run while this stage's MFMAs
+// do, one barrier per stage.  buffer_load_dwordx4 ... lds writes each lane's
+// 16 bytes at M0 + 16 lane, so the operands take no registers and no VALU or
+// LDS-write instructions; the rows (128 B) sit two to a 256-byte line with
+// chunk q of row R in slot ((R & 1) 8 + q) ^ ((R / 2) & 7), the layout of
+// lds_off, and each lane loads the global chunk that its LDS slot holds.
+constexpr int kDT = 512;                  // threads
+constexpr int kDOp = 256 * BK * 2;        // bytes of one operand's stage (32 KB)
+constexpr int kDStage = 2 * kDOp;         // A and B
+constexpr int kDLoads = kDOp / 1024 / 8;  // 1 KB loads per wave, operand and stage
+
+typedef int i4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ i4 dma_rsrc(const void *base, uint32_t bytes)
+{
+    const uint64_t x = (uint64_t)(uintptr_t)base;
+    i4 v;
+    v[0] = (int)(uint32_t)x;
+    v[1] = (int)((uint32_t)(x >> 32) & 0xFFFFu);
+    v[2] = (int)bytes;
+    v[3] = kBufferWord3;
+    return v;
+}
+// 16 bytes per lane from rs at voff + soff into LDS at lds + 16 lane; M0 (the
+// LDS destination, one wait state after writing it) is saved and restored in
+// the asm
+__device__ __forceinline__ void dma_b128(uint32_t lds, i4 rs, int voff, int soff)
+{
+    uint32_t keep;
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
+                 "buffer_load_dwordx4 %2, %3, %4 offen lds\n\ts_mov_b32 m0, %0"
+                 : "=&s"(keep)
+                 : "s"(lds), "v"(voff), "s"(rs), "s"(soff)
+                 : "memory");
+}
+// all of this wave's loads but the N most recent, and its LDS operations, done;
+// then the workgroup barrier (the waits are the compiler's own, so it counts
+// them when it places its LDS waits)
+template <int N> __device__ __forceinline__ void dma_barrier()
+{
+    __builtin_amdgcn_s_waitcnt((N & 15) | (((N >> 4) & 3) << 14) | (7 << 4));
+    __builtin_amdgcn_s_barrier();
+}
+
+// acc += the tile product over K (a multiple of 64); rows of A from rsA, of B
+// from rsB (resources that end at the last valid row: the rest read zero)
+__device__ __forceinline__ void dtile_product(f4 (&acc)[8][4], i4 rsA, i4 rsB, int K, int w,
+                                              int lane, uint32_t lbase)
+{
+    typedef __attribute__((address_space(3))) char lchar;
+    const int wm = w >> 2, wn = w & 3;
+    // load d of a wave (1 KB, rows 8 d' .. 8 d' + 7 with d' = w + 8 d): lane ->
+    // line rp = 4 d' + lane / 16, row 2 rp + (lane & 15) / 8, global chunk
+    // (lane & 7) ^ (rp & 7)
+    int vo[kDLoads];
+#pragma unroll
+    for (int d = 0; d < kDLoads; ++d) {
+        const int rp = 4 * (w + 8 * d) + (lane >> 4);
+        vo[d] = (2 * rp + ((lane & 15) >> 3)) * K * 2 + (((lane & 7) ^ (rp & 7)) << 4);
+    }
+    auto issue = [&](int s) {
+        const uint32_t st = lbase + (uint32_t)((s & 1) * kDStage);
+#pragma unroll
+        for (int d = 0; d < kDLoads; ++d) {
+            const uint32_t blk = (uint32_t)((w + 8 * d) * 1024);
+            dma_b128(__builtin_amdgcn_readfirstlane(st + blk), rsA, vo[d], s * BK * 2);
+            dma_b128(__builtin_amdgcn_readfirstlane(st + kDOp + blk), rsB, vo[d], s * BK * 2);
+        }
+    };
+    // operand reads: row lane & 15 of a 16-row block, chunk 4 ks + lane / 16
+    uint32_t ro[2];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+        ro[ks] = (uint32_t)(lds_off(lane & 15, 4 * ks + (lane >> 4)) * 2);
+    const int nk = K / BK;
+    issue(0);
+    for (int t = 0; t < nk; ++t) {
+        dma_barrier<0>();  // stage t complete; stage t - 1 read by every wave
+        if (t + 1 < nk)
+            issue(t + 1);
+        const uint32_t st = lbase + (uint32_t)((t & 1) * kDStage);
+        bf16x8 a[2][8], b[2][4];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                a[ks][i] = *(const bf16x8 *)(lchar *)(uintptr_t)(st + ro[ks] +
+                                                                  (wm * 128 + i * 16) * 128);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                b[ks][j] = *(const bf16x8 *)(lchar *)(uintptr_t)(st + kDOp + ro[ks] +
+                                                                  (wn * 64 + j * 16) * 128);
+        }
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks][i], b[ks][j],
+                                                                         acc[i][j], 0, 0, 0);
+        // all operand reads first, then the MFMAs (each waits only for its own)
+        __builtin_amdgcn_sched_group_barrier(0x100, 24, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 64, 0);
+    }
+}
+
+// ---- gen_dma: the first tangent product (GenArgs above), one 256 x 256 tile of
+//      one pair per workgroup; the epilogue scales by silu'(u) and stores bf16 ---
+__global__ __launch_bounds__(kDT) __attribute__((amdgpu_waves_per_eu(2, 2))) void gen_dma_kernel(
+    GenArgs a)
+{
+    __shared__ __attribute__((aligned(1024))) char smem[2 * kDStage];  // 128 KB
+    typedef __attribute__((address_space(3))) char lchar;
+    const uint32_t lbase = (uint32_t)(uintptr_t)(lchar *)smem;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t lg = xcd_order(blockIdx.x, (int64_t)gridDim.x);
+    const int tn = (int)(lg % a.ntn);
+    const int tm = (int)((lg / a.ntn) % a.ntm);
+    const int64_t z = lg / ((int64_t)a.ntn * a.ntm);
+    const int64_t k = (a.p0 + z) / a.Bn;
+    const int64_t Lr = a.L << a.rs;
+    const int64_t row0 = (int64_t)tm * 256, col0 = (int64_t)tn * 256;
+    const int vA = Lr - row0 < 256 ? (int)(Lr - row0) : 256;
+    const int vB = a.X - col0 < 256 ? (int)(a.X - col0) : 256;
     const int D = a.D;
-    const __bf16 *W = a.W1 + k * (int64_t)a.X * D;
-    const float *gz = a.g32 + z * a.L * a.X;
-    __bf16 *out = a.Vt + z * M * a.X;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wm = w >> 2, wn = w & 3;
-    const __amdgpu_buffer_rsrc_t rsJ = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)(a.JdT + pr * a.r * D), 0, a.r * D * 2, kBufferWord3);
-    const int64_t ltile = (BM >> RS) > 0 ? (BM >> RS) : 1;
-    const int x = tid >> 3, q = tid & 7;
-    uint32_t joff[NJ], coff[NT];
+    const i4 rsA = dma_rsrc(a.S + (z * Lr + row0) * D, (uint32_t)vA * D * 2);
+    const i4 rsB = dma_rsrc(a.W1 + (k * a.X + col0) * D, (uint32_t)vB * D * 2);
+    f4 acc[8][4];
 #pragma unroll
-    for (int u = 0; u < NJ; ++u)
-        joff[u] = (uint32_t)((((x + 64 * u) & ((1 << RS) - 1)) * D + q * 8) * 2);
-#pragma unroll
-    for (int u = 0; u < NT; ++u)
-        coff[u] = (uint32_t)((((x + 64 * u) >> RS) * D + q * 8) * 4);
-    f4 acc[4][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
             acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-    const int nk = D / BK;
-    int64_t lt = t0;
-    int lkb = 0;
-    uint32_t vob[WT<256>::CPT];
-    wtile_offsets<256>(vob, D);
-    struct Raw {
-        u4 j[NJ];
-        f4 c[NT][2];
-        u4 b[WT<256>::CPT];
-    };
-    auto load = [&](Raw &v) {
-        if (lt < t1) {
-            const int k0 = lkb * BK;
-            const int64_t l0 = (lt * BM) >> RS;
-            const int64_t nl = a.L - l0 < ltile ? a.L - l0 : ltile;
-            const __amdgpu_buffer_rsrc_t rsC = __builtin_amdgcn_make_buffer_rsrc(
-                (void *)(a.c32 + (z * a.L + l0) * D), 0, (int)(nl * D * 4), kBufferWord3);
+    dtile_product(acc, rsA, rsB, D, w, lane, lbase);
+    // (a 16-row block is one token: r is a multiple of 16.)  The scale factors
+    // are all loaded before the first store, so that one wait covers them.
+    const int wm = w >> 2, wn = w & 3;
+    const float *gz = a.g32 + z * a.L * a.X;
+    __bf16 *out = a.Vt + z * Lr * a.X;
+    float gs[8][4];
 #pragma unroll
-            for (int u = 0; u < NJ; ++u)
-                v.j[u] = __builtin_bit_cast(
-                    u4, __builtin_amdgcn_raw_buffer_load_b128(rsJ, joff[u] + k0 * 2, 0, 0));
+    for (int i = 0; i < 8; ++i) {
+        const int64_t rb = row0 + wm * 128 + i * 16;
 #pragma unroll
-            for (int u = 0; u < NT; ++u) {
-                v.c[u][0] = __builtin_bit_cast(
-                    f4, __builtin_amdgcn_raw_buffer_load_b128(rsC, coff[u] + k0 * 4, 0, 0));
-                v.c[u][1] = __builtin_bit_cast(
-                    f4, __builtin_amdgcn_raw_buffer_load_b128(rsC, coff[u] + k0 * 4 + 16, 0, 0));
-            }
-            wtile_load<256>(v.b, vob, W, D, n0, a.X, k0);
+        for (int j = 0; j < 4; ++j) {
+            const int64_t col = col0 + wn * 64 + j * 16 + (lane & 15);
+            gs[i][j] = rb < Lr && col < a.X ? gz[(rb >> a.rs) * a.X + col] : 0.0f;
         }
-        if (++lkb == nk) {
-            lkb = 0;
-            ++lt;
-        }
-    };
-    auto store = [&](const Raw &v, __bf16 *la, __bf16 *lb) {
+    }
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const bf16x8 jv = __builtin_bit_cast(bf16x8, v.j[RS == 7 ? i : 0]);
-            const f4 c0 = v.c[RS == 7 ? 0 : i][0], c1 = v.c[RS == 7 ? 0 : i][1];
-            bf16x8 o;
+    for (int i = 0; i < 8; ++i) {
+        const int64_t rb = row0 + wm * 128 + i * 16;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                o[e] = (__bf16)(c0[e] * (float)jv[e]);
-                o[4 + e] = (__bf16)(c1[e] * (float)jv[4 + e]);
-            }
-            const int c = tid + kTW * i;
-            *(bf16x8 *)(la + lds_off(c >> 3, c & 7)) = o;
-        }
-        wtile_store<256>(v.b, lb);
-    };
-    Raw r0, r1;
-    load(r0);
-    store(r0, sA(0), sB(0));
-    load(r0);
-    load(r1);
-    __syncthreads();
-    int64_t t = t0;
-    int kb = 0, cur = 0;
-    auto body = [&](Raw &v) -> bool {
-        mma_bk(acc, sA(cur), sB(cur), wm, wn, lane);
-        if (kb == nk - 1) {
+        for (int j = 0; j < 4; ++j) {
+            const int64_t col = col0 + wn * 64 + j * 16 + (lane & 15);
+            if (rb < Lr && col < a.X) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int64_t rb = t * BM + wm * 64 + i * 16;
-                const int64_t l = rb >> RS;
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int64_t col = n0 + wn * 64 + j * 16 + (lane & 15);
-                    const bool ok = l < a.L && col < a.X;
-                    const float gs = ok ? gz[l * a.X + col] : 0.0f;
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        const int64_t row = rb + 4 * (lane >> 4) + v;
-                        if (ok && row < M)
-                            out[row * a.X + col] = (__bf16)(acc[i][j][v] * gs);
-                    }
-                    acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-                }
+                for (int v = 0; v < 4; ++v)
+                    out[(rb + 4 * (lane >> 4) + v) * a.X + col] = (__bf16)(acc[i][j][v] * gs[i][j]);
             }
         }
-        if (++kb == nk) {
-            kb = 0;
-            ++t;
-        }
-        if (t >= t1)
-            return false;
-        store(v, sA(cur ^ 1), sB(cur ^ 1));
-        __syncthreads();
-        cur ^= 1;
-        load(v);
-        return true;
-    };
-    for (;;) {
-        if (!body(r0))
-            break;
-        if (!body(r1))
-            break;
     }
 }
 
@@ -1283,21 +1325,15 @@ hipError_t launch_region_jacobians_ssm(const RegionArgs &q, hipStream_t st)
                            dim3(64 * kSsmChunks), 0, st, q, p0);
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
-        // Vt = (S W1[k]^T) * silu'(u)[l][x]                (L r x X, K = D), bf16
-        const int64_t ntn = (X + BNW - 1) / BNW, ntm = (Lr + BM - 1) / BM;
-        // (at most 512 workgroups: two rounds of one per CU)
-        int64_t mch = 512 / (ntn * gz);
-        mch = mch < 1 ? 1 : (mch > ntm ? ntm : mch);
-        GenArgs ga{q.JdT, q.c32, W1, q.g32, q.Vt, L, p0, q.B, D, X, r, rs, ntn, ntm, (int)mch};
-        const dim3 ggrid((unsigned)(ntn * mch * gz));
-        if (rs == 4)
-            hipLaunchKernelGGL(gen_gemm_w_kernel<4>, ggrid, dim3(kTW), 0, st, ga);
-        else if (rs == 5)
-            hipLaunchKernelGGL(gen_gemm_w_kernel<5>, ggrid, dim3(kTW), 0, st, ga);
-        else if (rs == 6)
-            hipLaunchKernelGGL(gen_gemm_w_kernel<6>, ggrid, dim3(kTW), 0, st, ga);
-        else
-            hipLaunchKernelGGL(gen_gemm_w_kernel<7>, ggrid, dim3(kTW), 0, st, ga);
+        // S = c_l Jdec^T (bf16), then Vt = (S W1[k]^T) * silu'(u)[l][x]   (L r x X, K = D)
+        hipLaunchKernelGGL(ssm_s_kernel, dim3((unsigned)((Lr * (D / 8) + kT - 1) / kT),
+                                              (unsigned)gz),
+                           dim3(kT), 0, st, q, p0);
+        if ((e = hipGetLastError()) != hipSuccess)
+            return e;
+        const int ntn = (X + 255) / 256, ntm = (int)((Lr + 255) / 256);
+        GenArgs ga{q.S16, W1, q.g32, q.Vt, L, p0, q.B, D, X, rs, ntn, ntm};
+        hipLaunchKernelGGL(gen_dma_kernel, dim3((unsigned)(ntn * ntm * gz)), dim3(kDT), 0, st, ga);
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
         TokArgs ta{q.Vt, W2, q.s32, q.Tpart, L, p0, q.B, X, D, r, rs, q.nchunk};

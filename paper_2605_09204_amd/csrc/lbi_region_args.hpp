@@ -27,13 +27,13 @@ struct RegionArgs {
     // the token-mixing block: per-channel decay [K][D]; (sequence, region)
     // pairs p = k B + b taken G at a time, each with its states s (bf16 and
     // fp32) and the constant-input states c [L][D], silu / silu' of W1 s
-    // [L][X], y = W2 silu(W1 s) [L][D], the scaled first tangent product Vt
-    // [L r][X], the partial sums of the second over nchunk token chunks
-    // [nchunk][r][D], and w [D]
+    // [L][X], y = W2 silu(W1 s) [L][D], the first tangent product's left
+    // operand S [L r][D] and its scaled result Vt [L r][X], the partial sums
+    // of the second over nchunk token chunks [nchunk][r][D], and w [D]
     const float *decay;
     int64_t G;
     int32_t nchunk;
-    __bf16 *s16, *h16, *Vt;
+    __bf16 *s16, *h16, *Vt, *S16;
     float *s32, *c32, *g32, *y32, *Tpart, *wv;
 };
 
