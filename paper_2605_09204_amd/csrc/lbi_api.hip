@@ -598,8 +598,8 @@ RegionPlan region_plan(int64_t B, int64_t K, int64_t L, int32_t D, int32_t X, in
 // h16, Vt (bf16), s32, c32, g32, y32, wv, Tpart (fp32), S16 (bf16), after the
 // parts above.
 // G is what fits kSsmGroupBytes (at least 1, and few enough for a 1-D grid of
-// the first tangent product's tiles); the second tangent product splits each
-// pair's token tiles into nchunk chunks, at most 512 workgroups per group.
+// either tangent product's 256 x 256 tiles); the second tangent product
+// writes one partial sum per 256-row tile of a pair (nchunk of them).
 constexpr int kSsmParts = 10;
 constexpr size_t kSsmGroupBytes = (size_t)6 << 30;
 
@@ -616,13 +616,14 @@ SsmPlan ssm_plan(int64_t B, int64_t K, int64_t L, int32_t D, int32_t X, int32_t 
     SsmPlan p;
     p.base = region_plan(B, K, L, D, X, r);
     const size_t LD = (size_t)L * D, LX = (size_t)L * X, Lr = (size_t)L * r;
-    const size_t mtiles = (Lr + 127) / 128, nct = (size_t)(D + 255) / 256;
+    const size_t mtiles = (Lr + 255) / 256;  // the tangent products' row tiles
     const size_t pair = align256(LD * 2) + align256(LX * 2) + align256(Lr * X * 2) +
                         3 * align256(LD * 4) + align256(LX * 4) + align256((size_t)D * 4) +
                         align256(mtiles * r * D * 4) + align256(Lr * D * 2);
     int64_t G = (int64_t)(kSsmGroupBytes / pair);
     const int64_t BK = B * K;
-    const int64_t tiles = (int64_t)(mtiles * ((size_t)(X + 255) / 256));
+    const size_t nct = (size_t)((X > D ? X : D) + 255) / 256;
+    const int64_t tiles = (int64_t)(mtiles * nct);
     if (G > BK)
         G = BK;
     if (G > 65535)
@@ -631,13 +632,8 @@ SsmPlan ssm_plan(int64_t B, int64_t K, int64_t L, int32_t D, int32_t X, int32_t 
         G = (((int64_t)1 << 31) - 1) / tiles;
     if (G < 1)
         G = 1;
-    // (at most 512 workgroups of the second product's 128 x 256 tiles: two
-    // full rounds of one per CU, no third round for a few)
-    size_t nch = 512 / ((size_t)G * nct);
-    if (nch > mtiles)
-        nch = mtiles;
-    if (nch < 1)
-        nch = 1;
+    // (the second product writes one partial sum per row tile)
+    const size_t nch = mtiles;
     p.G = G;
     p.nchunk = (int32_t)nch;
     const size_t g = (size_t)G;

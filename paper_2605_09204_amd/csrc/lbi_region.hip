@@ -754,65 +754,15 @@ struct GenArgs {
 };
 
 // ---- the second tangent product: Tpart[z][c][j][d] = sum over the tokens l of
-//      chunk c of silu(s_l)[d] (Vt[z] W2[k]^T)[l r + j][d] ----------------------------
-// One workgroup: a column tile of D and the 128-row tiles of token chunk c (a
-// tile holds 128 / r tokens, so a tile row's j is its row mod r), in one
-// pipeline over consecutive row tiles; each tile's products are weighted by
-// silu(s_l) and summed over the tiles in registers, then over the tile's
-// tokens through LDS.
+//      256-row tile c of silu(s_l)[d] (Vt[z] W2[k]^T)[l r + j][d] ------------------
 struct TokArgs {
     const __bf16 *Vt;   // [G][L r][X]
     const __bf16 *W2;   // [K][D][X]
     const float *s32;   // [G][L][D]
-    float *Tpart;       // [G][nchunk][r][D]
+    float *Tpart;       // [G][nchunk][r][D], nchunk = the 256-row tiles of L r
     int64_t L, p0, Bn;  // pair z is p0 + z, of region (p0 + z) / Bn
     int X, D, r, rs, nchunk;
 };
-
-// ==== the tile pipeline of the two tangent products ===============================
-// 128 x 256 output tiles, eight waves of 64 x 64 (2 x 4): each k step brings
-// 48 KB of operands into LDS for 4.2 MFLOP (a 128 x 128 tile: 32 KB for 2.1).
-// 96 KB of LDS: one workgroup (eight waves) per CU.
-constexpr int kTW = 512;   // threads
-constexpr int BNW = 256;   // columns of a tile
-
-// ROWS x 64 k of a row-major bf16 matrix from row0 (rows >= nrows read zero);
-// thread t takes chunks c = t + 512 i: row c / 8, chunk c % 8.
-template <int ROWS> struct WT {
-    static constexpr int CPT = ROWS * 8 / kTW;
-};
-template <int ROWS>
-__device__ __forceinline__ void wtile_offsets(uint32_t (&voff)[WT<ROWS>::CPT], int ld)
-{
-#pragma unroll
-    for (int i = 0; i < WT<ROWS>::CPT; ++i) {
-        const int c = threadIdx.x + kTW * i;
-        voff[i] = (uint32_t)(((c >> 3) * ld + (c & 7) * 8) * 2);
-    }
-}
-template <int ROWS>
-__device__ __forceinline__ void wtile_load(u4 (&v)[WT<ROWS>::CPT],
-                                           const uint32_t (&voff)[WT<ROWS>::CPT],
-                                           const __bf16 *base, int64_t ld, int64_t row0,
-                                           int64_t nrows, int k0)
-{
-    const int64_t left = nrows - row0;
-    const int valid = left < ROWS ? (int)left : ROWS;
-    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)(base + row0 * ld + k0), 0, (int)(valid * (int)ld * 2 - k0 * 2), kBufferWord3);
-#pragma unroll
-    for (int i = 0; i < WT<ROWS>::CPT; ++i)
-        v[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, voff[i], 0, 0);
-}
-template <int ROWS>
-__device__ __forceinline__ void wtile_store(const u4 (&v)[WT<ROWS>::CPT], __bf16 *s)
-{
-#pragma unroll
-    for (int i = 0; i < WT<ROWS>::CPT; ++i) {
-        const int c = threadIdx.x + kTW * i;
-        *(u4 *)(s + lds_off(c >> 3, c & 7)) = v[i];
-    }
-}
 
 // ---- ssm_s: the first tangent product's left operand S (GenArgs above), rounded
 //      to bf16 as it is formed; thread e writes the 8 values of chunk e % (D / 8)
@@ -856,11 +806,13 @@ constexpr int kDLoads = kDOp / 1024 / 8;  // 1 KB loads per wave, operand and st
 typedef int i4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ i4 dma_rsrc(const void *base, uint32_t bytes)
 {
+    // (the values are wave-uniform; the scalar registers an asm operand of
+    // class "s" needs are made explicit)
     const uint64_t x = (uint64_t)(uintptr_t)base;
     i4 v;
-    v[0] = (int)(uint32_t)x;
-    v[1] = (int)((uint32_t)(x >> 32) & 0xFFFFu);
-    v[2] = (int)bytes;
+    v[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)x);
+    v[1] = __builtin_amdgcn_readfirstlane((int)((uint32_t)(x >> 32) & 0xFFFFu));
+    v[2] = __builtin_amdgcn_readfirstlane((int)bytes);
     v[3] = kBufferWord3;
     return v;
 }
@@ -1007,129 +959,98 @@ __global__ __launch_bounds__(kDT) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     }
 }
 
-// ---- tok_gemm_w: the second tangent product (TokArgs above) -----------------------
-__global__ __launch_bounds__(kTW) void tok_gemm_w_kernel(TokArgs a)
+// ---- tok_dma: the second tangent product (TokArgs above) on 256 x 256 tiles ------
+// One workgroup: one column tile of D and one 256-row tile c of a pair (a tile
+// row's token is row / r, its j is row mod r); it writes the tile's partial
+// sum Tpart[z][c].  The product is weighted by silu(s_l) and summed over the
+// tile's tokens: first over a wave's row blocks that share j (blocks i and
+// i + NB, NB = min(r, 128) / 16), then across the tile's two row halves
+// through LDS.
+template <int RS>
+__global__ __launch_bounds__(kDT) __attribute__((amdgpu_waves_per_eu(2, 2))) void tok_dma_kernel(
+    TokArgs a)
 {
-    __shared__ __attribute__((aligned(16))) __bf16 smem[6 * TILE];
-    // (buffers i of A, 128 x 64, and of B, 256 x 64)
-    auto sA = [&](int i) { return smem + i * TILE; };
-    auto sB = [&](int i) { return smem + (2 + 2 * i) * TILE; };
-    const int64_t nct = (a.D + BNW - 1) / BNW;
+    constexpr int NB = (RS >= 7 ? 128 : (1 << RS)) / 16;
+    __shared__ __attribute__((aligned(1024))) char smem[2 * kDStage];  // 128 KB
+    typedef __attribute__((address_space(3))) char lchar;
+    const uint32_t lbase = (uint32_t)(uintptr_t)(lchar *)smem;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6), wm = w >> 2, wn = w & 3;
+    const int64_t nct = (a.D + 255) / 256;
     const int64_t lg = xcd_order(blockIdx.x, (int64_t)gridDim.x);
     const int64_t z = lg / (nct * a.nchunk);
     const int c = (int)((lg / nct) % a.nchunk);
-    const int64_t n0 = (lg % nct) * BNW;
+    const int64_t col0 = (lg % nct) * 256;
     const int64_t k = (a.p0 + z) / a.Bn;
-    const int64_t M = a.L * a.r;
-    const int64_t mtiles = (M + BM - 1) / BM;
-    const int64_t per = (mtiles + a.nchunk - 1) / a.nchunk;
-    const int64_t t0 = (int64_t)c * per < mtiles ? (int64_t)c * per : mtiles;
-    const int64_t t1 = t0 + per < mtiles ? t0 + per : mtiles;
-    const __bf16 *Av = a.Vt + z * M * a.X;
-    const __bf16 *W = a.W2 + k * (int64_t)a.D * a.X;
-    const float *sz = a.s32 + z * a.L * a.D;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wm = w >> 2, wn = w & 3;
-    f4 acc[4][4], run[4][4];
+    const int64_t Lr = a.L << RS;
+    const int64_t row0 = (int64_t)c * 256;
+    const int vA = Lr - row0 < 256 ? (int)(Lr - row0) : 256;
+    const int vB = a.D - col0 < 256 ? (int)(a.D - col0) : 256;
+    const i4 rsA = dma_rsrc(a.Vt + (z * Lr + row0) * a.X, (uint32_t)vA * a.X * 2);
+    const i4 rsB = dma_rsrc(a.W2 + (k * a.D + col0) * a.X, (uint32_t)vB * a.X * 2);
+    f4 acc[8][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    dtile_product(acc, rsA, rsB, a.X, w, lane, lbase);
+    // weights, all loaded before they are used (rows past L r and columns past
+    // D are left out by selects: their products may be anything)
+    const float *sz = a.s32 + z * a.L * a.D;
+    float wt[8][4];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int64_t l = (row0 + wm * 128 + i * 16) >> RS;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-            run[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+            const int64_t col = col0 + wn * 64 + j * 16 + (lane & 15);
+            wt[i][j] = l < a.L && col < a.D ? silu(sz[l * a.D + col]) : 0.0f;
         }
-    if (t0 < t1) {
-        const int nk = a.X / BK;
-        int64_t lt = t0;
-        int lkb = 0;
-        uint32_t voa[WT<128>::CPT], vob[WT<256>::CPT];
-        wtile_offsets<128>(voa, a.X);
-        wtile_offsets<256>(vob, a.X);
-        struct Raw {
-            u4 a[WT<128>::CPT];
-            u4 b[WT<256>::CPT];
-        };
-        auto load = [&](Raw &v) {
-            if (lt < t1) {
-                wtile_load<128>(v.a, voa, Av, a.X, lt * BM, M, lkb * BK);
-                wtile_load<256>(v.b, vob, W, a.X, n0, a.D, lkb * BK);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const bool live = (row0 + wm * 128 + i * 16) < Lr;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const float x = live ? wt[i][j] * acc[i][j][v] : 0.0f;
+                if (i < NB)
+                    acc[i][j][v] = x;
+                else
+                    acc[i % NB][j][v] += x;
             }
-            if (++lkb == nk) {
-                lkb = 0;
-                ++lt;
-            }
-        };
-        Raw r0, r1;
-        load(r0);
-        wtile_store<128>(r0.a, sA(0));
-        wtile_store<256>(r0.b, sB(0));
-        load(r0);
-        load(r1);
-        __syncthreads();
-        int64_t t = t0;
-        int kb = 0, cur = 0;
-        auto body = [&](Raw &v) -> bool {
-            mma_bk(acc, sA(cur), sB(cur), wm, wn, lane);
-            if (kb == nk - 1) {
+    }
+    // the lower row half adds the upper one's sums through LDS ([j][256] fp32)
+    __syncthreads();  // (every wave is past its operand reads)
+    float *red = (float *)smem;
+    if (wm == 1) {
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int64_t l = (t * BM + wm * 64 + i * 16) >> a.rs;
+        for (int i = 0; i < NB; ++i)
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const int64_t col = n0 + wn * 64 + j * 16 + (lane & 15);
-                        const float wt = l < a.L && col < a.D ? silu(sz[l * a.D + col]) : 0.0f;
+            for (int j = 0; j < 4; ++j)
 #pragma unroll
-                        for (int v = 0; v < 4; ++v)
-                            run[i][j][v] = fmaf(wt, acc[i][j][v], run[i][j][v]);
-                        acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+                for (int v = 0; v < 4; ++v)
+                    red[(i * 16 + 4 * (lane >> 4) + v) * 256 + wn * 64 + j * 16 + (lane & 15)] =
+                        acc[i][j][v];
+    }
+    __syncthreads();
+    if (wm == 0) {
+        float *out = a.Tpart + (z * a.nchunk + c) * ((int64_t)a.D << RS);
+#pragma unroll
+        for (int i = 0; i < NB; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int cl = wn * 64 + j * 16 + (lane & 15);
+                if (col0 + cl < a.D) {
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const int jr = i * 16 + 4 * (lane >> 4) + v;
+                        out[(int64_t)jr * a.D + col0 + cl] = acc[i][j][v] + red[jr * 256 + cl];
                     }
                 }
             }
-            if (++kb == nk) {
-                kb = 0;
-                ++t;
-            }
-            if (t >= t1)
-                return false;
-            wtile_store<128>(v.a, sA(cur ^ 1));
-            wtile_store<256>(v.b, sB(cur ^ 1));
-            __syncthreads();
-            cur ^= 1;
-            load(v);
-            return true;
-        };
-        for (;;) {
-            if (!body(r0))
-                break;
-            if (!body(r1))
-                break;
-        }
-    }
-    // the 128 / r tokens of a tile, 128 columns at a time through LDS
-    float *red = (float *)smem;  // [128][128]
-    const int nq = 128 >> a.rs;
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-        __syncthreads();
-        if ((wn >> 1) == h) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-#pragma unroll
-                    for (int v = 0; v < 4; ++v)
-                        red[(wm * 64 + i * 16 + 4 * (lane >> 4) + v) * 128 + (wn & 1) * 64 +
-                            j * 16 + (lane & 15)] = run[i][j][v];
-        }
-        __syncthreads();
-        for (int idx = tid; idx < a.r * 128; idx += kTW) {
-            const int jr = idx >> 7, cl = idx & 127;
-            float sum = 0.0f;
-            for (int u = 0; u < nq; ++u)
-                sum += red[((u << a.rs) + jr) * 128 + cl];
-            const int64_t col = n0 + h * 128 + cl;
-            if (col < a.D)
-                a.Tpart[((z * a.nchunk + c) * a.r + jr) * (int64_t)a.D + col] = sum;
-        }
     }
 }
 
@@ -1304,7 +1225,7 @@ hipError_t launch_region_jacobians_ssm(const RegionArgs &q, hipStream_t st)
 
     // the token-mixing block, G (sequence, region) pairs at a time
     const int64_t Lr = L * r;
-    const int nctw = (D + BNW - 1) / BNW;
+    const int nctw = (D + 255) / 256;
     for (int64_t p0 = 0; p0 < BKn; p0 += q.G) {
         const int64_t gz = q.G < BKn - p0 ? q.G : BKn - p0;
         hipLaunchKernelGGL(ssm_fwd_kernel, dim3((unsigned)(D / 64), (unsigned)gz),
@@ -1337,8 +1258,15 @@ hipError_t launch_region_jacobians_ssm(const RegionArgs &q, hipStream_t st)
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
         TokArgs ta{q.Vt, W2, q.s32, q.Tpart, L, p0, q.B, X, D, r, rs, q.nchunk};
-        hipLaunchKernelGGL(tok_gemm_w_kernel, dim3((unsigned)(nctw * q.nchunk * gz)), dim3(kTW),
-                           0, st, ta);
+        const dim3 tgrid((unsigned)(nctw * q.nchunk * gz));
+        if (rs == 4)
+            hipLaunchKernelGGL(tok_dma_kernel<4>, tgrid, dim3(kDT), 0, st, ta);
+        else if (rs == 5)
+            hipLaunchKernelGGL(tok_dma_kernel<5>, tgrid, dim3(kDT), 0, st, ta);
+        else if (rs == 6)
+            hipLaunchKernelGGL(tok_dma_kernel<6>, tgrid, dim3(kDT), 0, st, ta);
+        else
+            hipLaunchKernelGGL(tok_dma_kernel<7>, tgrid, dim3(kDT), 0, st, ta);
         if ((e = hipGetLastError()) != hipSuccess)
             return e;
         hipLaunchKernelGGL(tfin_kernel, dim3((unsigned)((r * D + kT - 1) / kT), (unsigned)gz),
