@@ -37,7 +37,7 @@
 //   p1          per (b, k): P1 = (diag(silu'(a)) W_d1)^T
 //   bmv         cvec = W1 d
 //   xpart/xfin  per b: mean_l x_embed (two-stage)
-//   region_gemm per (k, b, 128 columns of X): the token product and its reductions
+//   region_dma  per (k, b, 128 columns of X): the token product and its reductions
 //   bmv x3      p = mean x_embed + d + W2 sbar; e -> silu(e), silu'(e); Enc_k
 //   ln_fwd      per (b, k): z = m + alpha Enc, LayerNorm -> m_{k+1}, zhat, 1/sigma
 //   gemm_nt x5  per k: Jdec^T, U'^T = (W1 Jdec)^T scaled by gbar, dp^T, T'^T, Jenc^T
@@ -122,6 +122,41 @@ __device__ __forceinline__ void tile_store(const u4 (&v)[4], __bf16 *s)
         const int c = threadIdx.x + kT * i;
         *(u4 *)(s + lds_off(c >> 3, c & 7)) = v[i];
     }
+}
+
+// ---- operands loaded straight into LDS ---------------------------------------------
+typedef int i4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ i4 dma_rsrc(const void *base, uint32_t bytes)
+{
+    // (the values are wave-uniform; the scalar registers an asm operand of
+    // class "s" needs are made explicit)
+    const uint64_t x = (uint64_t)(uintptr_t)base;
+    i4 v;
+    v[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)x);
+    v[1] = __builtin_amdgcn_readfirstlane((int)((uint32_t)(x >> 32) & 0xFFFFu));
+    v[2] = __builtin_amdgcn_readfirstlane((int)bytes);
+    v[3] = kBufferWord3;
+    return v;
+}
+// 16 bytes per lane from rs at voff + soff into LDS at lds + 16 lane; M0 (the
+// LDS destination, one wait state after writing it) is saved and restored in
+// the asm
+__device__ __forceinline__ void dma_b128(uint32_t lds, i4 rs, int voff, int soff)
+{
+    uint32_t keep;
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
+                 "buffer_load_dwordx4 %2, %3, %4 offen lds\n\ts_mov_b32 m0, %0"
+                 : "=&s"(keep)
+                 : "s"(lds), "v"(voff), "s"(rs), "s"(soff)
+                 : "memory");
+}
+// all of this wave's loads but the N most recent, and its LDS operations, done;
+// then the workgroup barrier (the waits are the compiler's own, so it counts
+// them when it places its LDS waits)
+template <int N> __device__ __forceinline__ void dma_barrier()
+{
+    __builtin_amdgcn_s_waitcnt((N & 15) | (((N >> 4) & 3) << 14) | (7 << 4));
+    __builtin_amdgcn_s_barrier();
 }
 
 // acc += A_tile(128 x 64) B_tile(128 x 64)^T for this wave's 64 x 64 quarter
@@ -312,19 +347,25 @@ __global__ __launch_bounds__(kT) void xfin_kernel(RegionArgs q)
     q.xbar[b * q.D + c] = s / (float)q.L;
 }
 
-// ---- region_gemm: sbar, gbar for 128 columns of X, one sequence and region ----
+// ---- region_dma: sbar, gbar for 128 columns of X, one sequence and region -----
 // H = x_embed[b] W1[k]^T + 1 cvec[b, k]^T (cvec = W1 d) over all L tokens in
 // 128-row tiles; the epilogue of each tile adds silu(H) and silu'(H) of its
-// valid rows into per-lane column sums.
-__global__ __launch_bounds__(kT) void region_gemm_kernel(RegionArgs q)
+// valid rows into per-lane column sums.  Both operands load straight into LDS
+// (buffer_load_dwordx4 ... lds, the row layout of lds_off): 128 x 128 tiles,
+// four waves of 64 x 64, two 64-deep stages (64 KB, two workgroups per CU), one
+// pipeline over (row tile, k block), so that a tile's epilogue runs while the
+// next tile's first stage loads.
+__global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(2, 2))) void region_dma_kernel(
+    RegionArgs q)
 {
-    __shared__ __attribute__((aligned(16))) __bf16 sA[2][TILE];
-    __shared__ __attribute__((aligned(16))) __bf16 sB[2][TILE];
+    constexpr int OP = BM * BK * 2;   // bytes of one operand's stage (16 KB)
+    constexpr int STG = 2 * OP;
+    constexpr int NL = OP / 1024 / 4; // 1 KB loads per wave, operand and stage
+    __shared__ __attribute__((aligned(1024))) char smem[2 * STG];
     __shared__ float sred[2][2][BN];
+    typedef __attribute__((address_space(3))) char lchar;
+    const uint32_t lbase = (uint32_t)(uintptr_t)(lchar *)smem;
     const int nxt = q.X / BN;
-    // workgroups that share W1[k]'s column tile (all b) run on one XCD: the
-    // scheduler deals workgroup i to XCD i % 8, so consecutive logical indices
-    // are gathered from every eighth workgroup
     const int64_t G = (int64_t)gridDim.x;
     int64_t lg = blockIdx.x;
     if (G % 8 == 0)
@@ -333,18 +374,44 @@ __global__ __launch_bounds__(kT) void region_gemm_kernel(RegionArgs q)
     const int64_t xt = (lg / q.B) % nxt;
     const int64_t k = lg / (q.B * nxt);
     const int D = q.D;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, wm = w >> 1, wn = w & 1;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6), wm = w >> 1, wn = w & 1;
     const int64_t bk = b * q.K + k;
     const __bf16 *Xe = (const __bf16 *)q.x_embed + b * q.L * D;
-    const __bf16 *W = (const __bf16 *)q.W1 + (k * q.X + xt * BN) * (int64_t)D;
-    // this lane's four columns of W1 d
+    const i4 rsB = dma_rsrc((const __bf16 *)q.W1 + (k * q.X + xt * BN) * (int64_t)D,
+                            (uint32_t)BN * D * 2);
     float cv[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
         cv[j] = q.cvec[bk * q.X + xt * BN + wn * 64 + j * 16 + (lane & 15)];
-
     const int nk = D / BK;
     const int ntile = (int)((q.L + BM - 1) / BM);
+    const int nstep = ntile * nk;
+    // load d of a wave: rows 8 d' .. 8 d' + 7 (d' = w + 4 d) of a tile, lane ->
+    // line rp = 4 d' + lane / 16, row 2 rp + (lane & 15) / 8, chunk (lane & 7) ^ (rp & 7)
+    int vo[NL];
+#pragma unroll
+    for (int d = 0; d < NL; ++d) {
+        const int rp = 4 * (w + 4 * d) + (lane >> 4);
+        vo[d] = (2 * rp + ((lane & 15) >> 3)) * D * 2 + (((lane & 7) ^ (rp & 7)) << 4);
+    }
+    auto issue = [&](int s) {
+        const int t = s / nk, kb = s - t * nk;
+        const int64_t row0 = (int64_t)t * BM;
+        const int vA = q.L - row0 < BM ? (int)(q.L - row0) : BM;
+        const i4 rsA = dma_rsrc(Xe + row0 * D, (uint32_t)vA * D * 2);
+        const uint32_t st = lbase + (uint32_t)((s & 1) * STG);
+#pragma unroll
+        for (int d = 0; d < NL; ++d) {
+            const uint32_t blk = (uint32_t)((w + 4 * d) * 1024);
+            dma_b128(__builtin_amdgcn_readfirstlane(st + blk), rsA, vo[d], kb * BK * 2);
+            dma_b128(__builtin_amdgcn_readfirstlane(st + OP + blk), rsB, vo[d], kb * BK * 2);
+        }
+    };
+    uint32_t ro[2];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+        ro[ks] = (uint32_t)(lds_off(lane & 15, 4 * ks + (lane >> 4)) * 2);
     // column sums of s = sigmoid(h), silu(h) = h s and silu(h) s
     float s1[4] = {0.0f, 0.0f, 0.0f, 0.0f}, s2[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     float s3[4] = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -354,55 +421,52 @@ __global__ __launch_bounds__(kT) void region_gemm_kernel(RegionArgs q)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
             acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-    // Loads run three stages ahead of the products (stage = one 64-wide k
-    // block of one row tile), rotating through three register sets: a fifth
-    // of the loads miss L2 and come from the last-level cache or HBM.
-    int lt = 0, lkb = 0;  // next stage to load
-    uint32_t voff[4];
-    tile_offsets(voff, D);
-    auto load = [&](u4 (&va)[4], u4 (&vb)[4]) {
-        if (lt < ntile) {
-            tile_load(va, voff, Xe, D, (int64_t)lt * BM, q.L, lkb * BK);
-            tile_load(vb, voff, W, D, 0, BN, lkb * BK);
-        }
-        if (++lkb == nk) {
-            lkb = 0;
-            ++lt;
-        }
-    };
-    u4 ra0[4], rb0[4], ra1[4], rb1[4], ra2[4], rb2[4];
-    load(ra0, rb0);
-    tile_store(ra0, sA[0]);
-    tile_store(rb0, sB[0]);
-    load(ra0, rb0);
-    load(ra1, rb1);
-    load(ra2, rb2);
-    __syncthreads();
-    int t = 0, kb = 0, cur = 0;  // the stage being multiplied
-    // one stage: products from LDS[cur]; the row tile's epilogue after its
-    // last k block; then the next stage (held in va, vb) into LDS[cur ^ 1] and
-    // the stage three ahead into va, vb
-    auto body = [&](u4 (&va)[4], u4 (&vb)[4]) -> bool {
-        mma_bk(acc, sA[cur], sB[cur], wm, wn, lane);
-        if (kb == nk - 1) {
-            // epilogue of row tile t over its valid rows: with s = sigmoid(h),
-            // silu = h s and silu' = s + silu - silu s, so the sums of s, silu
-            // and silu s carry both reductions
+    issue(0);
+    for (int s = 0; s < nstep; ++s) {
+        dma_barrier<0>();  // stage s complete; stage s - 1 read by every wave
+        if (s + 1 < nstep)
+            issue(s + 1);
+        const uint32_t st = lbase + (uint32_t)((s & 1) * STG);
+        bf16x8 a[2][4], bb[2][4];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                a[ks][i] = *(const bf16x8 *)(lchar *)(uintptr_t)(st + ro[ks] +
+                                                                  (wm * 64 + i * 16) * 128);
+                bb[ks][i] = *(const bf16x8 *)(lchar *)(uintptr_t)(st + OP + ro[ks] +
+                                                                   (wn * 64 + i * 16) * 128);
+            }
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[ks][i], bb[ks][j],
+                                                                         acc[i][j], 0, 0, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 32, 0);
+        const int t = s / nk;
+        if (s - t * nk == nk - 1) {
+            // epilogue of row tile t over its valid rows (selects: rows past L
+            // may hold anything); with s = sigmoid(h), silu = h s and
+            // silu' = s + silu - silu s, the sums of s, silu and silu s carry
+            // both reductions
             const int64_t rbase = (int64_t)t * BM + wm * 64 + 4 * (lane >> 4);
-            const bool full = (int64_t)(t + 1) * BM <= q.L;
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
-                    const float w8 = full || rbase + i * 16 + v < q.L ? 1.0f : 0.0f;
+                    const bool ok = rbase + i * 16 + v < q.L;
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
                         const float h = acc[i][j][v] + cv[j];
-                        const float sg = w8 * sigm(h);
+                        const float sg = sigm(h);
                         const float sl = h * sg;
-                        s1[j] += sg;
-                        s2[j] += sl;
-                        s3[j] = fmaf(sl, sg, s3[j]);
+                        s1[j] += ok ? sg : 0.0f;
+                        s2[j] += ok ? sl : 0.0f;
+                        s3[j] += ok ? sl * sg : 0.0f;
                     }
                 }
 #pragma unroll
@@ -411,26 +475,6 @@ __global__ __launch_bounds__(kT) void region_gemm_kernel(RegionArgs q)
                 for (int j = 0; j < 4; ++j)
                     acc[i][j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
         }
-        if (++kb == nk) {
-            kb = 0;
-            ++t;
-        }
-        if (t >= ntile)
-            return false;
-        tile_store(va, sA[cur ^ 1]);
-        tile_store(vb, sB[cur ^ 1]);
-        __syncthreads();
-        cur ^= 1;
-        load(va, vb);
-        return true;
-    };
-    for (;;) {
-        if (!body(ra0, rb0))
-            break;
-        if (!body(ra1, rb1))
-            break;
-        if (!body(ra2, rb2))
-            break;
     }
     // lanes l, l ^ 16, l ^ 32, l ^ 48 hold the same columns; then the two
     // waves of a column half through LDS
@@ -803,40 +847,6 @@ constexpr int kDOp = 256 * BK * 2;        // bytes of one operand's stage (32 KB
 constexpr int kDStage = 2 * kDOp;         // A and B
 constexpr int kDLoads = kDOp / 1024 / 8;  // 1 KB loads per wave, operand and stage
 
-typedef int i4 __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ i4 dma_rsrc(const void *base, uint32_t bytes)
-{
-    // (the values are wave-uniform; the scalar registers an asm operand of
-    // class "s" needs are made explicit)
-    const uint64_t x = (uint64_t)(uintptr_t)base;
-    i4 v;
-    v[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)x);
-    v[1] = __builtin_amdgcn_readfirstlane((int)((uint32_t)(x >> 32) & 0xFFFFu));
-    v[2] = __builtin_amdgcn_readfirstlane((int)bytes);
-    v[3] = kBufferWord3;
-    return v;
-}
-// 16 bytes per lane from rs at voff + soff into LDS at lds + 16 lane; M0 (the
-// LDS destination, one wait state after writing it) is saved and restored in
-// the asm
-__device__ __forceinline__ void dma_b128(uint32_t lds, i4 rs, int voff, int soff)
-{
-    uint32_t keep;
-    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\t"
-                 "buffer_load_dwordx4 %2, %3, %4 offen lds\n\ts_mov_b32 m0, %0"
-                 : "=&s"(keep)
-                 : "s"(lds), "v"(voff), "s"(rs), "s"(soff)
-                 : "memory");
-}
-// all of this wave's loads but the N most recent, and its LDS operations, done;
-// then the workgroup barrier (the waits are the compiler's own, so it counts
-// them when it places its LDS waits)
-template <int N> __device__ __forceinline__ void dma_barrier()
-{
-    __builtin_amdgcn_s_waitcnt((N & 15) | (((N >> 4) & 3) << 14) | (7 << 4));
-    __builtin_amdgcn_s_barrier();
-}
-
 // acc += the tile product over K (a multiple of 64); rows of A from rsA, of B
 // from rsB (resources that end at the last valid row: the rest read zero)
 __device__ __forceinline__ void dtile_product(f4 (&acc)[8][4], i4 rsA, i4 rsB, int K, int w,
@@ -1121,7 +1131,7 @@ hipError_t launch_region_jacobians(const RegionArgs &q, hipStream_t st)
                        0, st, q);
     if ((e = hipGetLastError()) != hipSuccess)
         return e;
-    hipLaunchKernelGGL(region_gemm_kernel, dim3((unsigned)(K * q.B * (X / BN))), dim3(kT), 0, st,
+    hipLaunchKernelGGL(region_dma_kernel, dim3((unsigned)(K * q.B * (X / BN))), dim3(kT), 0, st,
                        q);
     if ((e = hipGetLastError()) != hipSuccess)
         return e;
