@@ -1073,9 +1073,20 @@ __global__ __launch_bounds__(kT) void tfin_kernel(RegionArgs q, int64_t p0)
     if (idx >= r * D)
         return;
     const int j = idx / D, dch = idx % D;
-    float t = 0.0f;
-    for (int c = 0; c < q.nchunk; ++c)
-        t += q.Tpart[((z * q.nchunk + c) * r + j) * (int64_t)D + dch];
+    // four running sums over the row tiles' partials, so that four loads are
+    // in flight at a time
+    const float *tp = q.Tpart + (z * q.nchunk * r + j) * (int64_t)D + dch;
+    const int64_t stride = (int64_t)r * D;
+    float t4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    int c = 0;
+    for (; c + 4 <= q.nchunk; c += 4) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            t4[u] += tp[(c + u) * stride];
+    }
+    for (; c < q.nchunk; ++c)
+        t4[0] += tp[c * stride];
+    const float t = (t4[0] + t4[1]) + (t4[2] + t4[3]);
     const int64_t o = (pr * r + j) * D + dch;
     q.dpT[o] = (__bf16)((float)q.JdT[o] * (1.0f + q.wv[z * D + dch]) + t / (float)q.L);
 }
