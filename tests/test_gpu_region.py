@@ -58,11 +58,13 @@ def test_region_small_matches_oracle():
 
 
 @pytest.mark.parametrize("r", [16, 32, 64, 128])
-@pytest.mark.parametrize("shape", [(3, 2, 200, 192, 384), (1, 1, 64, 64, 128)],
-                         ids=["ragged", "minimal"])
+@pytest.mark.parametrize("shape", [(3, 2, 200, 192, 384), (1, 1, 64, 64, 128), (2, 2, 7, 64, 128),
+                                   (1, 2, 1, 128, 256)],
+                         ids=["ragged", "minimal", "few_tokens", "one_token"])
 def test_region_shapes(r, shape):
-    """Token counts off the 128-row tile, several column tiles of X, three
-    64-wide k blocks, B r off the 128-row tile."""
+    """Token counts off the 128-row tile (down to a single token, whose tile
+    is all rows past L but one), several column tiles of X, three 64-wide k
+    blocks, B r off the 128-row tile."""
     B, K, L, D, X = shape
     wl = synth.RegionWorkload(f"region_B{B}_K{K}_L{L}_D{D}_X{X}_r{r}", B, K, L, D, X, r,
                               seed=11 + r)
