@@ -145,3 +145,32 @@ def test_region_paper_config_sampled_columns(phi):
     _say(f"[region {phi}] paper configuration, 16 pairs x 2 columns: J rel err {err:.3g}, "
          f"m_next rel err {merr:.3g}")
     assert err <= TOL and merr <= TOL
+
+
+@pytest.mark.parametrize("phi", ["ssm", "mlp"])
+def test_region_largest_widths_sampled_columns(phi):
+    """D and X at the largest sizes the entry points accept (2048, 8192), so
+    that every 32-bit offset of the tile kernels reaches its largest value;
+    two regions, three columns of J each and m_next against the oracle's
+    forward-mode columns."""
+    wl = synth.RegionWorkload(f"region_wide_{phi}", 1, 2, 40, 2048, 8192, 64, seed=53)
+    _say(f"[region {phi}] D = 2048, X = 8192, GPU call")
+    x = synth.generate_region(wl)
+    g = x.to(DEV)
+    call = binding.lbi_region_jacobians_ssm if phi == "ssm" else binding.lbi_region_jacobians
+    A, mn = call(g.params, g.x_embed, g.m)
+    torch.cuda.synchronize()
+    A = A.cpu().numpy().astype(np.float64)
+    mn = mn.cpu().numpy().astype(np.float64)
+    assert np.isfinite(A).all()
+    got, want, mg, mw = [], [], [], []
+    for k, cols in ((0, [0, 31, 63]), (1, [5, 40, 62])):
+        c, m_ref = oracle.region_jacobian_columns(x.params, x.x_embed, x.m, 0, k, cols, phi=phi)
+        got.append(A[0, k][cols])
+        want.append(c)
+        mg.append(mn[0, k])
+        mw.append(m_ref)
+    err = oracle.rel_frobenius(np.stack(got), np.stack(want))
+    merr = oracle.rel_frobenius(np.stack(mg), np.stack(mw))
+    _say(f"[region {phi}] D = 2048, X = 8192: J rel err {err:.3g}, m_next rel err {merr:.3g}")
+    assert err <= TOL and merr <= TOL
