@@ -848,7 +848,8 @@ constexpr int kDStage = 2 * kDOp;         // A and B
 constexpr int kDLoads = kDOp / 1024 / 8;  // 1 KB loads per wave, operand and stage
 
 // acc += the tile product over K (a multiple of 64); rows of A from rsA, of B
-// from rsB (resources that end at the last valid row: the rest read zero)
+// from rsB (resources that end at the last valid row, so no load leaves them;
+// the callers do not rely on what the products of rows past it hold)
 __device__ __forceinline__ void dtile_product(f4 (&acc)[8][4], i4 rsA, i4 rsB, int K, int w,
                                               int lane, uint32_t lbase)
 {
