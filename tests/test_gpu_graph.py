@@ -8,7 +8,7 @@ replay is checked against the eager results bit for bit (the kernels are
 deterministic), with the outputs poisoned and other eager library work run
 between the replays.  The cases cover every scan algorithm's launch
 sequence (one launch, the two-level scan's three, the tree scan's levels),
-the LDS-ring kernel, the allocation-free entry point and Phase 1.
+the LDS-ring kernel, the allocation-free entry point and both Phase 1 blocks.
 """
 import sys
 
@@ -101,11 +101,18 @@ def test_scan_calls_replay_in_a_graph():
     assert e <= 1e-5
 
 
-def test_region_jacobians_replay_in_a_graph():
+@pytest.mark.parametrize("phi", ["ssm", "mlp"])
+def test_region_jacobians_replay_in_a_graph(phi):
     x = synth.generate_region(synth.REGION_WORKLOADS["region_small"]).to(DEV)
     wl = x.workload
-    A_e, m_e = binding.lbi_region_jacobians_ssm(x.params, x.x_embed, x.m)
-    need = binding.lbi_region_jacobians_ssm_workspace_bytes(wl.B, wl.K, wl.L, wl.D, wl.X, wl.r)
+    if phi == "ssm":
+        call = binding.lbi_region_jacobians_ssm
+        need = binding.lbi_region_jacobians_ssm_workspace_bytes(wl.B, wl.K, wl.L, wl.D, wl.X,
+                                                                wl.r)
+    else:
+        call = binding.lbi_region_jacobians
+        need = binding.lbi_region_jacobians_workspace_bytes(wl.B, wl.K, wl.L, wl.D, wl.X, wl.r)
+    A_e, m_e = call(x.params, x.x_embed, x.m)
     ws = torch.empty((need,), dtype=torch.uint8, device=DEV)
     A_g = torch.empty_like(A_e)
     m_g = torch.empty_like(m_e)
@@ -115,8 +122,7 @@ def test_region_jacobians_replay_in_a_graph():
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
         with torch.cuda.graph(g):
-            binding.lbi_region_jacobians_ssm(x.params, x.x_embed, x.m, A=A_g, m_next=m_g,
-                                             workspace=ws)
+            call(x.params, x.x_embed, x.m, A=A_g, m_next=m_g, workspace=ws)
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
     for rep in range(3):
@@ -127,4 +133,4 @@ def test_region_jacobians_replay_in_a_graph():
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(A_g, A_e) and torch.equal(m_g, m_e), f"replay {rep}"
-    _say("[graph] token-mixing Phase 1: 3 replays equal to the eager call")
+    _say(f"[graph] Phase 1 ({phi}): 3 replays equal to the eager call")
