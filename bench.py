@@ -655,6 +655,8 @@ def main(argv=None) -> int:
                    "alg_hbm_gbs": o2["extra"]["alg_hbm_gbs"],
                    "work_inflation_vs_sequential":
                        o2["extra"]["work_inflation_vs_sequential"]}
+            if "graph_replay" in o2["extra"]:
+                rec["graph_replay"] = o2["extra"]["graph_replay"]
             if not args.no_cpu_baseline:
                 print(f"[bench] timing the CPU oracle baseline on {name}", file=sys.stderr,
                       flush=True)
