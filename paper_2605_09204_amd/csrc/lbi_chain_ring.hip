@@ -124,10 +124,9 @@ __device__ __forceinline__ void dma_b32(uint32_t lds, i4 rs, int voff, int soff)
 
 // The slot barrier: this wave's own memory operations except the N most
 // recent, and all of its LDS operations, are complete; then s_barrier.  Both
-// are the compiler's own builtins, so its tracking of LDS waits sees them and
-// places no waits of its own on reads issued before the barrier (with the
-// same instructions in an asm statement it did, and the compact-storage call
-// on mixed widths took 6% longer).
+// are the compiler's own builtins, so that its tracking of LDS waits sees
+// them (the same instructions in an asm statement gave a different schedule
+// of the slot, 6% slower on mixed widths in compact storage).
 template <int N> __device__ __forceinline__ void ring_barrier()
 {
     __builtin_amdgcn_s_waitcnt((N & 15) | (((N >> 4) & 3) << 14) | (7 << 4));
